@@ -1,0 +1,52 @@
+"""Bifurcated attention evaluated as the paper writes it -- TEST INFRASTRUCTURE ONLY.
+
+numpy fp64, following Section 4.2 step by step (notation ``b g p n k``,
+``n = 1`` for incremental decoding, ``k`` = head dimension):
+
+1. Eq. 3, context logits: einsum(bgpnk, g m_c k -> bgpn m_c); the context
+   cache has no ``b`` axis because it is shared by all samples.
+2. Eq. 3, decode logits: einsum(bgpnk, b g m_d k -> bgpn m_d).
+3. Concatenate along the key axis and take one softmax over both parts
+   (the paper leaves the softmax out of its listing; the scaled,
+   max-subtracted softmax is the standard one). Decode positions at or beyond
+   a sample's valid length get weight 0.
+4. Eq. 4: split the weights at ``m_c`` and sum
+   einsum(bgpn m_c, g m_c k -> bgpnk) + einsum(bgpn m_d, b g m_d k -> bgpnk).
+
+This module shares no code with ``oracle.c``; the two agree only because the
+bifurcated method is exact (Appendix E.1).
+"""
+from __future__ import annotations
+
+import numpy as np
+
+from . import default_scale, widen_bf16
+
+
+def bifurcated_attention(q, Kc, Vc, Kd, Vd, lens, scale=None):
+    qf = widen_bf16(q)
+    Kcf, Vcf = widen_bf16(Kc), widen_bf16(Vc)
+    Kdf, Vdf = widen_bf16(Kd), widen_bf16(Vd)
+    lens = np.asarray(lens, dtype=np.int64)
+    b, h, k = qf.shape
+    g, m_c, _ = Kcf.shape
+    m_d = Kdf.shape[2]
+    p = h // g
+    if scale is None:
+        scale = default_scale(k)
+    valid = np.arange(m_d)[None, :] < lens[:, None]                   # [b, m_d]
+    # Rows past a sample's length take no part: zero them so that whatever
+    # they hold (NaN included) cannot reach the sums.
+    Kdf = np.where(valid[:, None, :, None], Kdf, 0.0)
+    Vdf = np.where(valid[:, None, :, None], Vdf, 0.0)
+    q5 = qf.reshape(b, g, p, 1, k)                                    # bgpnk, n = 1
+    logits_c = np.einsum("bgpnk,gmk->bgpnm", q5, Kcf)                 # Eq. 3, context part
+    logits_d = np.einsum("bgpnk,bgmk->bgpnm", q5, Kdf)                # Eq. 3, decode part
+    logits = np.concatenate([logits_c, logits_d], axis=-1) * scale
+    logits[..., m_c:] = np.where(valid[:, None, None, None, :], logits[..., m_c:], -np.inf)
+    mu = logits.max(axis=-1, keepdims=True)
+    w = np.exp(logits - mu)
+    w /= w.sum(axis=-1, keepdims=True)
+    o = np.einsum("bgpnm,gmk->bgpnk", w[..., :m_c], Vcf) \
+        + np.einsum("bgpnm,bgmk->bgpnk", w[..., m_c:], Vdf)           # Eq. 4
+    return o.reshape(b, h, k)

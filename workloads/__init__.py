@@ -1,0 +1,139 @@
+"""Seeded synthetic inputs for bifurcated decode attention.
+
+This module is the only code shared by the HIP path's callers (tests, bench,
+smoke) and the oracle's callers. It draws random numbers and rounds them to
+bf16 bit patterns; it contains none of the attention arithmetic.
+
+Shapes follow the paper's statement of the problem (Section 3.1 notation,
+Section 4.1-4.2): ``b`` samples sharing one context of length ``m_c``, ``h``
+query heads in ``g`` KV groups (``p = h/g`` heads per group, group-major:
+head ``j`` belongs to group ``j // p``), head dimension ``d`` (the paper's
+``k``), and per-sample decode lengths ``len_i <= m_d_max``.
+
+Layouts (row-major, bf16 stored as uint16 bit patterns):
+    q       [b, h, d]
+    Kc, Vc  [g, m_c, d]            one shared copy of the context cache
+    Kd, Vd  [b, g, m_d_max, d]     per-sample decode cache
+    lens    [b] int32              valid decode rows per sample
+
+Recipe: numpy PCG64 seeded per workload, draws in the order q, Kc, Vc, Kd, Vd,
+each ``standard_normal(float32)`` rounded to bf16 with round-to-nearest-even;
+then ``lens`` (``integers(1, m_d_max + 1)`` when ragged, else all ``m_d_max``).
+"""
+from __future__ import annotations
+
+import dataclasses
+
+import numpy as np
+
+BF16_NAN = np.uint16(0x7FC0)
+
+
+@dataclasses.dataclass(frozen=True)
+class Workload:
+    name: str
+    b: int
+    h: int
+    g: int
+    d: int
+    m_c: int
+    m_d_max: int
+    ragged: bool
+    seed: int
+
+    @property
+    def p(self) -> int:
+        return self.h // self.g
+
+
+# The five synthetic layers: a tiny MHA layer; 7B-shaped MHA layers (32 heads
+# of 128) at 16 and 32 samples over an 8k context; an MQA layer with 128
+# samples over 16k; and a GQA layer (8 KV groups) with 256 samples over 32k
+# and ragged decode lengths uniform in [1, 1024].
+WORKLOADS = {
+    w.name: w
+    for w in (
+        Workload("tiny_mha_b4_mc128", 4, 4, 4, 64, 128, 16, False, 1001),
+        Workload("mha7b_b16_mc8k_md256", 16, 32, 32, 128, 8192, 256, False, 1002),
+        Workload("mha7b_b32_mc8k_md512", 32, 32, 32, 128, 8192, 512, False, 1003),
+        Workload("mqa_b128_mc16k_md512", 128, 32, 1, 128, 16384, 512, False, 1004),
+        Workload("gqa8_b256_mc32k_ragged1024", 256, 32, 8, 128, 32768, 1024, True, 1005),
+    )
+}
+WORKLOAD_ORDER = list(WORKLOADS)
+HEADLINE = "mha7b_b32_mc8k_md512"
+
+
+def f32_to_bf16_bits(x: np.ndarray) -> np.ndarray:
+    """Round float32 to bf16 (nearest, ties to even); returns uint16 bits."""
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    u = x.view(np.uint32)
+    rounded = (u + np.uint32(0x7FFF) + ((u >> np.uint32(16)) & np.uint32(1))) >> np.uint32(16)
+    out = rounded.astype(np.uint16)
+    nan = np.isnan(x)
+    if nan.any():
+        out[nan] = BF16_NAN
+    return out
+
+
+def _normal_bf16(rng: np.random.Generator, shape) -> np.ndarray:
+    n = int(np.prod(shape))
+    out = np.empty(n, dtype=np.uint16)
+    step = 1 << 24  # bound the float32 temporary to 64 MiB
+    for s in range(0, n, step):
+        e = min(n, s + step)
+        out[s:e] = f32_to_bf16_bits(rng.standard_normal(e - s, dtype=np.float32))
+    return out.reshape(shape)
+
+
+def make_inputs(b, h, g, d, m_c, m_d_max, *, seed, ragged=False, lens=None,
+                poison_tail=False, with_decode_tail=True):
+    """Draw one problem instance.
+
+    ``lens`` overrides the drawn lengths (it is applied after all draws, so the
+    tensors stay identical). ``poison_tail`` fills decode rows ``t >= len_i``
+    with bf16 NaN, so any read of them shows up in the output.
+    """
+    if h % g:
+        raise ValueError("h must be a multiple of g")
+    rng = np.random.Generator(np.random.PCG64(seed))
+    q = _normal_bf16(rng, (b, h, d))
+    Kc = _normal_bf16(rng, (g, m_c, d))
+    Vc = _normal_bf16(rng, (g, m_c, d))
+    Kd = _normal_bf16(rng, (b, g, m_d_max, d))
+    Vd = _normal_bf16(rng, (b, g, m_d_max, d))
+    if ragged:
+        drawn = rng.integers(1, m_d_max + 1, size=b).astype(np.int32) if m_d_max > 0 \
+            else np.zeros(b, np.int32)
+    else:
+        drawn = np.full(b, m_d_max, dtype=np.int32)
+    if lens is not None:
+        drawn = np.asarray(lens, dtype=np.int32).reshape(b).copy()
+    if poison_tail:
+        for i in range(b):
+            Kd[i, :, drawn[i]:, :] = BF16_NAN
+            Vd[i, :, drawn[i]:, :] = BF16_NAN
+    return dict(q=q, Kc=Kc, Vc=Vc, Kd=Kd, Vd=Vd, lens=drawn)
+
+
+def make_workload_inputs(w: Workload, *, seed=None, poison_tail=False):
+    return make_inputs(w.b, w.h, w.g, w.d, w.m_c, w.m_d_max,
+                       seed=w.seed if seed is None else seed, ragged=w.ragged,
+                       poison_tail=poison_tail)
+
+
+def kv_bytes(g, d, m_c, lens) -> int:
+    """Algorithmic KV bytes of one bifurcated step: one bf16 copy of context
+    K and V plus every sample's valid decode K and V (Section 4.3)."""
+    return 2 * 2 * g * d * (int(m_c) + int(np.sum(lens, dtype=np.int64)))
+
+
+def replicated_kv_bytes(b, g, d, m_c, lens) -> int:
+    """KV bytes when the context is read once per sample (Section 4.3)."""
+    return 2 * 2 * g * d * (b * int(m_c) + int(np.sum(lens, dtype=np.int64)))
+
+
+def attention_flops(h, d, b, m_c, lens) -> int:
+    """Multiply-adds of QK^T and PV counted as 2 flops each: identical for the
+    bifurcated and the standard formulation (Section 4.2)."""
+    return 4 * h * d * (b * int(m_c) + int(np.sum(lens, dtype=np.int64)))
