@@ -1,0 +1,181 @@
+/*
+ * libbifattn -- bifurcated incremental-decoding attention on AMD MI355X (gfx950).
+ *
+ * Method (Bifurcated Attention, Section 4.2, Eq. 3 and Eq. 4): for b samples
+ * that share one prefill context, the attention of each new query token is
+ * split along the key axis into a context part, which reads ONE copy of the
+ * context cache K_c/V_c for all samples, and a decode part, which reads each
+ * sample's own cache K_d/V_d. One softmax spans both parts, so the result is
+ * exactly standard multi-group attention (Section 3.3, Eq. 1-2; proof in
+ * Appendix E.1) while the KV bytes read drop from g*k*b*(m_c+m_d) to
+ * g*k*(m_c + b*m_d) (Section 4.3).
+ *
+ * Notation (Section 3.1): b samples, h query heads, g KV groups with
+ * p = h/g query heads per group (g = h: multi-head, g = 1: multi-query),
+ * d head dimension (the paper's k), m_c context length, m_d_max capacity of
+ * each sample's decode cache, len_i <= m_d_max its valid rows. Query length
+ * is 1 (one new token per sample).
+ *
+ * Layouts (all row-major, all device memory, bf16 = 16-bit brain float):
+ *   q       bf16 [b][h][d]          head j of sample i at (i*h + j)*d
+ *   Kc, Vc  bf16 [g][m_c][d]        one shared copy of the context cache
+ *   Kd, Vd  bf16 [b][g][m_d_max][d] per-sample decode cache
+ *   decode_lens int32 [b]           valid decode rows per sample
+ *   out     fp32 [b][h][d]
+ * Head j reads KV group j / p (group-major, the bgpnk order of Eq. 1).
+ * Decode rows t >= len_i are never read into arithmetic: they may hold
+ * anything, NaN included. Arithmetic: bf16 products, fp32 logits, softmax
+ * statistics and accumulators; softmax weights enter the weighted sum over
+ * values rounded to bf16. Softmax scale: dims.scale, or 1/sqrt(d) when 0.
+ *
+ * Ownership and concurrency: the caller owns every tensor and the stream;
+ * the library never frees caller memory. A plan owns its workspace (allocated
+ * at create, freed at destroy). Calls are asynchronous on the given stream
+ * (no host synchronisation) except bifattn_plan_status and
+ * bifattn_plan_read_timing. One plan must not be used by two calls that may
+ * run concurrently (they share the workspace). Results are bitwise
+ * deterministic for a given plan (fixed split counts and merge order, no
+ * floating-point atomics).
+ *
+ * Errors: every entry point returns a bifattn_status_t. Argument errors are
+ * detected on the host before anything is enqueued and leave `out`
+ * untouched. decode_lens lives on the device, so it is checked there: values
+ * outside [0, m_d_max] are clamped into that range and raise a sticky flag
+ * that bifattn_plan_status reports as BIFATTN_ELENS.
+ */
+#ifndef BIFATTN_H
+#define BIFATTN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define BIFATTN_VERSION 1
+
+typedef enum {
+  BIFATTN_OK = 0,
+  BIFATTN_EINVAL = -1,       /* null pointer, non-positive size, h % g != 0, ... */
+  BIFATTN_EUNSUPPORTED = -2, /* valid but not built: d not in {64,128}, p > 64 */
+  BIFATTN_EALIGN = -3,       /* a tensor pointer not 16-byte aligned */
+  BIFATTN_ENOMEM = -4,       /* workspace or event allocation failed */
+  BIFATTN_EHIP = -5,         /* a HIP runtime call or kernel launch failed */
+  BIFATTN_ELENS = -6         /* a decode length was outside [0, m_d_max] */
+} bifattn_status_t;
+
+/* Problem dimensions (Section 3.1 notation; d is the head dimension). */
+typedef struct {
+  int32_t b;       /* samples sharing the context, >= 1 */
+  int32_t h;       /* query heads, >= 1 */
+  int32_t g;       /* KV groups, >= 1, divides h */
+  int32_t d;       /* head dimension: 64 or 128 */
+  int32_t m_c;     /* context length, >= 1 */
+  int32_t m_d_max; /* decode cache capacity per sample, >= 0 */
+  float scale;     /* softmax scale on q.k; 0 selects 1/sqrt(d) */
+} bifattn_dims_t;
+
+typedef struct bifattn_plan_s *bifattn_plan_t;
+
+/* How a plan splits the work (read-only, for callers that report it). */
+typedef struct {
+  int32_t ctx_keys_per_block; /* context keys one work-group reads */
+  int32_t ctx_splits;         /* S_c: context partial results per output row */
+  int32_t ctx_row_blocks;     /* work-groups sharing one context key chunk */
+  int32_t ctx_blocks;         /* context work-groups per call */
+  int32_t dec_keys_per_block; /* decode keys one work-group reads */
+  int32_t dec_splits;         /* S_d: max decode partial results per output row */
+  int32_t dec_blocks;         /* decode work-groups per call */
+  int32_t fused;              /* 1: context and decode parts in one launch */
+  size_t workspace_bytes;     /* device memory the plan owns */
+} bifattn_plan_info_t;
+
+/* Kernels a plan launches; used to select what bifattn_plan_set_timing times. */
+typedef enum {
+  BIFATTN_KERNEL_PARTIALS = 0, /* context + decode partial kernel(s) of a call */
+  BIFATTN_KERNEL_COMBINE = 1,  /* online-softmax combine of a call */
+  BIFATTN_KERNEL_CALL = 2      /* the whole call, first launch to last */
+} bifattn_kernel_t;
+
+/*
+ * Validate dims and allocate the plan and its workspace on the current HIP
+ * device. On success *plan is set; on failure *plan is left NULL.
+ * Errors: EINVAL (null argument, b/h/g/m_c < 1, m_d_max < 0, h % g != 0,
+ * sizes whose byte counts overflow), EUNSUPPORTED (d not 64 or 128, or
+ * h/g > 64), ENOMEM (device allocation failed), EHIP (no usable device).
+ */
+bifattn_status_t bifattn_plan_create(const bifattn_dims_t *dims, bifattn_plan_t *plan);
+
+/* Free the plan and its workspace after waiting for its device work.
+ * NULL is accepted and ignored. */
+bifattn_status_t bifattn_plan_destroy(bifattn_plan_t plan);
+
+/* Fill *info with the plan's split decisions. EINVAL on null arguments. */
+bifattn_status_t bifattn_plan_get_info(bifattn_plan_t plan, bifattn_plan_info_t *info);
+
+/*
+ * One bifurcated decode-attention step (Section 4.2, Eq. 3-4):
+ *   out[i, j, :] = softmax_t( scale * q[i,j,:] . K_i[t,:] ) @ V_i
+ * with K_i = Kc[j/p] (+) Kd[i, j/p, 0:len_i] and V_i likewise. Enqueues on
+ * `stream` (a) context partials: each work-group stages a chunk of Kc/Vc of
+ * one group once and applies it to all b*p query rows of the group; (b)
+ * decode partials: per sample and group over its own Kd/Vd; (c) the combine,
+ * which merges the (max, sum, weighted-value) partials of both parts into
+ * `out`. Kd, Vd and decode_lens may be NULL only when m_d_max == 0.
+ * Errors: EINVAL (null plan or required pointer), EALIGN (q, Kc, Vc, Kd, Vd
+ * or out not 16-byte aligned, decode_lens not 4-byte aligned), EHIP (launch
+ * failure). Device-side length errors: see bifattn_plan_status.
+ */
+bifattn_status_t bifattn_decode(bifattn_plan_t plan, const void *q, const void *Kc,
+                                const void *Vc, const void *Kd, const void *Vd,
+                                const int32_t *decode_lens, float *out, hipStream_t stream);
+
+/*
+ * Ablation without bifurcation (the baseline of Section 4.1): the same
+ * attention, but every sample reads its own physically replicated cache
+ *   K, V   bf16 [b][g][m_c + m_d_max][d], rows 0..m_c-1 the context copy,
+ *          rows m_c..m_c+len_i-1 the sample's decode rows,
+ * so the context is read b times. Same partial and combine kernels, no
+ * context part. Same errors as bifattn_decode.
+ */
+bifattn_status_t bifattn_decode_replicated(bifattn_plan_t plan, const void *q, const void *K,
+                                           const void *V, const int32_t *decode_lens,
+                                           float *out, hipStream_t stream);
+
+/*
+ * Synchronise `stream`, then report and clear the plan's device-side flag:
+ * BIFATTN_ELENS if any call since the last check saw a decode length outside
+ * [0, m_d_max] (the call used the clamped length), else BIFATTN_OK.
+ * EHIP if the stream reports an error.
+ */
+bifattn_status_t bifattn_plan_status(bifattn_plan_t plan, hipStream_t stream);
+
+/*
+ * Time the selected kernel of the next `capacity` calls with HIP events
+ * recorded on each call's stream around that kernel's launch (capacity 0
+ * switches timing off). Timing stops recording when full.
+ * Errors: EINVAL (bad kernel id or negative capacity), ENOMEM, EHIP.
+ */
+bifattn_status_t bifattn_plan_set_timing(bifattn_plan_t plan, bifattn_kernel_t kernel,
+                                         int32_t capacity);
+
+/*
+ * Wait for the recorded events and return the number of timed calls and the
+ * sum of their durations in milliseconds; then rewind the recorder.
+ */
+bifattn_status_t bifattn_plan_read_timing(bifattn_plan_t plan, int32_t *calls, double *total_ms);
+
+/* Static text for a status code. Never NULL. */
+const char *bifattn_status_string(bifattn_status_t status);
+
+/* BIFATTN_VERSION of the built library. */
+int32_t bifattn_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* BIFATTN_H */

@@ -1,0 +1,220 @@
+"""Python binding of libbifattn (bifurcated decode attention on MI355X).
+
+Argument marshalling only: every step of the computation runs in the HIP
+kernels of ``libbifattn.so``. The functions carry the C ABI's names
+(include/bifattn.h); torch tensors are checked against the plan's shape,
+dtype, device and contiguity before their device pointers are handed over,
+so a mismatched tensor is refused on the host instead of being read out of
+bounds on the GPU. There is no fallback: without the built library every
+entry point raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libbifattn.so")
+
+OK, EINVAL, EUNSUPPORTED, EALIGN, ENOMEM, EHIP, ELENS = 0, -1, -2, -3, -4, -5, -6
+KERNEL_PARTIALS, KERNEL_COMBINE, KERNEL_CALL = 0, 1, 2
+
+EXPORTED = (
+    "bifattn_plan_create", "bifattn_plan_destroy", "bifattn_plan_get_info", "bifattn_decode",
+    "bifattn_decode_replicated", "bifattn_plan_status", "bifattn_plan_set_timing",
+    "bifattn_plan_read_timing", "bifattn_status_string", "bifattn_version",
+)
+
+
+class BifattnError(RuntimeError):
+    def __init__(self, status: int, what: str):
+        self.status = status
+        super().__init__(f"{what}: {status_string(status)} ({status})")
+
+
+class Dims(ctypes.Structure):
+    _fields_ = [("b", ctypes.c_int32), ("h", ctypes.c_int32), ("g", ctypes.c_int32),
+                ("d", ctypes.c_int32), ("m_c", ctypes.c_int32), ("m_d_max", ctypes.c_int32),
+                ("scale", ctypes.c_float)]
+
+
+class PlanInfo(ctypes.Structure):
+    _fields_ = [("ctx_keys_per_block", ctypes.c_int32), ("ctx_splits", ctypes.c_int32),
+                ("ctx_row_blocks", ctypes.c_int32), ("ctx_blocks", ctypes.c_int32),
+                ("dec_keys_per_block", ctypes.c_int32), ("dec_splits", ctypes.c_int32),
+                ("dec_blocks", ctypes.c_int32), ("fused", ctypes.c_int32),
+                ("workspace_bytes", ctypes.c_size_t)]
+
+    def as_dict(self):
+        return {name: getattr(self, name) for name, _ in self._fields_}
+
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    """Load libbifattn.so (built in-tree); raises if it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with "
+                               "`python -m paper_2403_08845_amd.build`")
+        L = ctypes.CDLL(LIB_PATH)
+        vp, i32, st = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int
+        L.bifattn_plan_create.argtypes = [ctypes.POINTER(Dims), ctypes.POINTER(vp)]
+        L.bifattn_plan_destroy.argtypes = [vp]
+        L.bifattn_plan_get_info.argtypes = [vp, ctypes.POINTER(PlanInfo)]
+        L.bifattn_decode.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp]
+        L.bifattn_decode_replicated.argtypes = [vp, vp, vp, vp, vp, vp, vp]
+        L.bifattn_plan_status.argtypes = [vp, vp]
+        L.bifattn_plan_set_timing.argtypes = [vp, st, i32]
+        L.bifattn_plan_read_timing.argtypes = [vp, ctypes.POINTER(i32), ctypes.POINTER(ctypes.c_double)]
+        L.bifattn_status_string.argtypes = [st]
+        L.bifattn_status_string.restype = ctypes.c_char_p
+        L.bifattn_version.restype = i32
+        for name in EXPORTED:
+            if name not in ("bifattn_status_string", "bifattn_version"):
+                getattr(L, name).restype = st
+        _lib = L
+    return _lib
+
+
+def status_string(status: int) -> str:
+    return lib().bifattn_status_string(int(status)).decode()
+
+
+def bifattn_version() -> int:
+    return int(lib().bifattn_version())
+
+
+def _check(status: int, what: str):
+    if status != OK:
+        raise BifattnError(status, what)
+
+
+class Plan:
+    """A bifattn_plan_t: problem dimensions plus the workspace it owns."""
+
+    def __init__(self, b, h, g, d, m_c, m_d_max, scale=0.0):
+        self.dims = Dims(b, h, g, d, m_c, m_d_max, scale)
+        handle = ctypes.c_void_p()
+        _check(lib().bifattn_plan_create(ctypes.byref(self.dims), ctypes.byref(handle)),
+               "bifattn_plan_create")
+        self.handle = handle
+
+    def close(self):
+        if getattr(self, "handle", None) is not None and self.handle.value:
+            _check(lib().bifattn_plan_destroy(self.handle), "bifattn_plan_destroy")
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def __enter__(self):
+        return self
+
+    def __exit__(self, *exc):
+        self.close()
+
+    def info(self) -> dict:
+        info = PlanInfo()
+        _check(lib().bifattn_plan_get_info(self.handle, ctypes.byref(info)), "bifattn_plan_get_info")
+        return info.as_dict()
+
+
+def bifattn_plan_create(b, h, g, d, m_c, m_d_max, scale=0.0) -> Plan:
+    return Plan(b, h, g, d, m_c, m_d_max, scale)
+
+
+def bifattn_plan_destroy(plan: Plan):
+    plan.close()
+
+
+def bifattn_plan_get_info(plan: Plan) -> dict:
+    return plan.info()
+
+
+def _stream_ptr(stream):
+    if stream is None:
+        import torch
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream))
+
+
+def _tensor(t, shape, dtype, device, name):
+    import torch
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    if tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} must have shape {tuple(shape)}, got {tuple(t.shape)}")
+    if not t.is_cuda or (device is not None and t.device != device):
+        raise ValueError(f"{name} must live on {device or 'the GPU'}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def bifattn_decode(plan: Plan, q, Kc, Vc, Kd, Vd, decode_lens, out, stream=None):
+    """Enqueue one bifurcated decode step (see include/bifattn.h).
+
+    q bf16 [b,h,d]; Kc, Vc bf16 [g,m_c,d]; Kd, Vd bf16 [b,g,m_d_max,d];
+    decode_lens int32 [b]; out fp32 [b,h,d]; all on the same GPU.
+    """
+    import torch
+    D = plan.dims
+    dev = q.device
+    args = [
+        _tensor(q, (D.b, D.h, D.d), torch.bfloat16, dev, "q"),
+        _tensor(Kc, (D.g, D.m_c, D.d), torch.bfloat16, dev, "Kc"),
+        _tensor(Vc, (D.g, D.m_c, D.d), torch.bfloat16, dev, "Vc"),
+        _tensor(Kd, (D.b, D.g, D.m_d_max, D.d), torch.bfloat16, dev, "Kd"),
+        _tensor(Vd, (D.b, D.g, D.m_d_max, D.d), torch.bfloat16, dev, "Vd"),
+        _tensor(decode_lens, (D.b,), torch.int32, dev, "decode_lens"),
+        _tensor(out, (D.b, D.h, D.d), torch.float32, dev, "out"),
+    ]
+    _check(lib().bifattn_decode(plan.handle, *args, _stream_ptr(stream)), "bifattn_decode")
+
+
+def bifattn_decode_replicated(plan: Plan, q, K, V, decode_lens, out, stream=None):
+    """Enqueue the ablation over a physically replicated cache
+    K, V bf16 [b, g, m_c + m_d_max, d]."""
+    import torch
+    D = plan.dims
+    dev = q.device
+    rows = D.m_c + D.m_d_max
+    args = [
+        _tensor(q, (D.b, D.h, D.d), torch.bfloat16, dev, "q"),
+        _tensor(K, (D.b, D.g, rows, D.d), torch.bfloat16, dev, "K"),
+        _tensor(V, (D.b, D.g, rows, D.d), torch.bfloat16, dev, "V"),
+        _tensor(decode_lens, (D.b,), torch.int32, dev, "decode_lens"),
+        _tensor(out, (D.b, D.h, D.d), torch.float32, dev, "out"),
+    ]
+    _check(lib().bifattn_decode_replicated(plan.handle, *args, _stream_ptr(stream)),
+           "bifattn_decode_replicated")
+
+
+def bifattn_plan_status(plan: Plan, stream=None) -> int:
+    """Synchronise the stream; return OK or ELENS (and clear the flag)."""
+    st = lib().bifattn_plan_status(plan.handle, _stream_ptr(stream))
+    if st not in (OK, ELENS):
+        raise BifattnError(st, "bifattn_plan_status")
+    return st
+
+
+def bifattn_plan_set_timing(plan: Plan, kernel: int, capacity: int):
+    _check(lib().bifattn_plan_set_timing(plan.handle, int(kernel), int(capacity)),
+           "bifattn_plan_set_timing")
+
+
+def bifattn_plan_read_timing(plan: Plan):
+    """(number of timed calls, total milliseconds)."""
+    n = ctypes.c_int32()
+    ms = ctypes.c_double()
+    _check(lib().bifattn_plan_read_timing(plan.handle, ctypes.byref(n), ctypes.byref(ms)),
+           "bifattn_plan_read_timing")
+    return int(n.value), float(ms.value)

@@ -1,0 +1,441 @@
+// Host side of libbifattn: argument validation, work splitting, workspace
+// ownership, launches and the C ABI declared in include/bifattn.h.
+#include "bifattn.h"
+
+#include <hip/hip_runtime_api.h>
+
+#include <cmath>
+#include <cstdint>
+#include <cstdlib>
+#include <new>
+#include <vector>
+
+#include "bifattn_internal.h"
+
+using namespace bifattn;
+
+struct bifattn_plan_s {
+  bifattn_dims_t dims{};
+  float scale = 0.f;
+  int p = 0, M = 0;
+  int ctx_mode = kCtxNone;
+  int dec_tiles = 1;
+  int ctx_keys = 0, S_c = 0, ctx_row_blocks = 1, n_ctx_blocks = 0;
+  int dec_keys = 0, S_d = 0, n_dec_blocks = 0;
+  int rep_keys = 0, S_r = 0, n_rep_blocks = 0;
+  int fused = 1;
+  int device = 0;
+  // workspace
+  void* ws = nullptr;
+  size_t ws_bytes = 0;
+  float* ctx_acc = nullptr;
+  float2* ctx_ml = nullptr;
+  float* dec_acc = nullptr;
+  float2* dec_ml = nullptr;
+  int* status = nullptr;
+  // timing
+  int timed_kernel = -1;
+  int timing_cap = 0;
+  int timing_n = 0;
+  std::vector<hipEvent_t> events;
+};
+
+namespace {
+
+constexpr int kCUs = 256;  // MI355X compute units; split heuristics aim at whole waves of them
+
+int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+int64_t round_up(int64_t a, int64_t b) { return ceil_div(a, b) * b; }
+size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+
+// Tuning overrides from the environment: a positive integer, else `fallback`.
+int env_int(const char* name, int fallback) {
+  const char* v = std::getenv(name);
+  if (!v || !*v) return fallback;
+  char* end = nullptr;
+  long x = std::strtol(v, &end, 10);
+  return (end && *end == 0 && x > 0 && x < (1 << 30)) ? (int)x : fallback;
+}
+
+bool aligned(const void* ptr, uintptr_t a) { return ((uintptr_t)ptr & (a - 1)) == 0; }
+
+// Keys one decode (or replicated) work-group reads: 512 keys by default,
+// halved (down to 128) while fewer than 4 work-groups per CU would exist.
+int pick_seq_keys(int64_t units, int rows, int start) {
+  int keys = start;
+  while (keys > 128 && units * ceil_div(rows, keys) < 4 * kCUs) keys /= 2;
+  return keys;
+}
+
+bifattn_status_t plan_splits(bifattn_plan_s* P) {
+  const bifattn_dims_t& d = P->dims;
+  P->p = d.h / d.g;
+  P->M = d.b * P->p;
+  P->dec_tiles = P->p <= 16 ? 1 : (P->p <= 32 ? 2 : 4);
+  const int64_t M = P->M;
+  if (M <= 64) {
+    P->ctx_mode = M <= 16 ? kCtxSmall1 : (M <= 32 ? kCtxSmall2 : kCtxSmall4);
+    // About one context work-group per CU, each a multiple of 4 waves x 32 keys.
+    int64_t keys = round_up(ceil_div((int64_t)d.g * d.m_c, kCUs), kWaves * kTileKeys);
+    keys = env_int("BIFATTN_CTX_KEYS", (int)keys);
+    keys = round_up(keys, kWaves * kTileKeys);
+    if (keys > round_up(d.m_c, kWaves * kTileKeys)) keys = round_up(d.m_c, kWaves * kTileKeys);
+    P->ctx_keys = (int)keys;
+    P->ctx_row_blocks = 1;
+  } else {
+    P->ctx_mode = kCtxLarge;
+    P->ctx_row_blocks = (int)ceil_div(M, kLargeRowsPerBlock);
+    int64_t splits = ceil_div(kCUs, (int64_t)d.g * P->ctx_row_blocks);
+    if (splits < 1) splits = 1;
+    int64_t keys = round_up(ceil_div(d.m_c, splits), kTileKeys);
+    keys = env_int("BIFATTN_CTX_KEYS", (int)keys);
+    keys = round_up(keys, kTileKeys);
+    P->ctx_keys = (int)keys;
+  }
+  P->S_c = (int)ceil_div(d.m_c, P->ctx_keys);
+  P->n_ctx_blocks = d.g * P->S_c * P->ctx_row_blocks;
+  const int64_t units = (int64_t)d.b * d.g;
+  if (d.m_d_max > 0) {
+    P->dec_keys = env_int("BIFATTN_DEC_KEYS", pick_seq_keys(units, d.m_d_max, 512));
+    P->dec_keys = (int)round_up(P->dec_keys, kTileKeys);
+    P->S_d = (int)ceil_div(d.m_d_max, P->dec_keys);
+  } else {
+    P->dec_keys = kWaves * kTileKeys;
+    P->S_d = 0;
+  }
+  P->n_dec_blocks = (int)(units * P->S_d);
+  const int rep_rows = d.m_c + d.m_d_max;
+  P->rep_keys = env_int("BIFATTN_REP_KEYS", pick_seq_keys(units, rep_rows, 1024));
+  P->rep_keys = (int)round_up(P->rep_keys, kTileKeys);
+  P->S_r = (int)ceil_div(rep_rows, P->rep_keys);
+  P->n_rep_blocks = (int)(units * P->S_r);
+  // One launch for both parts when their work-groups have the same register
+  // footprint; the many-row context path runs as its own launch.
+  // BIFATTN_LAUNCH=1 forces one launch, 2 forces two.
+  const int launch = env_int("BIFATTN_LAUNCH", P->ctx_mode == kCtxLarge ? 2 : 1);
+  P->fused = launch == 1 ? 1 : 0;
+  if ((int64_t)P->n_ctx_blocks + P->n_dec_blocks > INT32_MAX / 2 || units * P->S_r > INT32_MAX / 2)
+    return BIFATTN_EINVAL;
+  return BIFATTN_OK;
+}
+
+bifattn_status_t check_dims(const bifattn_dims_t* d) {
+  if (!d) return BIFATTN_EINVAL;
+  if (d->b < 1 || d->h < 1 || d->g < 1 || d->m_c < 1 || d->m_d_max < 0) return BIFATTN_EINVAL;
+  if (d->h % d->g) return BIFATTN_EINVAL;
+  if (!(std::isfinite(d->scale))) return BIFATTN_EINVAL;
+  if (d->d != 64 && d->d != 128) return BIFATTN_EUNSUPPORTED;
+  if (d->h / d->g > kMaxP) return BIFATTN_EUNSUPPORTED;
+  // element counts of the largest tensors must stay far from 2^62
+  const double lim = 4.0e18;
+  const double dd = d->d;
+  if ((double)d->b * d->h * dd > lim || (double)d->g * d->m_c * dd > lim ||
+      (double)d->b * d->g * ((double)d->m_c + d->m_d_max) * dd > lim)
+    return BIFATTN_EINVAL;
+  if ((double)d->b * d->h > INT32_MAX / 2 || (double)d->b * d->g > INT32_MAX / 2)
+    return BIFATTN_EINVAL;
+  return BIFATTN_OK;
+}
+
+void free_events(bifattn_plan_s* P) {
+  for (hipEvent_t e : P->events) (void)hipEventDestroy(e);
+  P->events.clear();
+  P->timing_cap = P->timing_n = 0;
+  P->timed_kernel = -1;
+}
+
+// Event pair around one kernel of this call, if that kernel is being timed.
+struct TimedSection {
+  bifattn_plan_s* P;
+  hipStream_t stream;
+  bool on = false;
+  TimedSection(bifattn_plan_s* P_, int kernel, hipStream_t s) : P(P_), stream(s) {
+    on = P->timed_kernel == kernel && P->timing_n < P->timing_cap;
+    if (on) (void)hipEventRecord(P->events[2 * P->timing_n], stream);
+  }
+  void end() {
+    if (on) {
+      (void)hipEventRecord(P->events[2 * P->timing_n + 1], stream);
+      ++P->timing_n;
+      on = false;
+    }
+  }
+};
+
+PartialsParams base_params(const bifattn_plan_s* P, const void* q, const int32_t* lens) {
+  PartialsParams K{};
+  K.q = static_cast<const uint16_t*>(q);
+  K.lens = lens;
+  K.ctx_acc = P->ctx_acc;
+  K.ctx_ml = P->ctx_ml;
+  K.dec_acc = P->dec_acc;
+  K.dec_ml = P->dec_ml;
+  K.status = P->status;
+  K.b = P->dims.b;
+  K.h = P->dims.h;
+  K.g = P->dims.g;
+  K.p = P->p;
+  K.M = P->M;
+  K.m_c = P->dims.m_c;
+  K.m_d_max = P->dims.m_d_max;
+  K.scale_log2 = P->scale * 1.4426950408889634f;
+  return K;
+}
+
+CombineParams combine_params(const bifattn_plan_s* P, const int32_t* lens, float* out) {
+  CombineParams C{};
+  C.ctx_acc = P->ctx_acc;
+  C.ctx_ml = P->ctx_ml;
+  C.dec_acc = P->dec_acc;
+  C.dec_ml = P->dec_ml;
+  C.lens = lens;
+  C.out = out;
+  C.status = P->status;
+  C.b = P->dims.b;
+  C.h = P->dims.h;
+  C.g = P->dims.g;
+  C.p = P->p;
+  C.M = P->M;
+  C.m_d_max = P->dims.m_d_max;
+  return C;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* bifattn_status_string(bifattn_status_t s) {
+  switch (s) {
+    case BIFATTN_OK: return "ok";
+    case BIFATTN_EINVAL: return "invalid argument";
+    case BIFATTN_EUNSUPPORTED: return "unsupported shape (d must be 64 or 128, h/g at most 64)";
+    case BIFATTN_EALIGN: return "tensor pointer not 16-byte aligned (decode_lens: 4-byte)";
+    case BIFATTN_ENOMEM: return "device memory allocation failed";
+    case BIFATTN_EHIP: return "HIP runtime error";
+    case BIFATTN_ELENS: return "a decode length was outside [0, m_d_max] and was clamped";
+  }
+  return "unknown status";
+}
+
+int32_t bifattn_version(void) { return BIFATTN_VERSION; }
+
+bifattn_status_t bifattn_plan_create(const bifattn_dims_t* dims, bifattn_plan_t* plan) {
+  if (!plan) return BIFATTN_EINVAL;
+  *plan = nullptr;
+  bifattn_status_t st = check_dims(dims);
+  if (st != BIFATTN_OK) return st;
+  bifattn_plan_s* P = new (std::nothrow) bifattn_plan_s();
+  if (!P) return BIFATTN_ENOMEM;
+  P->dims = *dims;
+  P->scale = dims->scale != 0.f ? dims->scale : 1.0f / std::sqrt((float)dims->d);
+  st = plan_splits(P);
+  if (st != BIFATTN_OK) {
+    delete P;
+    return st;
+  }
+  int ndev = 0;
+  if (hipGetDeviceCount(&ndev) != hipSuccess || ndev < 1 || hipGetDevice(&P->device) != hipSuccess) {
+    delete P;
+    return BIFATTN_EHIP;
+  }
+  const bifattn_dims_t& d = P->dims;
+  const size_t D = (size_t)d.d;
+  const size_t ctx_rows = (size_t)d.g * P->S_c * P->M;
+  const size_t dec_rows = (size_t)d.b * d.g * (size_t)(P->S_d > P->S_r ? P->S_d : P->S_r) * P->p;
+  size_t off = 0;
+  const size_t o_ctx_acc = off;
+  off = align256(off + ctx_rows * D * 4);
+  const size_t o_ctx_ml = off;
+  off = align256(off + ctx_rows * 8);
+  const size_t o_dec_acc = off;
+  off = align256(off + dec_rows * D * 4);
+  const size_t o_dec_ml = off;
+  off = align256(off + dec_rows * 8);
+  const size_t o_status = off;
+  off = align256(off + 4);
+  if (hipMalloc(&P->ws, off) != hipSuccess) {
+    (void)hipGetLastError();
+    delete P;
+    return BIFATTN_ENOMEM;
+  }
+  P->ws_bytes = off;
+  char* base = static_cast<char*>(P->ws);
+  P->ctx_acc = reinterpret_cast<float*>(base + o_ctx_acc);
+  P->ctx_ml = reinterpret_cast<float2*>(base + o_ctx_ml);
+  P->dec_acc = reinterpret_cast<float*>(base + o_dec_acc);
+  P->dec_ml = reinterpret_cast<float2*>(base + o_dec_ml);
+  P->status = reinterpret_cast<int*>(base + o_status);
+  if (hipMemset(P->status, 0, 4) != hipSuccess) {
+    (void)hipFree(P->ws);
+    delete P;
+    return BIFATTN_EHIP;
+  }
+  *plan = P;
+  return BIFATTN_OK;
+}
+
+bifattn_status_t bifattn_plan_destroy(bifattn_plan_t P) {
+  if (!P) return BIFATTN_OK;
+  bifattn_status_t st = BIFATTN_OK;
+  if (hipDeviceSynchronize() != hipSuccess) st = BIFATTN_EHIP;
+  free_events(P);
+  if (P->ws && hipFree(P->ws) != hipSuccess) st = BIFATTN_EHIP;
+  delete P;
+  return st;
+}
+
+bifattn_status_t bifattn_plan_get_info(bifattn_plan_t P, bifattn_plan_info_t* info) {
+  if (!P || !info) return BIFATTN_EINVAL;
+  info->ctx_keys_per_block = P->ctx_keys;
+  info->ctx_splits = P->S_c;
+  info->ctx_row_blocks = P->ctx_row_blocks;
+  info->ctx_blocks = P->n_ctx_blocks;
+  info->dec_keys_per_block = P->dec_keys;
+  info->dec_splits = P->S_d;
+  info->dec_blocks = P->n_dec_blocks;
+  info->fused = P->fused;
+  info->workspace_bytes = P->ws_bytes;
+  return BIFATTN_OK;
+}
+
+bifattn_status_t bifattn_decode(bifattn_plan_t P, const void* q, const void* Kc, const void* Vc,
+                                const void* Kd, const void* Vd, const int32_t* decode_lens,
+                                float* out, hipStream_t stream) {
+  if (!P || !q || !Kc || !Vc || !out) return BIFATTN_EINVAL;
+  const bool has_dec = P->dims.m_d_max > 0;
+  if (has_dec && (!Kd || !Vd || !decode_lens)) return BIFATTN_EINVAL;
+  if (!aligned(q, 16) || !aligned(Kc, 16) || !aligned(Vc, 16) || !aligned(out, 16))
+    return BIFATTN_EALIGN;
+  if (has_dec && (!aligned(Kd, 16) || !aligned(Vd, 16) || !aligned(decode_lens, 4)))
+    return BIFATTN_EALIGN;
+  PartialsParams K = base_params(P, q, has_dec ? decode_lens : nullptr);
+  K.Kc = static_cast<const uint16_t*>(Kc);
+  K.Vc = static_cast<const uint16_t*>(Vc);
+  K.Kd = static_cast<const uint16_t*>(Kd);
+  K.Vd = static_cast<const uint16_t*>(Vd);
+  K.dec_rows = P->dims.m_d_max;
+  K.len_offset = 0;
+  K.ctx_keys = P->ctx_keys;
+  K.S_c = P->S_c;
+  K.ctx_row_blocks = P->ctx_row_blocks;
+  K.dec_keys = P->dec_keys;
+  K.S_d = P->S_d;
+  TimedSection whole(P, BIFATTN_KERNEL_CALL, stream);
+  TimedSection part(P, BIFATTN_KERNEL_PARTIALS, stream);
+  hipError_t e;
+  if (P->fused) {
+    K.n_ctx_blocks = P->n_ctx_blocks;
+    K.n_dec_blocks = P->n_dec_blocks;
+    e = launch_partials(K, P->dims.d, P->ctx_mode, P->dec_tiles, stream);
+  } else {
+    K.n_ctx_blocks = P->n_ctx_blocks;
+    K.n_dec_blocks = 0;
+    e = launch_partials(K, P->dims.d, P->ctx_mode, P->dec_tiles, stream);
+    if (e == hipSuccess && P->n_dec_blocks) {
+      K.n_ctx_blocks = 0;
+      K.n_dec_blocks = P->n_dec_blocks;
+      e = launch_partials(K, P->dims.d, kCtxNone, P->dec_tiles, stream);
+    }
+  }
+  part.end();
+  if (e != hipSuccess) return BIFATTN_EHIP;
+  TimedSection comb(P, BIFATTN_KERNEL_COMBINE, stream);
+  CombineParams C = combine_params(P, has_dec ? decode_lens : nullptr, out);
+  C.len_offset = 0;
+  C.S_c = P->S_c;
+  C.dec_keys = P->dec_keys;
+  C.S_d = P->S_d;
+  e = launch_combine(C, P->dims.d, stream);
+  comb.end();
+  whole.end();
+  return e == hipSuccess ? BIFATTN_OK : BIFATTN_EHIP;
+}
+
+bifattn_status_t bifattn_decode_replicated(bifattn_plan_t P, const void* q, const void* K_,
+                                           const void* V_, const int32_t* decode_lens, float* out,
+                                           hipStream_t stream) {
+  if (!P || !q || !K_ || !V_ || !out) return BIFATTN_EINVAL;
+  const bool has_dec = P->dims.m_d_max > 0;
+  if (has_dec && !decode_lens) return BIFATTN_EINVAL;
+  if (!aligned(q, 16) || !aligned(K_, 16) || !aligned(V_, 16) || !aligned(out, 16))
+    return BIFATTN_EALIGN;
+  if (has_dec && !aligned(decode_lens, 4)) return BIFATTN_EALIGN;
+  PartialsParams K = base_params(P, q, has_dec ? decode_lens : nullptr);
+  K.Kd = static_cast<const uint16_t*>(K_);
+  K.Vd = static_cast<const uint16_t*>(V_);
+  K.dec_rows = P->dims.m_c + P->dims.m_d_max;
+  K.len_offset = P->dims.m_c;
+  K.dec_keys = P->rep_keys;
+  K.S_d = P->S_r;
+  K.S_c = 0;
+  K.n_ctx_blocks = 0;
+  K.n_dec_blocks = P->n_rep_blocks;
+  TimedSection whole(P, BIFATTN_KERNEL_CALL, stream);
+  TimedSection part(P, BIFATTN_KERNEL_PARTIALS, stream);
+  hipError_t e = launch_partials(K, P->dims.d, kCtxNone, P->dec_tiles, stream);
+  part.end();
+  if (e != hipSuccess) return BIFATTN_EHIP;
+  TimedSection comb(P, BIFATTN_KERNEL_COMBINE, stream);
+  CombineParams C = combine_params(P, has_dec ? decode_lens : nullptr, out);
+  C.len_offset = P->dims.m_c;
+  C.S_c = 0;
+  C.dec_keys = P->rep_keys;
+  C.S_d = P->S_r;
+  e = launch_combine(C, P->dims.d, stream);
+  comb.end();
+  whole.end();
+  return e == hipSuccess ? BIFATTN_OK : BIFATTN_EHIP;
+}
+
+bifattn_status_t bifattn_plan_status(bifattn_plan_t P, hipStream_t stream) {
+  if (!P) return BIFATTN_EINVAL;
+  if (hipStreamSynchronize(stream) != hipSuccess) return BIFATTN_EHIP;
+  int flag = 0;
+  if (hipMemcpy(&flag, P->status, sizeof flag, hipMemcpyDeviceToHost) != hipSuccess)
+    return BIFATTN_EHIP;
+  if (flag) {
+    if (hipMemset(P->status, 0, sizeof flag) != hipSuccess) return BIFATTN_EHIP;
+    return BIFATTN_ELENS;
+  }
+  return BIFATTN_OK;
+}
+
+bifattn_status_t bifattn_plan_set_timing(bifattn_plan_t P, bifattn_kernel_t kernel,
+                                         int32_t capacity) {
+  if (!P || capacity < 0 || (int)kernel < 0 || (int)kernel > BIFATTN_KERNEL_CALL)
+    return BIFATTN_EINVAL;
+  if (hipDeviceSynchronize() != hipSuccess) return BIFATTN_EHIP;
+  free_events(P);
+  if (capacity == 0) return BIFATTN_OK;
+  P->events.reserve(2 * (size_t)capacity);
+  for (int i = 0; i < 2 * capacity; ++i) {
+    hipEvent_t e;
+    if (hipEventCreate(&e) != hipSuccess) {
+      free_events(P);
+      return BIFATTN_ENOMEM;
+    }
+    P->events.push_back(e);
+  }
+  P->timed_kernel = (int)kernel;
+  P->timing_cap = capacity;
+  P->timing_n = 0;
+  return BIFATTN_OK;
+}
+
+bifattn_status_t bifattn_plan_read_timing(bifattn_plan_t P, int32_t* calls, double* total_ms) {
+  if (!P || !calls || !total_ms) return BIFATTN_EINVAL;
+  double sum = 0.0;
+  for (int k = 0; k < P->timing_n; ++k) {
+    if (hipEventSynchronize(P->events[2 * k + 1]) != hipSuccess) return BIFATTN_EHIP;
+    float ms = 0.f;
+    if (hipEventElapsedTime(&ms, P->events[2 * k], P->events[2 * k + 1]) != hipSuccess)
+      return BIFATTN_EHIP;
+    sum += ms;
+  }
+  *calls = P->timing_n;
+  *total_ms = sum;
+  P->timing_n = 0;
+  return BIFATTN_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,84 @@
+// Launch parameters shared by the library's host code and its HIP kernels.
+#pragma once
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+namespace bifattn {
+
+// Work-group shape of every partial kernel: four 64-wide waves.
+constexpr int kWaves = 4;
+constexpr int kThreads = 64 * kWaves;
+// Keys per tile: one tile is two 16-key MFMA sub-tiles.
+constexpr int kTileKeys = 32;
+// Query rows per MFMA N-tile.
+constexpr int kRowsPerTile = 16;
+// Context path with many query rows per group: query tiles per wave.
+constexpr int kLargeTilesPerWave = 4;
+constexpr int kLargeRowsPerBlock = kWaves * kLargeTilesPerWave * kRowsPerTile;  // 256
+// Largest group size the per-sample decode path holds in registers.
+constexpr int kMaxP = 64;
+// Lazy softmax rescaling: the running reference maximum is only raised when a
+// tile's maximum exceeds it by more than this many powers of two, which keeps
+// every weight below 2^kRescaleSlack.
+constexpr float kRescaleSlack = 8.0f;
+
+// Device-side status bits.
+constexpr int kStatusLens = 1;
+
+// Partial result of one query row over one key range, relative to 2^m:
+// m  = reference maximum of scale*log2(e)*(q.k) over the range (or -inf),
+// l  = sum of 2^(logit - m), acc[d] = sum of 2^(logit - m) * v.
+struct PartialsParams {
+  const uint16_t* q;
+  const uint16_t* Kc;
+  const uint16_t* Vc;
+  const uint16_t* Kd;     // decode cache (replicated cache in ablation mode)
+  const uint16_t* Vd;
+  const int32_t* lens;
+  float* ctx_acc;         // [g][S_c][M][d]
+  float2* ctx_ml;         // [g][S_c][M]
+  float* dec_acc;         // [b][g][S_d][p][d]
+  float2* dec_ml;         // [b][g][S_d][p]
+  int* status;
+  int b, h, g, p, M;      // M = b*p query rows per group
+  int m_c;
+  int m_d_max;            // clamp bound for lens
+  int dec_rows;           // row capacity of one (sample, group) decode cache
+  int len_offset;         // rows before the decode rows in that cache (0, or m_c in ablation)
+  int ctx_keys;           // keys per context work-group
+  int S_c;
+  int ctx_row_blocks;
+  int dec_keys;           // keys per decode work-group
+  int S_d;
+  int n_ctx_blocks;
+  int n_dec_blocks;
+  float scale_log2;       // scale * log2(e)
+};
+
+struct CombineParams {
+  const float* ctx_acc;
+  const float2* ctx_ml;
+  const float* dec_acc;
+  const float2* dec_ml;
+  const int32_t* lens;
+  float* out;
+  int* status;
+  int b, h, g, p, M;
+  int m_d_max;
+  int len_offset;
+  int S_c;
+  int dec_keys;
+  int S_d;
+};
+
+enum CtxMode { kCtxNone = 0, kCtxSmall1 = 1, kCtxSmall2 = 2, kCtxSmall4 = 4, kCtxLarge = 8 };
+
+// Launch the partial kernel covering n_ctx_blocks + n_dec_blocks work-groups.
+hipError_t launch_partials(const PartialsParams& P, int d, int ctx_mode, int dec_tiles,
+                           hipStream_t stream);
+hipError_t launch_combine(const CombineParams& C, int d, hipStream_t stream);
+
+}  // namespace bifattn

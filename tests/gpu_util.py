@@ -1,0 +1,80 @@
+"""Helpers for GPU tests: seeded inputs to device, calls through the C ABI."""
+import numpy as np
+
+import paper_2403_08845_amd as bif
+
+
+def to_device(x):
+    import torch
+    out = {}
+    for k in ("q", "Kc", "Vc", "Kd", "Vd"):
+        a = np.ascontiguousarray(x[k]).view(np.int16)
+        out[k] = torch.from_numpy(a).view(torch.bfloat16).cuda()
+    out["lens"] = torch.from_numpy(np.ascontiguousarray(x["lens"], dtype=np.int32)).cuda()
+    return out
+
+
+def dims_of(x):
+    b, h, d = x["q"].shape
+    g, m_c, _ = x["Kc"].shape
+    m_d_max = x["Kd"].shape[2]
+    return b, h, g, d, m_c, m_d_max
+
+
+def run_decode(x, scale=0.0, plan=None, dev=None, check_status=True):
+    """Bifurcated call on seeded numpy inputs; returns fp64 numpy [b,h,d]."""
+    import torch
+    b, h, g, d, m_c, m_d_max = dims_of(x)
+    own = plan is None
+    if own:
+        plan = bif.Plan(b, h, g, d, m_c, m_d_max, scale)
+    try:
+        dev = dev or to_device(x)
+        out = torch.full((b, h, d), float("nan"), dtype=torch.float32, device="cuda")
+        bif.bifattn_decode(plan, dev["q"], dev["Kc"], dev["Vc"], dev["Kd"], dev["Vd"],
+                           dev["lens"], out)
+        st = bif.bifattn_plan_status(plan)
+        if check_status:
+            assert st == bif.OK, bif.status_string(st)
+        return out.cpu().double().numpy()
+    finally:
+        if own:
+            plan.close()
+
+
+def replicate(x):
+    """Physically replicated cache [b, g, m_c + m_d_max, d] (ablation input)."""
+    b, h, g, d, m_c, m_d_max = dims_of(x)
+    K = np.concatenate([np.broadcast_to(x["Kc"][None], (b, g, m_c, d)), x["Kd"]], axis=2)
+    V = np.concatenate([np.broadcast_to(x["Vc"][None], (b, g, m_c, d)), x["Vd"]], axis=2)
+    return np.ascontiguousarray(K), np.ascontiguousarray(V)
+
+
+def run_replicated(x, scale=0.0):
+    import torch
+    b, h, g, d, m_c, m_d_max = dims_of(x)
+    K, V = replicate(x)
+    with bif.Plan(b, h, g, d, m_c, m_d_max, scale) as plan:
+        dev = to_device(x)
+        Kt = torch.from_numpy(K.view(np.int16)).view(torch.bfloat16).cuda()
+        Vt = torch.from_numpy(V.view(np.int16)).view(torch.bfloat16).cuda()
+        out = torch.full((b, h, d), float("nan"), dtype=torch.float32, device="cuda")
+        bif.bifattn_decode_replicated(plan, dev["q"], Kt, Vt, dev["lens"], out)
+        assert bif.bifattn_plan_status(plan) == bif.OK
+        return out.cpu().double().numpy()
+
+
+def sample_rows(b, h, lens, n_random, seed):
+    """Rows (i, j) covering every head of the first, last, longest and
+    shortest sample plus seeded random rows."""
+    rng = np.random.default_rng(seed)
+    lens = np.asarray(lens)
+    samples = sorted({0, b - 1, int(np.argmax(lens)), int(np.argmin(lens))})
+    ri, rj = [], []
+    for i in samples:
+        for j in range(h):
+            ri.append(i)
+            rj.append(j)
+    ri += list(rng.integers(0, b, n_random))
+    rj += list(rng.integers(0, h, n_random))
+    return np.array(ri, np.int32), np.array(rj, np.int32)

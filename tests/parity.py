@@ -3,17 +3,23 @@
 The contract is max |gpu - oracle| <= 1e-2 for bf16 inputs with fp32
 accumulation. That bound alone would accept a kernel that silently drops the
 decode part on long contexts (output entries there are only ~0.005-0.02 in
-size), so every GPU comparison also applies a tighter gate derived from the
-kernel's arithmetic: fp32 logits, softmax statistics and accumulators, with
-the softmax weights rounded to bf16 (relative error <= 2^-9) before the
-weighted sum over values. Summed over m independent keys that rounding gives
-an output error of order 2^-9 * |o| / sqrt(m) per entry, well under 1e-4 for
-these workloads; 2e-3 max-abs and 5e-3 relative L2 leave a wide margin.
+size), so every GPU comparison also applies a relative-L2 gate derived from
+the kernel's arithmetic.
+
+Error model: logits, softmax statistics and accumulators are fp32; the
+softmax weights enter the weighted sum over values rounded to bf16 (relative
+error <= 2^-9 each, independent across keys). The output is a weighted mean
+of value rows with random signs, so those roundings perturb it by about
+2^-9/sqrt(3) ~ 1.1e-3 of its own norm (measured: 1.1e-3 to 1.7e-3 relative
+L2 on every workload); fp32 summation adds orders of magnitude less. The
+gate allows 5e-3 relative L2. Per entry the same rounding is bounded by
+2^-9 * max_t |v_t| (~1e-2 for N(0,1) values), but few-key rows with O(1)
+outputs reach ~2e-3 in practice, so the max-abs gate is 5e-3.
 """
 import numpy as np
 
 CONTRACT_MAX_ABS = 1e-2
-GATE_MAX_ABS = 2e-3
+GATE_MAX_ABS = 5e-3
 GATE_REL_L2 = 5e-3
 
 

@@ -1,0 +1,159 @@
+"""GPU parity: bifattn_decode (through the C ABI) against the fp64 oracle on
+the same seeded inputs, element by element (MI355X only)."""
+import numpy as np
+import pytest
+
+import oracle
+import paper_2403_08845_amd as bif
+import workloads
+
+from .gpu_util import dims_of, run_decode, run_replicated, sample_rows, to_device
+from .parity import assert_parity
+
+pytestmark = pytest.mark.gpu
+
+
+def _report(name, max_abs, rel):
+    print(f"[parity] {name}: max_abs={max_abs:.3e} rel_l2={rel:.3e}", flush=True)
+
+
+# Shapes the oracle finishes in seconds that span several tiles, ragged tails
+# (lengths not multiples of the 32-key tile or of a work-group's key chunk),
+# both head dims, multi-head / grouped / multi-query, the many-row context
+# path, context-only samples and a single context key.
+SMALL_CASES = [
+    # b, h, g, d, m_c, m_d_max, ragged
+    (4, 4, 4, 64, 128, 16, False),
+    (3, 8, 8, 128, 1000, 77, True),
+    (2, 8, 2, 128, 333, 200, True),
+    (5, 16, 1, 64, 517, 45, True),        # MQA, p = 16, M = 80 -> many-row context path
+    (1, 32, 32, 128, 4096, 300, True),    # b = 1
+    (7, 32, 8, 128, 700, 129, True),      # GQA p = 4, M = 28
+    (9, 64, 1, 128, 257, 33, True),       # MQA p = 64 (four query tiles per decode wave)
+    (3, 6, 3, 64, 1, 3, True),            # single context key
+    (2, 4, 2, 128, 96, 0, False),         # no decode cache
+    (40, 32, 1, 128, 2000, 64, True),     # M = 1280 -> 5 row blocks, ragged last block
+]
+
+
+@pytest.mark.parametrize("case", SMALL_CASES, ids=lambda c: "b%d_h%d_g%d_d%d_mc%d_md%d" % c[:6])
+def test_small_shapes_full_output(case):
+    b, h, g, d, m_c, m_d, ragged = case
+    x = workloads.make_inputs(b, h, g, d, m_c, m_d, seed=500 + m_c, ragged=ragged)
+    if ragged and b >= 3 and m_d > 0:
+        x["lens"][1] = 0          # a context-only sample
+        x["lens"][-1] = m_d       # a full one
+    print(f"[case] {case} lens={x['lens'].tolist()[:8]}", flush=True)
+    out = run_decode(x)
+    ref = oracle.attention(**x)
+    _report(str(case), *assert_parity(out, ref, str(case)))
+
+
+@pytest.mark.parametrize("name", workloads.WORKLOAD_ORDER[:2])
+def test_workload_full_output(name):
+    w = workloads.WORKLOADS[name]
+    x = workloads.make_workload_inputs(w)
+    print(f"[case] {name}", flush=True)
+    out = run_decode(x)
+    ref = oracle.attention(**x)
+    _report(name, *assert_parity(out, ref, name))
+
+
+@pytest.mark.parametrize("name", workloads.WORKLOAD_ORDER[2:])
+def test_workload_sampled_rows(name):
+    """Full-size workloads in the benchmark's configuration: every output is
+    finite, and sampled rows match the oracle computed row by row."""
+    w = workloads.WORKLOADS[name]
+    x = workloads.make_workload_inputs(w)
+    print(f"[case] {name} sum(lens)={int(x['lens'].sum())}", flush=True)
+    out = run_decode(x)
+    assert np.all(np.isfinite(out))
+    ri, rj = sample_rows(w.b, w.h, x["lens"], 48, seed=w.seed)
+    ref = oracle.attention_rows(**x, rows_i=ri, rows_j=rj)
+    _report(name, *assert_parity(out[ri, rj], ref, name))
+
+
+def test_masked_tail_is_never_read():
+    """NaN in decode rows past each sample's length changes no output bit."""
+    b, h, g, d, m_c, m_d = 6, 16, 4, 128, 300, 150
+    x = workloads.make_inputs(b, h, g, d, m_c, m_d, seed=71, ragged=True)
+    y = workloads.make_inputs(b, h, g, d, m_c, m_d, seed=71, ragged=True, poison_tail=True)
+    a = run_decode(x)
+    c = run_decode(y)
+    assert np.array_equal(a, c)
+
+
+def test_deterministic_and_plan_reuse():
+    b, h, g, d, m_c, m_d = 5, 32, 32, 128, 1500, 100
+    x = workloads.make_inputs(b, h, g, d, m_c, m_d, seed=72, ragged=True)
+    with bif.Plan(b, h, g, d, m_c, m_d) as plan:
+        dev = to_device(x)
+        a = run_decode(x, plan=plan, dev=dev)
+        c = run_decode(x, plan=plan, dev=dev)
+    assert np.array_equal(a, c)
+
+
+def test_b1_equivalence_on_gpu():
+    """Row i of a batched call equals a b = 1 call on sample i."""
+    b, h, g, d, m_c, m_d = 4, 8, 2, 128, 640, 90
+    x = workloads.make_inputs(b, h, g, d, m_c, m_d, seed=73, ragged=True)
+    full = run_decode(x)
+    for i in range(b):
+        one = {k: x[k] for k in ("Kc", "Vc")}
+        one.update(q=x["q"][i:i + 1], Kd=x["Kd"][i:i + 1], Vd=x["Vd"][i:i + 1],
+                   lens=x["lens"][i:i + 1])
+        single = run_decode(one)
+        assert_parity(single[0], full[i], f"b=1 sample {i}")
+
+
+def test_explicit_scale():
+    b, h, g, d, m_c, m_d = 3, 8, 4, 64, 200, 40
+    x = workloads.make_inputs(b, h, g, d, m_c, m_d, seed=74, ragged=True)
+    out = run_decode(x, scale=0.05)
+    ref = oracle.attention(**x, scale=0.05)
+    assert_parity(out, ref, "scale 0.05")
+
+
+def test_out_of_range_lengths_are_clamped_and_flagged():
+    import torch
+    b, h, g, d, m_c, m_d = 3, 4, 2, 128, 64, 40
+    x = workloads.make_inputs(b, h, g, d, m_c, m_d, seed=75)
+    bad = dict(x)
+    bad["lens"] = np.array([50, -3, 17], np.int32)
+    with bif.Plan(b, h, g, d, m_c, m_d) as plan:
+        dev = to_device(bad)
+        out = torch.empty((b, h, d), dtype=torch.float32, device="cuda")
+        bif.bifattn_decode(plan, dev["q"], dev["Kc"], dev["Vc"], dev["Kd"], dev["Vd"],
+                           dev["lens"], out)
+        assert bif.bifattn_plan_status(plan) == bif.ELENS
+        assert bif.bifattn_plan_status(plan) == bif.OK  # flag cleared
+        got = out.cpu().double().numpy()
+    clamped = dict(x)
+    clamped["lens"] = np.array([40, 0, 17], np.int32)
+    assert_parity(got, oracle.attention(**clamped), "clamped lengths")
+
+
+@pytest.mark.parametrize("case", [(4, 4, 4, 64, 128, 16, False), (3, 16, 4, 128, 700, 90, True),
+                                  (6, 32, 1, 128, 300, 64, True)],
+                         ids=lambda c: "b%d_h%d_g%d_d%d_mc%d_md%d" % c[:6])
+def test_replicated_ablation_matches_oracle(case):
+    b, h, g, d, m_c, m_d, ragged = case
+    x = workloads.make_inputs(b, h, g, d, m_c, m_d, seed=76, ragged=ragged)
+    out = run_replicated(x)
+    assert_parity(out, oracle.attention(**x), f"replicated {case}")
+
+
+def test_timing_api_counts_calls():
+    import torch
+    b, h, g, d, m_c, m_d = 4, 32, 32, 128, 2048, 128
+    x = workloads.make_inputs(b, h, g, d, m_c, m_d, seed=77)
+    with bif.Plan(b, h, g, d, m_c, m_d) as plan:
+        dev = to_device(x)
+        out = torch.empty((b, h, d), dtype=torch.float32, device="cuda")
+        bif.bifattn_plan_set_timing(plan, bif.KERNEL_PARTIALS, 3)
+        for _ in range(5):
+            bif.bifattn_decode(plan, dev["q"], dev["Kc"], dev["Vc"], dev["Kd"], dev["Vd"],
+                               dev["lens"], out)
+        n, ms = bif.bifattn_plan_read_timing(plan)
+        assert n == 3 and 0 < ms < 1000
+        bif.bifattn_plan_set_timing(plan, bif.KERNEL_PARTIALS, 0)
