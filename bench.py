@@ -1,0 +1,241 @@
+#!/usr/bin/env python3
+"""Benchmark: one bifurcated decode-attention step per timed step on MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
+
+A step is one bifattn_decode call (context partials, decode partials and the
+combine) over one batch of seeded synthetic inputs that are already resident
+in HBM. Steps rotate over several device copies of the inputs (about 1.2 GB
+or more in total) so that no step finds its KV cache in the 256 MB Infinity
+Cache left behind by the previous one. The timed region is bracketed by
+torch.cuda.synchronize() on both sides.
+
+Prints ONE JSON line: value = algorithmic KV bytes per step (one copy of the
+context K/V plus every sample's valid decode K/V, Section 4.3) divided by the
+measured time per step, in GB/s. ``roofline`` reports the partial kernel
+(the dominant launch) against the 8 TB/s HBM peak, its duration measured with
+HIP events recorded by the library around that launch on its stream, over a
+second pass of the same steps (events are kept out of the value loop because
+each record costs GPU time between kernels). ``cpu_baseline`` times the fp64 CPU oracle on the host on the same
+workload. ``ablation`` times the replicated-KV kernel (no bifurcation).
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+import numpy as np  # noqa: E402
+
+import workloads  # noqa: E402
+
+METRIC = ("decode-step attention µs and achieved HBM GB/s (% of peak), "
+          "b=32 m_c=8k MHA")
+HBM_PEAK_GBS = 8000.0
+MALL_BYTES = 256 << 20
+KERNEL_SRC = os.path.join(ROOT, "paper_2403_08845_amd", "csrc", "bifattn_kernels.hip")
+TRAFFIC_DIR = os.path.join(ROOT, "profiles")
+
+
+def log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+def kernel_source_hash() -> str:
+    return hashlib.sha256(open(KERNEL_SRC, "rb").read()).hexdigest()[:16]
+
+
+def measured_traffic(workload: str):
+    """HBM bytes per launch of the partial kernel from the committed rocprofv3
+    counter summary, or None when it is missing or the kernel source changed
+    since the counters were taken."""
+    path = os.path.join(TRAFFIC_DIR, f"traffic_partials_{workload}.json")
+    if not os.path.exists(path):
+        return None
+    rec = json.load(open(path))
+    if rec.get("kernel_source_sha256_16") != kernel_source_hash():
+        return None
+    return rec.get("hbm_bytes_per_launch")
+
+
+def to_device(x):
+    import torch
+    out = {}
+    for k in ("q", "Kc", "Vc", "Kd", "Vd"):
+        out[k] = torch.from_numpy(np.ascontiguousarray(x[k]).view(np.int16)).view(torch.bfloat16).cuda()
+    out["lens"] = torch.from_numpy(np.ascontiguousarray(x["lens"], dtype=np.int32)).cuda()
+    return out
+
+
+def cpu_baseline(x, w, min_seconds):
+    """The fp64 oracle on the host's cores, repeated over the whole workload
+    until min_seconds have elapsed (at least once)."""
+    import oracle
+    threads = oracle.max_threads()
+    reps, t0 = 0, time.perf_counter()
+    while True:
+        oracle.attention(**x)
+        reps += 1
+        el = time.perf_counter() - t0
+        if el >= min_seconds:
+            break
+    per = el / reps
+    B = workloads.kv_bytes(w.g, w.d, w.m_c, x["lens"])
+    return {"value": round(B / per / 1e9, 4), "unit": "GB/s", "cores": threads, "kind": "oracle",
+            "sample": f"whole {w.name} step (b={w.b}), fp64, repeated {reps}x over {el:.1f} s; "
+                      f"{per * 1e3:.1f} ms per step"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--workload", default=workloads.HEADLINE, choices=workloads.WORKLOAD_ORDER)
+    ap.add_argument("--cpu-seconds", type=float, default=10.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-ablation", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU: the bifurcated decode step runs on a single MI355X "
+              "(see DESIGN.md for how it would shard); --gpus must be 1.", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import paper_2403_08845_amd as bif
+
+    w = workloads.WORKLOADS[args.workload]
+    log(f"[bench] generating {w.name}")
+    x = workloads.make_workload_inputs(w)
+    B_kv = workloads.kv_bytes(w.g, w.d, w.m_c, x["lens"])
+    flops = workloads.attention_flops(w.h, w.d, w.b, w.m_c, x["lens"])
+    torch.cuda.set_device(0)
+    dev0 = to_device(x)
+    # Rotate over device copies so each step's KV is cold in the Infinity Cache.
+    copies = max(3, -(-4 * MALL_BYTES // B_kv))
+    devs = [dev0] + [{k: v.clone() for k, v in dev0.items()} for _ in range(copies - 1)]
+    out = torch.empty((w.b, w.h, w.d), dtype=torch.float32, device="cuda")
+    plan = bif.Plan(w.b, w.h, w.g, w.d, w.m_c, w.m_d_max)
+    info = plan.info()
+    log(f"[bench] plan {info}, {copies} input copies")
+
+    def step(k):
+        d = devs[k % copies]
+        bif.bifattn_decode(plan, d["q"], d["Kc"], d["Vc"], d["Kd"], d["Vd"], d["lens"], out)
+
+    for k in range(args.warmup):
+        step(k)
+    torch.cuda.synchronize()
+    assert bif.bifattn_plan_status(plan) == bif.OK
+    log(f"[bench] warmup done ({args.warmup} steps)")
+
+    # Timed region (value, ms_per_step): plain back-to-back steps.
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for k in range(args.steps):
+        step(k)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    ms_per_step = elapsed * 1e3 / args.steps
+    # Kernel timing (roofline): the same steps again, with the library
+    # recording HIP events on the launch stream around its partial kernel in
+    # every step. Kept out of the loop above because each event record costs
+    # a few microseconds of GPU time between kernels.
+    bif.bifattn_plan_set_timing(plan, bif.KERNEL_PARTIALS, args.steps)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for k in range(args.steps):
+        step(k)
+    torch.cuda.synchronize()
+    evt_loop_us = (time.perf_counter() - t0) * 1e6 / args.steps
+    n_timed, part_ms = bif.bifattn_plan_read_timing(plan)
+    bif.bifattn_plan_set_timing(plan, bif.KERNEL_PARTIALS, 0)
+    assert n_timed == args.steps
+    part_us = part_ms * 1e3 / n_timed
+    log(f"[bench] timed {args.steps} steps: {ms_per_step * 1e3:.2f} us/step, "
+        f"partial kernel {part_us:.2f} us (event loop {evt_loop_us:.2f} us/step)")
+
+    # Warm variant (same inputs every step: KV partly served by the Infinity Cache).
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step(0)
+    torch.cuda.synchronize()
+    warm_us = (time.perf_counter() - t0) * 1e6 / args.steps
+
+    extra = {"warm_us_per_step": round(warm_us, 3), "event_loop_us_per_step": round(evt_loop_us, 3),
+             "plan": info, "input_copies": copies,
+             "kv_bytes_per_step": B_kv, "flops_per_step": flops}
+
+    ablation = None
+    if not args.no_ablation:
+        # Replicated cache built on the device: every sample's own copy of the context.
+        rows = w.m_c + w.m_d_max
+        rep_bytes = 2 * w.b * w.g * rows * w.d * 2
+        if rep_bytes < 40e9:
+            K = torch.cat([dev0["Kc"].unsqueeze(0).expand(w.b, -1, -1, -1), dev0["Kd"]], dim=2).contiguous()
+            V = torch.cat([dev0["Vc"].unsqueeze(0).expand(w.b, -1, -1, -1), dev0["Vd"]], dim=2).contiguous()
+            ref_out = out.clone()
+            bif.bifattn_decode_replicated(plan, dev0["q"], K, V, dev0["lens"], out)
+            torch.cuda.synchronize()
+            rep_steps = max(5, args.steps // 10)
+            t0 = time.perf_counter()
+            for _ in range(rep_steps):
+                bif.bifattn_decode_replicated(plan, dev0["q"], K, V, dev0["lens"], out)
+            torch.cuda.synchronize()
+            rep_us = (time.perf_counter() - t0) * 1e6 / rep_steps
+            B_rep = workloads.replicated_kv_bytes(w.b, w.g, w.d, w.m_c, x["lens"])
+            step(0)
+            torch.cuda.synchronize()
+            ablation = {"kernel": "bifattn_decode_replicated", "us_per_step": round(rep_us, 3),
+                        "kv_bytes_per_step": B_rep,
+                        "GBps": round(B_rep / (rep_us * 1e-6) / 1e9, 1),
+                        "speedup_of_bifurcation": round(rep_us / (ms_per_step * 1e3), 3)}
+            del K, V, ref_out
+    plan.close()
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        log("[bench] timing the CPU oracle")
+        cpu = cpu_baseline(x, w, args.cpu_seconds)
+
+    value = B_kv / (ms_per_step * 1e-3) / 1e9
+    achieved = B_kv / (part_us * 1e-6) / 1e9
+    traffic = measured_traffic(w.name)
+    rec = {
+        "metric": METRIC,
+        "value": round(value, 1),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 6),
+        "us_per_step": round(ms_per_step * 1e3, 3),
+        "pct_of_hbm_peak": round(100 * value / HBM_PEAK_GBS, 2),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": w.name, "b": w.b, "h": w.h, "g": w.g, "d": w.d, "m_c": w.m_c,
+                   "m_d": w.m_d_max, "decode_lens": "ragged" if w.ragged else "uniform",
+                   "parallelism": "single GPU"},
+        "roofline": {"kernel": "partials_kernel (context + decode partials)", "bound": "hbm",
+                     "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
+                     "avg_launch_us": round(part_us, 3)},
+        "cpu_baseline": cpu,
+        "ablation": ablation,
+        "extra": extra,
+    }
+    print(json.dumps(rec), flush=True)
+
+
+if __name__ == "__main__":
+    main()

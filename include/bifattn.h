@@ -87,7 +87,7 @@ typedef struct {
   int32_t ctx_row_blocks;     /* work-groups sharing one context key chunk */
   int32_t ctx_blocks;         /* context work-groups per call */
   int32_t dec_keys_per_block; /* decode keys one work-group reads */
-  int32_t dec_splits;         /* S_d: max decode partial results per output row */
+  int32_t dec_splits;         /* decode partial results per output row */
   int32_t dec_blocks;         /* decode work-groups per call */
   int32_t fused;              /* 1: context and decode parts in one launch */
   size_t workspace_bytes;     /* device memory the plan owns */

@@ -42,8 +42,8 @@ class PlanInfo(ctypes.Structure):
     _fields_ = [("ctx_keys_per_block", ctypes.c_int32), ("ctx_splits", ctypes.c_int32),
                 ("ctx_row_blocks", ctypes.c_int32), ("ctx_blocks", ctypes.c_int32),
                 ("dec_keys_per_block", ctypes.c_int32), ("dec_splits", ctypes.c_int32),
-                ("dec_blocks", ctypes.c_int32), ("fused", ctypes.c_int32),
-                ("workspace_bytes", ctypes.c_size_t)]
+                ("dec_blocks", ctypes.c_int32),
+                ("fused", ctypes.c_int32), ("workspace_bytes", ctypes.c_size_t)]
 
     def as_dict(self):
         return {name: getattr(self, name) for name, _ in self._fields_}

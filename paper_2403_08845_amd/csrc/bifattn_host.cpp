@@ -20,7 +20,7 @@ struct bifattn_plan_s {
   int p = 0, M = 0;
   int ctx_mode = kCtxNone;
   int dec_tiles = 1;
-  int ctx_keys = 0, S_c = 0, ctx_row_blocks = 1, n_ctx_blocks = 0;
+  int ctx_keys = 0, S_c = 0, ctx_row_blocks = 1, n_ctx_blocks = 0, n_ctx_small_blocks = 0;
   int dec_keys = 0, S_d = 0, n_dec_blocks = 0;
   int rep_keys = 0, S_r = 0, n_rep_blocks = 0;
   int fused = 1;
@@ -59,11 +59,11 @@ int env_int(const char* name, int fallback) {
 
 bool aligned(const void* ptr, uintptr_t a) { return ((uintptr_t)ptr & (a - 1)) == 0; }
 
-// Keys one decode (or replicated) work-group reads: 512 keys by default,
-// halved (down to 128) while fewer than 4 work-groups per CU would exist.
-int pick_seq_keys(int64_t units, int rows, int start) {
+// Keys one decode (or replicated) work-group reads: `start` by default,
+// halved (down to 128) while fewer than two work-groups per CU would exist.
+int seq_keys(int64_t units, int64_t rows, int start) {
   int keys = start;
-  while (keys > 128 && units * ceil_div(rows, keys) < 4 * kCUs) keys /= 2;
+  while (keys > 128 && units * ceil_div(rows, keys) < 2 * kCUs) keys /= 2;
   return keys;
 }
 
@@ -73,48 +73,48 @@ bifattn_status_t plan_splits(bifattn_plan_s* P) {
   P->M = d.b * P->p;
   P->dec_tiles = P->p <= 16 ? 1 : (P->p <= 32 ? 2 : 4);
   const int64_t M = P->M;
+  const int64_t units = (int64_t)d.b * d.g;
   if (M <= 64) {
+    // Few rows per group: S_c work-groups per group, interleaved over the
+    // group's tiles; 1024 keys each by default (twice a decode work-group).
     P->ctx_mode = M <= 16 ? kCtxSmall1 : (M <= 32 ? kCtxSmall2 : kCtxSmall4);
-    // About one context work-group per CU, each a multiple of 4 waves x 32 keys.
-    int64_t keys = round_up(ceil_div((int64_t)d.g * d.m_c, kCUs), kWaves * kTileKeys);
-    keys = env_int("BIFATTN_CTX_KEYS", (int)keys);
-    keys = round_up(keys, kWaves * kTileKeys);
-    if (keys > round_up(d.m_c, kWaves * kTileKeys)) keys = round_up(d.m_c, kWaves * kTileKeys);
-    P->ctx_keys = (int)keys;
+    const int keys = (int)round_up(env_int("BIFATTN_CTX_KEYS", 1024), kWaves * kTileKeys);
+    P->ctx_keys = keys;
     P->ctx_row_blocks = 1;
   } else {
+    // Many rows: work-groups of 256 rows share each staged K_c/V_c tile;
+    // about one work-group per CU.
     P->ctx_mode = kCtxLarge;
     P->ctx_row_blocks = (int)ceil_div(M, kLargeRowsPerBlock);
     int64_t splits = ceil_div(kCUs, (int64_t)d.g * P->ctx_row_blocks);
     if (splits < 1) splits = 1;
-    int64_t keys = round_up(ceil_div(d.m_c, splits), kTileKeys);
-    keys = env_int("BIFATTN_CTX_KEYS", (int)keys);
-    keys = round_up(keys, kTileKeys);
-    P->ctx_keys = (int)keys;
+    const int64_t ck = round_up(ceil_div(d.m_c, splits), kTileKeys);
+    P->ctx_keys = (int)round_up(env_int("BIFATTN_CTX_KEYS", (int)ck), kTileKeys);
   }
   P->S_c = (int)ceil_div(d.m_c, P->ctx_keys);
-  P->n_ctx_blocks = d.g * P->S_c * P->ctx_row_blocks;
-  const int64_t units = (int64_t)d.b * d.g;
+  P->n_ctx_blocks = P->ctx_mode == kCtxLarge ? d.g * P->S_c * P->ctx_row_blocks : 0;
+  P->n_ctx_small_blocks = P->ctx_mode == kCtxLarge ? 0 : d.g * P->S_c;
   if (d.m_d_max > 0) {
-    P->dec_keys = env_int("BIFATTN_DEC_KEYS", pick_seq_keys(units, d.m_d_max, 512));
-    P->dec_keys = (int)round_up(P->dec_keys, kTileKeys);
+    P->dec_keys = (int)round_up(env_int("BIFATTN_DEC_KEYS", seq_keys(units, d.m_d_max, 512)),
+                                kTileKeys);
     P->S_d = (int)ceil_div(d.m_d_max, P->dec_keys);
   } else {
-    P->dec_keys = kWaves * kTileKeys;
+    P->dec_keys = kTileKeys;
     P->S_d = 0;
   }
   P->n_dec_blocks = (int)(units * P->S_d);
-  const int rep_rows = d.m_c + d.m_d_max;
-  P->rep_keys = env_int("BIFATTN_REP_KEYS", pick_seq_keys(units, rep_rows, 1024));
-  P->rep_keys = (int)round_up(P->rep_keys, kTileKeys);
+  const int64_t rep_rows = (int64_t)d.m_c + d.m_d_max;
+  P->rep_keys = (int)round_up(env_int("BIFATTN_REP_KEYS", seq_keys(units, rep_rows, 1024)),
+                              kTileKeys);
   P->S_r = (int)ceil_div(rep_rows, P->rep_keys);
   P->n_rep_blocks = (int)(units * P->S_r);
-  // One launch for both parts when their work-groups have the same register
+  // One launch for both parts when their waves have the same register
   // footprint; the many-row context path runs as its own launch.
   // BIFATTN_LAUNCH=1 forces one launch, 2 forces two.
   const int launch = env_int("BIFATTN_LAUNCH", P->ctx_mode == kCtxLarge ? 2 : 1);
   P->fused = launch == 1 ? 1 : 0;
-  if ((int64_t)P->n_ctx_blocks + P->n_dec_blocks > INT32_MAX / 2 || units * P->S_r > INT32_MAX / 2)
+  if ((int64_t)P->n_ctx_blocks + P->n_ctx_small_blocks + P->n_dec_blocks > INT32_MAX / 2 ||
+      units * P->S_r > INT32_MAX / 2)
     return BIFATTN_EINVAL;
   return BIFATTN_OK;
 }
@@ -241,7 +241,8 @@ bifattn_status_t bifattn_plan_create(const bifattn_dims_t* dims, bifattn_plan_t*
   const bifattn_dims_t& d = P->dims;
   const size_t D = (size_t)d.d;
   const size_t ctx_rows = (size_t)d.g * P->S_c * P->M;
-  const size_t dec_rows = (size_t)d.b * d.g * (size_t)(P->S_d > P->S_r ? P->S_d : P->S_r) * P->p;
+  const size_t dec_rows =
+      (size_t)d.b * d.g * (size_t)(P->S_d > P->S_r ? P->S_d : P->S_r) * kWaves * P->p;
   size_t off = 0;
   const size_t o_ctx_acc = off;
   off = align256(off + ctx_rows * D * 4);
@@ -289,9 +290,9 @@ bifattn_status_t bifattn_plan_get_info(bifattn_plan_t P, bifattn_plan_info_t* in
   info->ctx_keys_per_block = P->ctx_keys;
   info->ctx_splits = P->S_c;
   info->ctx_row_blocks = P->ctx_row_blocks;
-  info->ctx_blocks = P->n_ctx_blocks;
+  info->ctx_blocks = P->n_ctx_blocks + P->n_ctx_small_blocks;
   info->dec_keys_per_block = P->dec_keys;
-  info->dec_splits = P->S_d;
+  info->dec_splits = P->S_d * kWaves;
   info->dec_blocks = P->n_dec_blocks;
   info->fused = P->fused;
   info->workspace_bytes = P->ws_bytes;
@@ -323,16 +324,17 @@ bifattn_status_t bifattn_decode(bifattn_plan_t P, const void* q, const void* Kc,
   TimedSection whole(P, BIFATTN_KERNEL_CALL, stream);
   TimedSection part(P, BIFATTN_KERNEL_PARTIALS, stream);
   hipError_t e;
+  K.n_ctx_blocks = P->n_ctx_blocks;
+  K.n_ctx_small_blocks = P->n_ctx_small_blocks;
   if (P->fused) {
-    K.n_ctx_blocks = P->n_ctx_blocks;
     K.n_dec_blocks = P->n_dec_blocks;
     e = launch_partials(K, P->dims.d, P->ctx_mode, P->dec_tiles, stream);
   } else {
-    K.n_ctx_blocks = P->n_ctx_blocks;
     K.n_dec_blocks = 0;
     e = launch_partials(K, P->dims.d, P->ctx_mode, P->dec_tiles, stream);
     if (e == hipSuccess && P->n_dec_blocks) {
       K.n_ctx_blocks = 0;
+      K.n_ctx_small_blocks = 0;
       K.n_dec_blocks = P->n_dec_blocks;
       e = launch_partials(K, P->dims.d, kCtxNone, P->dec_tiles, stream);
     }
@@ -341,10 +343,8 @@ bifattn_status_t bifattn_decode(bifattn_plan_t P, const void* q, const void* Kc,
   if (e != hipSuccess) return BIFATTN_EHIP;
   TimedSection comb(P, BIFATTN_KERNEL_COMBINE, stream);
   CombineParams C = combine_params(P, has_dec ? decode_lens : nullptr, out);
-  C.len_offset = 0;
   C.S_c = P->S_c;
-  C.dec_keys = P->dec_keys;
-  C.S_d = P->S_d;
+  C.S_d = P->S_d * kWaves;
   e = launch_combine(C, P->dims.d, stream);
   comb.end();
   whole.end();
@@ -369,6 +369,7 @@ bifattn_status_t bifattn_decode_replicated(bifattn_plan_t P, const void* q, cons
   K.S_d = P->S_r;
   K.S_c = 0;
   K.n_ctx_blocks = 0;
+  K.n_ctx_small_blocks = 0;
   K.n_dec_blocks = P->n_rep_blocks;
   TimedSection whole(P, BIFATTN_KERNEL_CALL, stream);
   TimedSection part(P, BIFATTN_KERNEL_PARTIALS, stream);
@@ -377,10 +378,8 @@ bifattn_status_t bifattn_decode_replicated(bifattn_plan_t P, const void* q, cons
   if (e != hipSuccess) return BIFATTN_EHIP;
   TimedSection comb(P, BIFATTN_KERNEL_COMBINE, stream);
   CombineParams C = combine_params(P, has_dec ? decode_lens : nullptr, out);
-  C.len_offset = P->dims.m_c;
   C.S_c = 0;
-  C.dec_keys = P->rep_keys;
-  C.S_d = P->S_r;
+  C.S_d = P->S_r * kWaves;
   e = launch_combine(C, P->dims.d, stream);
   comb.end();
   whole.end();

@@ -40,21 +40,22 @@ struct PartialsParams {
   const int32_t* lens;
   float* ctx_acc;         // [g][S_c][M][d]
   float2* ctx_ml;         // [g][S_c][M]
-  float* dec_acc;         // [b][g][S_d][p][d]
-  float2* dec_ml;         // [b][g][S_d][p]
+  float* dec_acc;         // [b][g][S_d][4 waves][p][d]
+  float2* dec_ml;         // [b][g][S_d][4 waves][p]
   int* status;
   int b, h, g, p, M;      // M = b*p query rows per group
   int m_c;
   int m_d_max;            // clamp bound for lens
   int dec_rows;           // row capacity of one (sample, group) decode cache
   int len_offset;         // rows before the decode rows in that cache (0, or m_c in ablation)
-  int ctx_keys;           // keys per context work-group
+  int ctx_keys;           // keys per context work-group (many-row path)
   int S_c;
   int ctx_row_blocks;
   int dec_keys;           // keys per decode work-group
   int S_d;
-  int n_ctx_blocks;
-  int n_dec_blocks;
+  int n_ctx_blocks;       // work-groups of the many-row context path
+  int n_ctx_small_blocks; // work-groups of the few-row context path (g * S_c)
+  int n_dec_blocks;       // decode work-groups (b * g * S_d); 4 partials each
   float scale_log2;       // scale * log2(e)
 };
 
@@ -68,15 +69,14 @@ struct CombineParams {
   int* status;
   int b, h, g, p, M;
   int m_d_max;
-  int len_offset;
   int S_c;
-  int dec_keys;
   int S_d;
 };
 
 enum CtxMode { kCtxNone = 0, kCtxSmall1 = 1, kCtxSmall2 = 2, kCtxSmall4 = 4, kCtxLarge = 8 };
 
-// Launch the partial kernel covering n_ctx_blocks + n_dec_blocks work-groups.
+// Launch the partial kernel over n_ctx_blocks + n_ctx_small_blocks +
+// n_dec_blocks work-groups.
 hipError_t launch_partials(const PartialsParams& P, int d, int ctx_mode, int dec_tiles,
                            hipStream_t stream);
 hipError_t launch_combine(const CombineParams& C, int d, hipStream_t stream);

@@ -35,6 +35,7 @@ typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef __attribute__((address_space(3))) u32x4 lds_u32x4;  // LDS-qualified operand slot
 
 constexpr float kNegInf = -__builtin_inff();
 
@@ -50,6 +51,12 @@ __device__ __forceinline__ uint32_t pack_bf16(float lo, float hi) {
 
 __device__ __forceinline__ float exp2_fast(float x) { return __builtin_amdgcn_exp2f(x); }
 
+// Wave index within the work-group, as a wave-uniform (scalar) value so that
+// branches on it and on tile bounds derived from it stay scalar.
+__device__ __forceinline__ int wave_id() {
+  return __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+}
+
 // Value row slice a lane loads: DV consecutive bf16 (16 B for d=128, 8 B for d=64).
 template <int D> struct VSlice;
 template <> struct VSlice<128> {
@@ -58,6 +65,9 @@ template <> struct VSlice<128> {
     return *reinterpret_cast<const u32x4*>(p);
   }
   static __device__ __forceinline__ type zero() { return u32x4{0, 0, 0, 0}; }
+  static __device__ __forceinline__ type load_buf(__amdgpu_buffer_rsrc_t r, int off) {
+    return __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0);
+  }
 };
 template <> struct VSlice<64> {
   typedef u32x2 type;
@@ -65,6 +75,9 @@ template <> struct VSlice<64> {
     return *reinterpret_cast<const u32x2*>(p);
   }
   static __device__ __forceinline__ type zero() { return u32x2{0, 0}; }
+  static __device__ __forceinline__ type load_buf(__amdgpu_buffer_rsrc_t r, int off) {
+    return __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, 0);
+  }
 };
 
 __device__ __forceinline__ u32x4 load16(const uint16_t* p) {
@@ -102,23 +115,26 @@ template <int D, int NT> struct RowState {
 };
 
 // One 32-key tile against NT query tiles: S^T = K Q^T on MFMA, online softmax
-// with lazy rescaling, O^T += V^T P^T on MFMA. kop/vop are this lane's K and
-// V^T operands, qop[nt][s] the Q^T operands. Keys >= nvalid are masked.
-template <int D, int NT>
+// with lazy rescaling, O^T += V^T P^T on MFMA. kop are this lane's K
+// operands, vop_at(t) yields its V^T operand of dimension block t (built on
+// demand, so only one is live at a time), q_at(nt, s) its Q^T operands. Keys
+// >= nvalid are masked.
+template <int D, int NT, typename VOp, typename QOp>
 __device__ __forceinline__ void tile_update(RowState<D, NT>& st, const u32x4 (&kop)[2][D / 32],
-                                            const u32x4 (&vop)[D / 16],
-                                            const u32x4 (&qop)[NT][D / 32], int nvalid,
+                                            VOp&& vop_at, QOp&& q_at, int nvalid,
                                             float scale_log2, int lane) {
   constexpr int KS = D / 32;
   constexpr int DV = D / 16;
   const int G = lane >> 4;
+  u32x4 pb[NT];
 #pragma unroll
   for (int nt = 0; nt < NT; ++nt) {
     f32x4 s0 = {0.f, 0.f, 0.f, 0.f}, s1 = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int s = 0; s < KS; ++s) {
-      s0 = mfma_bf16(kop[0][s], qop[nt][s], s0);
-      s1 = mfma_bf16(kop[1][s], qop[nt][s], s1);
+      const u32x4 qo = q_at(nt, s);
+      s0 = mfma_bf16(kop[0][s], qo, s0);
+      s1 = mfma_bf16(kop[1][s], qo, s1);
     }
     float x[8];
 #pragma unroll
@@ -154,11 +170,14 @@ __device__ __forceinline__ void tile_update(RowState<D, NT>& st, const u32x4 (&k
       psum += pr[e];
     }
     st.l[nt] += psum;
-    u32x4 pb;
 #pragma unroll
-    for (int w = 0; w < 4; ++w) pb[w] = pack_bf16(pr[2 * w], pr[2 * w + 1]);
+    for (int w = 0; w < 4; ++w) pb[nt][w] = pack_bf16(pr[2 * w], pr[2 * w + 1]);
+  }
 #pragma unroll
-    for (int t = 0; t < DV; ++t) st.acc[nt][t] = mfma_bf16(vop[t], pb, st.acc[nt][t]);
+  for (int t = 0; t < DV; ++t) {
+    const u32x4 v = vop_at(t);
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) st.acc[nt][t] = mfma_bf16(v, pb[nt], st.acc[nt][t]);
   }
 }
 
@@ -176,44 +195,45 @@ __device__ __forceinline__ void load_q(u32x4 (&qop)[NT][D / 32], RowPtr row_ptr,
   }
 }
 
-// Register path: one wave loads a whole 32-key tile into its own operands.
-template <int D>
-__device__ __forceinline__ void load_tile_regs(u32x4 (&kop)[2][D / 32], u32x4 (&vop)[D / 16],
-                                               const uint16_t* K, const uint16_t* V, int nvalid,
-                                               int lane) {
-  constexpr int KS = D / 32;
-  constexpr int DV = D / 16;
+// Register path: one wave loads a whole 32-key tile into its own registers:
+// K operands directly, value rows raw (lane (r, G) holds keys 8G..8G+7 at
+// dims DV*r .. DV*r+DV-1); V^T operands are formed from them on demand.
+// Loads go through buffer resources whose range ends at the item's last key,
+// so rows past it read as zero without a branch and without a memory access.
+template <int D> struct TileRegs {
+  static constexpr int KS = D / 32;
+  static constexpr int DV = D / 16;
   typedef typename VSlice<D>::type VS;
-  const int r = lane & 15, G = lane >> 4;
+  u32x4 kop[2][KS];
   VS vrow[8];
-  if (nvalid >= kTileKeys) {
+
+  __device__ __forceinline__ void load(__amdgpu_buffer_rsrc_t rk, __amdgpu_buffer_rsrc_t rv,
+                                       int key0, int lane) {
+    const int r = lane & 15, G = lane >> 4;
 #pragma unroll
     for (int a = 0; a < 2; ++a) {
-      const uint16_t* kp = K + (size_t)qk_key(a, r) * D + G * 8;
+      const int off = ((key0 + qk_key(a, r)) * D + G * 8) * 2;
 #pragma unroll
-      for (int s = 0; s < KS; ++s) kop[a][s] = load16(kp + s * 32);
+      for (int s = 0; s < KS; ++s) kop[a][s] = __builtin_amdgcn_raw_buffer_load_b128(rk, off + s * 64, 0, 0);
     }
+    const int voff = ((key0 + 8 * G) * D + DV * r) * 2;
 #pragma unroll
-    for (int e = 0; e < 8; ++e) vrow[e] = VSlice<D>::load(V + (size_t)(8 * G + e) * D + DV * r);
-  } else {
-#pragma unroll
-    for (int a = 0; a < 2; ++a) {
-      const int key = qk_key(a, r);
-      const uint16_t* kp = K + (size_t)key * D + G * 8;
-#pragma unroll
-      for (int s = 0; s < KS; ++s) kop[a][s] = key < nvalid ? load16(kp + s * 32) : u32x4{0, 0, 0, 0};
-    }
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      const int key = 8 * G + e;
-      vrow[e] = key < nvalid ? VSlice<D>::load(V + (size_t)key * D + DV * r) : VSlice<D>::zero();
-    }
+    for (int e = 0; e < 8; ++e) vrow[e] = VSlice<D>::load_buf(rv, voff + e * D * 2);
   }
+  // V^T operand of dimension block t: keys 8G+2w, 8G+2w+1 in word w.
+  __device__ __forceinline__ u32x4 vop(int t) const {
+    u32x4 v;
 #pragma unroll
-  for (int t = 0; t < DV; ++t)
-#pragma unroll
-    for (int w = 0; w < 4; ++w)
-      vop[t][w] = pair_elem(vword(vrow[2 * w], t), vword(vrow[2 * w + 1], t), t);
+    for (int w = 0; w < 4; ++w) v[w] = pair_elem(vword(vrow[2 * w], t), vword(vrow[2 * w + 1], t), t);
+    return v;
+  }
+};
+
+// Buffer resource over `rows` rows of d bf16 starting at `base` (raw, stride 0).
+template <int D>
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t rows_rsrc(const uint16_t* base, int rows) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(base), (short)0, rows * D * 2,
+                                           0x00020000);
 }
 
 // Row totals of the per-lane sums (the four lanes of a row share the row).
@@ -226,20 +246,131 @@ __device__ __forceinline__ void finish_sums(RowState<D, NT>& st) {
   }
 }
 
+// Write the wave's partials of rows row0 + nt*16 + n < nrows: lane (n, G)
+// stores dims [4*DV*G, 4*DV*G + 4*DV) of its row (contiguous), lane G = 0
+// the row's (m, l).
+template <int D, int NT>
+__device__ __forceinline__ void store_partials(RowState<D, NT>& st, int nrows, float* acc_out,
+                                               float2* ml_out, int lane) {
+  constexpr int DV = D / 16;
+  const int n = lane & 15, G = lane >> 4;
+  finish_sums(st);
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt) {
+    const int row = nt * kRowsPerTile + n;
+    if (row < nrows) {
+      float* dst = acc_out + (size_t)row * D + 4 * DV * G;
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int t4 = 0; t4 < DV; t4 += 4)
+          *reinterpret_cast<f32x4*>(dst + DV * j + t4) =
+              f32x4{st.acc[nt][t4][j], st.acc[nt][t4 + 1][j], st.acc[nt][t4 + 2][j],
+                    st.acc[nt][t4 + 3][j]};
+      if (G == 0) ml_out[row] = float2{st.mref[nt], st.l[nt]};
+    }
+  }
+}
+
+// One wave streams the 32-key tiles starting at keys k0, k0 + stride,
+// k0 + 2*stride, ... below k1 of one cache segment (rows of d bf16 from K/V)
+// through tile_update, double-buffered: the loads of the next tile are issued
+// before the current one is consumed, so a tile is always in flight. The
+// waves that share a segment start at neighbouring tiles, so together they
+// sweep one window of it. qw: this wave's Q^T operands in LDS,
+// [NT][d/32][64 lanes].
+template <int D, int NT>
+__device__ __forceinline__ void stream_keys(RowState<D, NT>& st, const u32x4* qw,
+                                            const uint16_t* K, const uint16_t* V, int k0, int k1,
+                                            int stride, float scale_log2, int lane) {
+  constexpr int KS = D / 32;
+  if (k0 >= k1) return;
+  const __amdgpu_buffer_rsrc_t rk = rows_rsrc<D>(K, k1), rv = rows_rsrc<D>(V, k1);
+  // Volatile: a real LDS read at each use, not a register copy kept alive
+  // across the loop (which would cost 16 registers per query tile).
+  auto q_at = [&](int nt, int s) -> u32x4 {
+    return *(volatile const lds_u32x4*)(qw + (nt * KS + s) * 64 + lane);
+  };
+  TileRegs<D> A, B;
+  // Prefetches are unconditional: past k1 the buffer range check returns
+  // zeros without a memory access, and a fixed count of loads in flight lets
+  // each wait cover only the tile being consumed.
+  A.load(rk, rv, k0, lane);
+  for (int key = k0;; key += 2 * stride) {
+    const int key1 = key + stride;
+    B.load(rk, rv, key1, lane);
+    tile_update<D, NT>(st, A.kop, [&](int t) { return A.vop(t); }, q_at, min(kTileKeys, k1 - key),
+                       scale_log2, lane);
+    if (key1 >= k1) break;
+    const int key2 = key1 + stride;
+    A.load(rk, rv, key2, lane);
+    tile_update<D, NT>(st, B.kop, [&](int t) { return B.vop(t); }, q_at, min(kTileKeys, k1 - key1),
+                       scale_log2, lane);
+    if (key2 >= k1) break;
+  }
+}
+
+// Stage this wave's Q^T operands of NT query tiles in its LDS slice qw.
+// row_ptr(r) gives the bf16 row of tile row r (r = nt*16 + n) or nullptr
+// for padding rows.
+template <int D, int NT, typename RowPtr>
+__device__ __forceinline__ void stage_q(u32x4* qw, RowPtr row_ptr, int lane) {
+  constexpr int KS = D / 32;
+  u32x4 qop[NT][KS];
+  load_q<D, NT>(qop, row_ptr, lane);
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+    for (int s = 0; s < KS; ++s)
+      *(volatile lds_u32x4*)(qw + (nt * KS + s) * 64 + lane) = qop[nt][s];
+}
+
+__device__ __forceinline__ int clamp_len(const int32_t* lens, int i, int m_d_max) {
+  const int raw = lens ? lens[i] : 0;
+  return raw < 0 ? 0 : (raw > m_d_max ? m_d_max : raw);
+}
+
+// ---------------------------------------------------------------------------
+// Decode part (and the replicated ablation): work-group (sample i, group gam,
+// key chunk s) over the sample's own cache rows [s*dec_keys,
+// min((s+1)*dec_keys, len)). Its four waves take interleaved tiles and each
+// writes its own partial of the p query rows of group gam (partial slot
+// (chunk, wave)); a wave without keys writes the empty partial
+// (m = -inf, l = 0, acc = 0).
+template <int D, int NT>
+__device__ void decode_block(const PartialsParams& P, int blk, int wave, int lane, u32x4* qw) {
+  const int s = blk % P.S_d;
+  const int ig = blk / P.S_d;
+  const int gam = ig % P.g, i = ig / P.g;
+  const int total = P.len_offset + clamp_len(P.lens, i, P.m_d_max);
+  const int k0 = s * P.dec_keys;
+  const int k1 = min(total, k0 + P.dec_keys);
+  const size_t cache = (size_t)(i * P.g + gam) * P.dec_rows * D;
+  const uint16_t* qbase = P.q + ((size_t)i * P.h + (size_t)gam * P.p) * D;
+  const int p = P.p;
+  stage_q<D, NT>(qw, [&](int r) -> const uint16_t* { return r < p ? qbase + (size_t)r * D : nullptr; },
+                 lane);
+  RowState<D, NT> st;
+  st.init();
+  stream_keys<D, NT>(st, qw, P.Kd + cache, P.Vd + cache, k0 + wave * kTileKeys, k1,
+                     kWaves * kTileKeys, P.scale_log2, lane);
+  const size_t prow = ((size_t)blk * kWaves + wave) * P.p;
+  store_partials<D, NT>(st, p, P.dec_acc + prow * D, P.dec_ml + prow, lane);
+}
+
 // Merge the four waves' states of the same NT*16 rows through LDS (in wave
-// order, so the result is deterministic) and write rows < nrows to
-// acc_out[row * row_stride_acc] / ml_out[row * row_stride_ml].
+// order, so the result is deterministic) and write rows < nrows of the
+// merged partial to acc_out / ml_out.
 template <int D, int NT>
 __device__ __forceinline__ void merge_waves_and_store(RowState<D, NT>& st, float* lds, int nrows,
-                                                      float* acc_out, size_t row_stride_acc,
-                                                      float2* ml_out, size_t row_stride_ml) {
+                                                      float* acc_out, float2* ml_out, int wave,
+                                                      int lane) {
   constexpr int DV = D / 16;
   constexpr int LD = D + 4;  // padded LDS row
   constexpr int ROWS = NT * kRowsPerTile;
   float* acc_s = lds;
   float* m_s = lds + ROWS * LD;
   float* l_s = m_s + ROWS;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int n = lane & 15, G = lane >> 4;
   finish_sums(st);
   for (int turn = 0; turn < kWaves; ++turn) {
@@ -272,88 +403,42 @@ __device__ __forceinline__ void merge_waves_and_store(RowState<D, NT>& st, float
     }
     __syncthreads();
   }
-  // Cooperative copy of the valid rows to the workspace.
   constexpr int V4 = D / 4;
   for (int idx = threadIdx.x; idx < nrows * V4; idx += kThreads) {
     const int row = idx / V4, c = idx % V4;
-    *reinterpret_cast<f32x4*>(acc_out + row * row_stride_acc + 4 * c) =
+    *reinterpret_cast<f32x4*>(acc_out + (size_t)row * D + 4 * c) =
         *reinterpret_cast<const f32x4*>(acc_s + row * LD + 4 * c);
   }
-  for (int row = threadIdx.x; row < nrows; row += kThreads)
-    ml_out[row * row_stride_ml] = float2{m_s[row], l_s[row]};
+  for (int row = threadIdx.x; row < nrows; row += kThreads) ml_out[row] = float2{m_s[row], l_s[row]};
 }
-
-__device__ __forceinline__ int clamp_len(const int32_t* lens, int i, int m_d_max) {
-  const int raw = lens ? lens[i] : 0;
-  return raw < 0 ? 0 : (raw > m_d_max ? m_d_max : raw);
-}
-
-// ---------------------------------------------------------------------------
-// Decode part (and the replicated ablation): work-group (sample i, group gam,
-// key split s) over the sample's own cache rows [s*dec_keys, ...). Query rows
-// are the p heads of group gam. Waves take interleaved tiles and merge.
-template <int D, int NT>
-__device__ void decode_block(const PartialsParams& P, int blk, float* lds) {
-  const int s = blk % P.S_d;
-  const int ig = blk / P.S_d;
-  const int gam = ig % P.g, i = ig / P.g;
-  const int total = P.len_offset + clamp_len(P.lens, i, P.m_d_max);
-  const int k0 = s * P.dec_keys;
-  if (k0 >= total) return;  // whole work-group: nothing to do for this split
-  const int k1 = min(total, k0 + P.dec_keys);
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const size_t cache = (size_t)(i * P.g + gam) * P.dec_rows * D;
-  const uint16_t* Kb = P.Kd + cache;
-  const uint16_t* Vb = P.Vd + cache;
-  u32x4 qop[NT][D / 32];
-  const uint16_t* qbase = P.q + ((size_t)i * P.h + (size_t)gam * P.p) * D;
-  const int p = P.p;
-  load_q<D, NT>(qop, [&](int r) -> const uint16_t* { return r < p ? qbase + (size_t)r * D : nullptr; },
-                lane);
-  RowState<D, NT> st;
-  st.init();
-  for (int key0 = k0 + wave * kTileKeys; key0 < k1; key0 += kWaves * kTileKeys) {
-    u32x4 kop[2][D / 32];
-    u32x4 vop[D / 16];
-    const int nvalid = min(kTileKeys, k1 - key0);
-    load_tile_regs<D>(kop, vop, Kb + (size_t)key0 * D, Vb + (size_t)key0 * D, nvalid, lane);
-    tile_update<D, NT>(st, kop, vop, qop, nvalid, P.scale_log2, lane);
-  }
-  const size_t prow = ((size_t)ig * P.S_d + s) * P.p;
-  merge_waves_and_store<D, NT>(st, lds, p, P.dec_acc + prow * D, D, P.dec_ml + prow, 1);
-}
+template <int D, int NT> struct MergeLds {
+  static constexpr int bytes = (NT * kRowsPerTile * (D + 4) + 2 * NT * kRowsPerTile) * 4;
+};
 
 // Context part, few query rows per group (M = b*p <= 64): work-group
-// (group gam, key split s) reads Kc/Vc rows [s*ctx_keys, ...) once, each tile
-// straight into the operands of the wave that uses it for all M rows.
+// (group gam, split s) of S_c per group. The 4*S_c waves of a group take the
+// group's 32-key tiles round robin (wave w of split s: tiles 4s+w,
+// 4s+w+4*S_c, ...), so they sweep K_c/V_c together and each tile is read
+// once, straight into the operands that serve all M query rows. The four
+// waves' states merge in LDS into the split's partial.
 template <int D, int NT>
-__device__ void ctx_small_block(const PartialsParams& P, int blk, float* lds) {
+__device__ void ctx_small_block(const PartialsParams& P, int blk, int wave, int lane, u32x4* qw,
+                                float* merge_lds) {
   const int s = blk % P.S_c, gam = blk / P.S_c;
-  const int k0 = s * P.ctx_keys;
-  const int k1 = min(P.m_c, k0 + P.ctx_keys);
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const size_t cache = (size_t)gam * P.m_c * D;
-  const uint16_t* Kb = P.Kc + cache;
-  const uint16_t* Vb = P.Vc + cache;
   const int M = P.M, p = P.p, h = P.h;
   const uint16_t* q = P.q;
-  u32x4 qop[NT][D / 32];
-  load_q<D, NT>(qop, [&](int r) -> const uint16_t* {
+  stage_q<D, NT>(qw, [&](int r) -> const uint16_t* {
     if (r >= M) return nullptr;
     const int i = r / p, jp = r - i * p;
     return q + ((size_t)i * h + (size_t)gam * p + jp) * D;
   }, lane);
   RowState<D, NT> st;
   st.init();
-  for (int key0 = k0 + wave * kTileKeys; key0 < k1; key0 += kWaves * kTileKeys) {
-    u32x4 kop[2][D / 32];
-    u32x4 vop[D / 16];
-    const int nvalid = min(kTileKeys, k1 - key0);
-    load_tile_regs<D>(kop, vop, Kb + (size_t)key0 * D, Vb + (size_t)key0 * D, nvalid, lane);
-    tile_update<D, NT>(st, kop, vop, qop, nvalid, P.scale_log2, lane);
-  }
-  const size_t prow = ((size_t)gam * P.S_c + s) * P.M;
-  merge_waves_and_store<D, NT>(st, lds, M, P.ctx_acc + prow * D, D, P.ctx_ml + prow, 1);
+  stream_keys<D, NT>(st, qw, P.Kc + cache, P.Vc + cache, (s * kWaves + wave) * kTileKeys, P.m_c,
+                     P.S_c * kWaves * kTileKeys, P.scale_log2, lane);
+  const size_t prow = (size_t)blk * P.M;
+  merge_waves_and_store<D, NT>(st, merge_lds, M, P.ctx_acc + prow * D, P.ctx_ml + prow, wave, lane);
 }
 
 // Context part, many query rows per group: work-group (group gam, key split
@@ -377,7 +462,7 @@ __device__ void ctx_large_block(const PartialsParams& P, int blk, float* lds) {
   const int s = sg % P.S_c, gam = sg / P.S_c;
   const int k0 = s * P.ctx_keys;
   const int k1 = min(P.m_c, k0 + P.ctx_keys);
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63, wave = wave_id();
   const int r = lane & 15, G = lane >> 4;
   const size_t cache = (size_t)gam * P.m_c * D;
   const uint16_t* Kb = P.Kc + cache;
@@ -435,15 +520,13 @@ __device__ void ctx_large_block(const PartialsParams& P, int blk, float* lds) {
     const int buf = it & 1;
     if (it + 1 < ntiles) fetch(k0 + (it + 1) * kTileKeys);
     u32x4 kop[2][KS];
-    u32x4 vop[DV];
 #pragma unroll
     for (int a = 0; a < 2; ++a)
 #pragma unroll
       for (int ss = 0; ss < KS; ++ss) kop[a][ss] = slot(buf, a * KS + ss)[lane];
-#pragma unroll
-    for (int t = 0; t < DV; ++t) vop[t] = slot(buf, KOPS + t)[lane];
     const int nvalid = min(kTileKeys, k1 - (k0 + it * kTileKeys));
-    tile_update<D, NT>(st, kop, vop, qop, nvalid, P.scale_log2, lane);
+    tile_update<D, NT>(st, kop, [&](int t) { return slot(buf, KOPS + t)[lane]; },
+                       [&](int nt, int ss) { return qop[nt][ss]; }, nvalid, P.scale_log2, lane);
     if (it + 1 < ntiles) stage(buf ^ 1);
     __syncthreads();
   }
@@ -466,9 +549,6 @@ __device__ void ctx_large_block(const PartialsParams& P, int blk, float* lds) {
   }
 }
 
-template <int D, int NT> struct MergeLds {
-  static constexpr int bytes = (NT * kRowsPerTile * (D + 4) + 2 * NT * kRowsPerTile) * 4;
-};
 template <int D> struct LargeLds {
   static constexpr int bytes = 2 * (2 * (D / 32) + D / 16) * 64 * 16;
 };
@@ -484,67 +564,124 @@ __device__ __forceinline__ int xcd_logical(int bid, int n) {
   return (bid % X) * per + bid / X;
 }
 
+// Grid: n_ctx_blocks work-groups of the many-row context path, then
+// n_ctx_small_blocks of the few-row context path, then n_dec_blocks decode
+// work-groups.
+template <int D, int CTX, int NTD>
+__device__ __forceinline__ void partials_body(const PartialsParams& P) {
+  constexpr bool kSmall = CTX != kCtxNone && CTX != kCtxLarge;
+  constexpr int NTC = kSmall ? CTX : 1;
+  constexpr int NTQ = NTC > NTD ? NTC : NTD;
+  constexpr int QSLOTS = kWaves * NTQ * (D / 32) * 64;  // u32x4 slots for Q^T operands
+  constexpr int MERGE = kSmall ? (MergeLds<D, NTC>::bytes + 15) / 16 : 0;
+  constexpr int LDS = CTX == kCtxLarge ? cmax(LargeLds<D>::bytes / 16, QSLOTS) : QSLOTS + MERGE;
+  __shared__ __attribute__((aligned(16))) u32x4 lds[LDS];
+  const int bid = blockIdx.x;
+  if constexpr (CTX == kCtxLarge) {
+    if (bid < P.n_ctx_blocks) {
+      ctx_large_block<D>(P, xcd_logical(bid, P.n_ctx_blocks), reinterpret_cast<float*>(lds));
+      return;
+    }
+  }
+  const int lane = threadIdx.x & 63, wave = wave_id();
+  u32x4* qw = lds + wave * NTQ * (D / 32) * 64;
+  const int blk = bid - P.n_ctx_blocks;
+  if (blk < P.n_ctx_small_blocks) {
+    if constexpr (kSmall)
+      ctx_small_block<D, NTC>(P, blk, wave, lane, qw, reinterpret_cast<float*>(lds + QSLOTS));
+  } else if (blk - P.n_ctx_small_blocks < P.n_dec_blocks) {
+    decode_block<D, NTD>(P, blk - P.n_ctx_small_blocks, wave, lane, qw);
+  }
+}
+
+// Variants whose waves hold at most two query tiles fit two waves
+// per SIMD (<= 256 registers) and are compiled for that occupancy; the others
+// keep the compiler's choice.
+template <int D, int CTX, int NTD>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) void
+partials_kernel_2w(PartialsParams P) {
+  partials_body<D, CTX, NTD>(P);
+}
 template <int D, int CTX, int NTD>
 __global__ __launch_bounds__(kThreads) void partials_kernel(PartialsParams P) {
-  constexpr int LDS_CTX = CTX == kCtxLarge ? LargeLds<D>::bytes
-                          : CTX == kCtxNone ? 0 : MergeLds<D, (CTX > 0 ? CTX : 1)>::bytes;
-  constexpr int LDS = cmax(cmax(LDS_CTX, MergeLds<D, NTD>::bytes), 16);
-  __shared__ __attribute__((aligned(16))) float lds[LDS / 4];
-  const int bid = blockIdx.x;
-  if (bid < P.n_ctx_blocks) {
-    if constexpr (CTX == kCtxLarge) {
-      ctx_large_block<D>(P, xcd_logical(bid, P.n_ctx_blocks), lds);
-    } else if constexpr (CTX != kCtxNone) {
-      ctx_small_block<D, CTX>(P, bid, lds);
-    }
-  } else {
-    decode_block<D, NTD>(P, bid - P.n_ctx_blocks, lds);
-  }
+  partials_body<D, CTX, NTD>(P);
+}
+template <int D, int CTX, int NTD>
+constexpr bool fits_two_waves() {
+  return CTX != kCtxLarge && CTX != kCtxSmall4 && NTD <= 2;
 }
 
 // Combine (the joint softmax of Eq. 3-4): one wave per output row (i, j)
 // merges the row's context partials (group j/p, every split) and decode
-// partials (sample i, group j/p, the splits that hold keys) into
+// partials (sample i, group j/p, every chunk; empty ones weigh 0) into
 // out = sum_k 2^(m_k - M) acc_k / sum_k 2^(m_k - M) l_k, M = max_k m_k.
+// Lane k first fetches the statistics of partial k (all in parallel), so the
+// weights need one wave reduction; the value rows are then summed in a fixed
+// order with their loads issued ahead in batches.
 template <int D>
 __global__ __launch_bounds__(256) void combine_kernel(CombineParams C) {
   constexpr int PER = D / 64;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  constexpr int BATCH = 8;
+  const int lane = threadIdx.x & 63, wave = wave_id();
   const int row = blockIdx.x * 4 + wave;
   if (row >= C.b * C.h) return;
   const int i = row / C.h, j = row - i * C.h;
   const int gam = j / C.p, jp = j - gam * C.p;
-  const int raw = C.lens ? C.lens[i] : 0;
-  const int len = clamp_len(C.lens, i, C.m_d_max);
-  if (raw != len && j == 0 && lane == 0) atomicOr(C.status, kStatusLens);
-  const int total = C.len_offset + len;
-  const int nsd = C.S_d ? (total + C.dec_keys - 1) / C.dec_keys : 0;
-  const int np = C.S_c + nsd;
+  if (j == 0 && lane == 0 && C.lens) {
+    const int raw = C.lens[i];
+    if (raw < 0 || raw > C.m_d_max) atomicOr(C.status, kStatusLens);
+  }
+  const int np = C.S_c + C.S_d;  // every decode item wrote a partial (maybe empty)
   const size_t cbase = (size_t)gam * C.S_c * C.M + (size_t)i * C.p + jp;  // + k*M
   const size_t dbase = ((size_t)(i * C.g + gam) * C.S_d) * C.p + jp;      // + k*p
   auto idx = [&](int k) -> size_t {
     return k < C.S_c ? cbase + (size_t)k * C.M : dbase + (size_t)(k - C.S_c) * C.p;
   };
-  auto ml = [&](int k) -> float2 { return k < C.S_c ? C.ctx_ml[idx(k)] : C.dec_ml[idx(k)]; };
   auto accp = [&](int k) -> const float* {
-    return (k < C.S_c ? C.ctx_acc : C.dec_acc) + idx(k) * D;
+    return (k < C.S_c ? C.ctx_acc : C.dec_acc) + idx(k) * D + lane * PER;
   };
-  float mx = kNegInf;
-  for (int k = lane; k < np; k += 64) mx = fmaxf(mx, ml(k).x);
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) mx = fmaxf(mx, __shfl_xor(mx, o));
-  const float base = mx == kNegInf ? 0.f : mx;
   float acc[PER];
 #pragma unroll
   for (int e = 0; e < PER; ++e) acc[e] = 0.f;
   float L = 0.f;
-  for (int k = 0; k < np; ++k) {
-    const float2 v = ml(k);
-    const float w = exp2_fast(v.x - base);
-    L += w * v.y;
-    const float* a = accp(k) + lane * PER;
+  float mx = kNegInf;
+  for (int k0 = 0; k0 < np; k0 += 64) {  // running max over chunks of 64 partials
+    const int k = k0 + lane;
+    const float2 ml = k < np ? (k < C.S_c ? C.ctx_ml[idx(k)] : C.dec_ml[idx(k)])
+                             : float2{kNegInf, 0.f};
+    float cm = ml.x;
 #pragma unroll
-    for (int e = 0; e < PER; ++e) acc[e] += w * a[e];
+    for (int o = 32; o > 0; o >>= 1) cm = fmaxf(cm, __shfl_xor(cm, o));
+    const float mnew = fmaxf(mx, cm);
+    const float base = mnew == kNegInf ? 0.f : mnew;
+    const float rescale = exp2_fast(mx - base);  // 0 on the first chunk
+    L *= rescale;
+#pragma unroll
+    for (int e = 0; e < PER; ++e) acc[e] *= rescale;
+    mx = mnew;
+    const float w = exp2_fast(ml.x - base);      // 0 for padding lanes
+    float lw = w * ml.y;
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) lw += __shfl_xor(lw, o);
+    L += lw;
+    const int kn = min(64, np - k0);
+    for (int kb = 0; kb < kn; kb += BATCH) {
+      float v[BATCH][PER];
+#pragma unroll
+      for (int u = 0; u < BATCH; ++u) {
+        const float* a = accp(k0 + min(kb + u, kn - 1));
+#pragma unroll
+        for (int e = 0; e < PER; ++e) v[u][e] = a[e];
+      }
+#pragma unroll
+      for (int u = 0; u < BATCH; ++u) {
+        const float wu = __shfl(w, kb + u);
+        if (kb + u < kn) {
+#pragma unroll
+          for (int e = 0; e < PER; ++e) acc[e] += wu * v[u][e];
+        }
+      }
+    }
   }
   float* o = C.out + (size_t)row * D + lane * PER;
   const float inv = 1.f / L;
@@ -554,11 +691,21 @@ __global__ __launch_bounds__(256) void combine_kernel(CombineParams C) {
 
 template <int D, int CTX>
 hipError_t launch_partials_ctx(const PartialsParams& P, int dec_tiles, hipStream_t stream) {
-  const int grid = P.n_ctx_blocks + P.n_dec_blocks;
+  const int grid = P.n_ctx_blocks + P.n_ctx_small_blocks + P.n_dec_blocks;
   if (grid == 0) return hipSuccess;
   switch (dec_tiles) {
-    case 1: partials_kernel<D, CTX, 1><<<grid, kThreads, 0, stream>>>(P); break;
-    case 2: partials_kernel<D, CTX, 2><<<grid, kThreads, 0, stream>>>(P); break;
+    case 1:
+      if constexpr (fits_two_waves<D, CTX, 1>())
+        partials_kernel_2w<D, CTX, 1><<<grid, kThreads, 0, stream>>>(P);
+      else
+        partials_kernel<D, CTX, 1><<<grid, kThreads, 0, stream>>>(P);
+      break;
+    case 2:
+      if constexpr (fits_two_waves<D, CTX, 2>())
+        partials_kernel_2w<D, CTX, 2><<<grid, kThreads, 0, stream>>>(P);
+      else
+        partials_kernel<D, CTX, 2><<<grid, kThreads, 0, stream>>>(P);
+      break;
     case 4: partials_kernel<D, CTX, 4><<<grid, kThreads, 0, stream>>>(P); break;
     default: return hipErrorInvalidValue;
   }
