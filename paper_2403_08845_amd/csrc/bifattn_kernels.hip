@@ -84,8 +84,11 @@ __device__ __forceinline__ u32x4 load16(const uint16_t* p) {
   return *reinterpret_cast<const u32x4*>(p);
 }
 
-// Row r of a QK sub-tile a holds tile key 8*(r>>2) + 4a + (r&3).
-__device__ __forceinline__ int qk_key(int a, int r) { return 8 * (r >> 2) + 4 * a + (r & 3); }
+// Row r of QK sub-tile a holds tile key 16a + 4(r&3) + (r>>2). The logit
+// accumulator of sub-tile a then gives lane (n, G) keys 16a + 4j + G
+// (j = 0..3), i.e. keys 4e + G for e = 4a + j = 0..7: the same keys, in the
+// same order, as the V^T operand a lane builds from value rows 4e + G.
+__device__ __forceinline__ int qk_key(int a, int r) { return 16 * a + 4 * (r & 3) + (r >> 2); }
 
 // Element t of a value slice: 16-bit lane t of the slice's words.
 template <typename S>
@@ -115,37 +118,42 @@ template <int D, int NT> struct RowState {
 };
 
 // One 32-key tile against NT query tiles: S^T = K Q^T on MFMA, online softmax
-// with lazy rescaling, O^T += V^T P^T on MFMA. kop are this lane's K
-// operands, vop_at(t) yields its V^T operand of dimension block t (built on
-// demand, so only one is live at a time), q_at(nt, s) its Q^T operands. Keys
-// >= nvalid are masked.
-template <int D, int NT, typename VOp, typename QOp>
-__device__ __forceinline__ void tile_update(RowState<D, NT>& st, const u32x4 (&kop)[2][D / 32],
-                                            VOp&& vop_at, QOp&& q_at, int nvalid,
-                                            float scale_log2, int lane) {
+// with lazy rescaling, O^T += V^T P^T on MFMA. k_at(a, s) yields this lane's
+// K operand of sub-tile a and k-step s, vop_at(t) its V^T operand of
+// dimension block t (built on demand, so only one is live at a time),
+// q_at(nt, s) its Q^T operands. Keys >= nvalid are masked.
+template <int D, int NT, typename KOp, typename VOp, typename QOp>
+__device__ __forceinline__ void tile_update(RowState<D, NT>& st, KOp&& k_at, VOp&& vop_at,
+                                            QOp&& q_at, int nvalid, float scale_log2, int lane) {
   constexpr int KS = D / 32;
   constexpr int DV = D / 16;
   const int G = lane >> 4;
+  f32x4 sacc[NT][2];
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt) sacc[nt][0] = sacc[nt][1] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int s = 0; s < KS; ++s) {
+    const u32x4 k0 = k_at(0, s), k1 = k_at(1, s);
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) {
+      const u32x4 qo = q_at(nt, s);
+      sacc[nt][0] = mfma_bf16(k0, qo, sacc[nt][0]);
+      sacc[nt][1] = mfma_bf16(k1, qo, sacc[nt][1]);
+    }
+  }
   u32x4 pb[NT];
 #pragma unroll
   for (int nt = 0; nt < NT; ++nt) {
-    f32x4 s0 = {0.f, 0.f, 0.f, 0.f}, s1 = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int s = 0; s < KS; ++s) {
-      const u32x4 qo = q_at(nt, s);
-      s0 = mfma_bf16(kop[0][s], qo, s0);
-      s1 = mfma_bf16(kop[1][s], qo, s1);
-    }
-    float x[8];
+    float x[8];  // x[e]: key 4e + G
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-      x[j] = s0[j] * scale_log2;
-      x[4 + j] = s1[j] * scale_log2;
+      x[j] = sacc[nt][0][j] * scale_log2;
+      x[4 + j] = sacc[nt][1][j] * scale_log2;
     }
     if (nvalid < kTileKeys) {
 #pragma unroll
       for (int e = 0; e < 8; ++e)
-        if (8 * G + e >= nvalid) x[e] = kNegInf;
+        if (4 * e + G >= nvalid) x[e] = kNegInf;
     }
     float tmax = x[0];
 #pragma unroll
@@ -195,32 +203,70 @@ __device__ __forceinline__ void load_q(u32x4 (&qop)[NT][D / 32], RowPtr row_ptr,
   }
 }
 
-// Register path: one wave loads a whole 32-key tile into its own registers:
-// K operands directly, value rows raw (lane (r, G) holds keys 8G..8G+7 at
-// dims DV*r .. DV*r+DV-1); V^T operands are formed from them on demand.
+// Register path: one wave loads a whole 32-key tile, every load instruction
+// reading whole consecutive rows (1 KB contiguous for d = 128):
+//   K: lane l holds row RPI*e + l/CPR, 16-byte chunk l%CPR (CPR = d/8 chunks
+//      per row, RPI = 64/CPR rows per instruction); staged through a
+//      per-wave LDS tile to reach the MFMA operand layout, whose 16 lanes
+//      each want a different row (XOR-swizzled so those reads are
+//      bank-conflict free);
+//   V: lane (c, G) holds row 4e + G, dims DV*c .. DV*c+DV-1 (e = 0..7), which
+//      is already what its V^T operands need: formed on demand by a 16-bit
+//      transpose inside the lane.
 // Loads go through buffer resources whose range ends at the item's last key,
 // so rows past it read as zero without a branch and without a memory access.
 template <int D> struct TileRegs {
   static constexpr int KS = D / 32;
   static constexpr int DV = D / 16;
+  static constexpr int CPR = D / 8;
+  static constexpr int RPI = 64 / CPR;
+  static constexpr int KI = kTileKeys / RPI;
   typedef typename VSlice<D>::type VS;
-  u32x4 kop[2][KS];
+  u32x4 kraw[KI];
   VS vrow[8];
+
+  // Swizzled 16-byte slot of (row, chunk) in a K tile staged in LDS.
+  static __device__ __forceinline__ int kslot(int row, int chunk) {
+    const int swz = D == 128 ? (row & 15) : ((row >> 1) & 7);
+    return row * CPR + (chunk ^ swz);
+  }
 
   __device__ __forceinline__ void load(__amdgpu_buffer_rsrc_t rk, __amdgpu_buffer_rsrc_t rv,
                                        int key0, int lane) {
-    const int r = lane & 15, G = lane >> 4;
+    const int koff = ((key0 + lane / CPR) * D + (lane % CPR) * 8) * 2;
 #pragma unroll
-    for (int a = 0; a < 2; ++a) {
-      const int off = ((key0 + qk_key(a, r)) * D + G * 8) * 2;
+    for (int e = 0; e < KI; ++e)
+      kraw[e] = __builtin_amdgcn_raw_buffer_load_b128(rk, koff + e * RPI * D * 2, 0, 0);
+    const int c = lane & 15, G = lane >> 4;
+    const int voff = ((key0 + G) * D + DV * c) * 2;
 #pragma unroll
-      for (int s = 0; s < KS; ++s) kop[a][s] = __builtin_amdgcn_raw_buffer_load_b128(rk, off + s * 64, 0, 0);
-    }
-    const int voff = ((key0 + 8 * G) * D + DV * r) * 2;
-#pragma unroll
-    for (int e = 0; e < 8; ++e) vrow[e] = VSlice<D>::load_buf(rv, voff + e * D * 2);
+    for (int e = 0; e < 8; ++e) vrow[e] = VSlice<D>::load_buf(rv, voff + 4 * e * D * 2);
   }
-  // V^T operand of dimension block t: keys 8G+2w, 8G+2w+1 in word w.
+  // Write the raw K rows into this wave's LDS tile (KI*64 16-byte slots).
+  // Lanes read each other's rows afterwards; a wave executes its LDS
+  // instructions in order, and the wave barriers stop the compiler from
+  // moving reads of the previous tile below these writes or reads of this
+  // tile above them.
+  __device__ __forceinline__ void stage_k(u32x4* kl, int lane) const {
+    __builtin_amdgcn_wave_barrier();
+#pragma unroll
+    for (int e = 0; e < KI; ++e)
+      *(lds_u32x4*)(kl + kslot(RPI * e + lane / CPR, lane % CPR)) = kraw[e];
+    __builtin_amdgcn_wave_barrier();
+  }
+  // K operand of sub-tile a, k-step s: row qk_key(a, n), dims 32s + 8G .. +7.
+  static __device__ __forceinline__ u32x4 kop(const u32x4* kl, int a, int s, int lane) {
+    return *(const lds_u32x4*)(kl + kslot(qk_key(a, lane & 15), 4 * s + (lane >> 4)));
+  }
+  // Zero the value rows of keys >= nvalid (rows past a sample's length may
+  // hold anything; their weight is 0 but 0 * NaN is not).
+  __device__ __forceinline__ void mask_v(int nvalid, int lane) {
+    const int G = lane >> 4;
+#pragma unroll
+    for (int e = 0; e < 8; ++e)
+      if (4 * e + G >= nvalid) vrow[e] = VSlice<D>::zero();
+  }
+  // V^T operand of dimension block t: keys 4(2w) + G, 4(2w+1) + G in word w.
   __device__ __forceinline__ u32x4 vop(int t) const {
     u32x4 v;
 #pragma unroll
@@ -273,39 +319,45 @@ __device__ __forceinline__ void store_partials(RowState<D, NT>& st, int nrows, f
 }
 
 // One wave streams the 32-key tiles starting at keys k0, k0 + stride,
-// k0 + 2*stride, ... below k1 of one cache segment (rows of d bf16 from K/V)
-// through tile_update, double-buffered: the loads of the next tile are issued
-// before the current one is consumed, so a tile is always in flight. The
-// waves that share a segment start at neighbouring tiles, so together they
-// sweep one window of it. qw: this wave's Q^T operands in LDS,
-// [NT][d/32][64 lanes].
+// k0 + 2*stride, ... below k1 of one cache segment (buffer resources rk/rv
+// over rows of d bf16) through tile_update, double-buffered: the loads of the
+// next tile are issued before the current one is consumed, so a tile is
+// always in flight. The caller has already issued the loads of the first tile
+// into A (before anything else, so that they overlap the set-up). The waves
+// that share a segment start at neighbouring tiles, so together they sweep
+// one window of it. qw: this wave's Q^T operands in LDS, [NT][d/32][64
+// lanes]; kl: this wave's LDS K tile (32*d*2 bytes).
 template <int D, int NT>
-__device__ __forceinline__ void stream_keys(RowState<D, NT>& st, const u32x4* qw,
-                                            const uint16_t* K, const uint16_t* V, int k0, int k1,
-                                            int stride, float scale_log2, int lane) {
+__device__ __forceinline__ void stream_keys(RowState<D, NT>& st, const u32x4* qw, u32x4* kl,
+                                            __amdgpu_buffer_rsrc_t rk, __amdgpu_buffer_rsrc_t rv,
+                                            TileRegs<D>& A, int k0, int k1, int stride,
+                                            float scale_log2, int lane) {
   constexpr int KS = D / 32;
   if (k0 >= k1) return;
-  const __amdgpu_buffer_rsrc_t rk = rows_rsrc<D>(K, k1), rv = rows_rsrc<D>(V, k1);
   // Volatile: a real LDS read at each use, not a register copy kept alive
   // across the loop (which would cost 16 registers per query tile).
   auto q_at = [&](int nt, int s) -> u32x4 {
     return *(volatile const lds_u32x4*)(qw + (nt * KS + s) * 64 + lane);
   };
-  TileRegs<D> A, B;
-  // Prefetches are unconditional: past k1 the buffer range check returns
-  // zeros without a memory access, and a fixed count of loads in flight lets
-  // each wait cover only the tile being consumed.
-  A.load(rk, rv, k0, lane);
+  auto k_at = [&](int a, int s) { return TileRegs<D>::kop(kl, a, s, lane); };
+  TileRegs<D> B;
+  // Prefetches are unconditional: past the resource range the buffer load
+  // returns zeros without a memory access, and a fixed count of loads in
+  // flight lets each wait cover only the tile being consumed.
   for (int key = k0;; key += 2 * stride) {
     const int key1 = key + stride;
     B.load(rk, rv, key1, lane);
-    tile_update<D, NT>(st, A.kop, [&](int t) { return A.vop(t); }, q_at, min(kTileKeys, k1 - key),
-                       scale_log2, lane);
+    const int nv0 = min(kTileKeys, k1 - key);
+    if (nv0 < kTileKeys) A.mask_v(nv0, lane);
+    A.stage_k(kl, lane);
+    tile_update<D, NT>(st, k_at, [&](int t) { return A.vop(t); }, q_at, nv0, scale_log2, lane);
     if (key1 >= k1) break;
     const int key2 = key1 + stride;
     A.load(rk, rv, key2, lane);
-    tile_update<D, NT>(st, B.kop, [&](int t) { return B.vop(t); }, q_at, min(kTileKeys, k1 - key1),
-                       scale_log2, lane);
+    const int nv1 = min(kTileKeys, k1 - key1);
+    if (nv1 < kTileKeys) B.mask_v(nv1, lane);
+    B.stage_k(kl, lane);
+    tile_update<D, NT>(st, k_at, [&](int t) { return B.vop(t); }, q_at, nv1, scale_log2, lane);
     if (key2 >= k1) break;
   }
 }
@@ -338,22 +390,28 @@ __device__ __forceinline__ int clamp_len(const int32_t* lens, int i, int m_d_max
 // (chunk, wave)); a wave without keys writes the empty partial
 // (m = -inf, l = 0, acc = 0).
 template <int D, int NT>
-__device__ void decode_block(const PartialsParams& P, int blk, int wave, int lane, u32x4* qw) {
+__device__ void decode_block(const PartialsParams& P, int blk, int wave, int lane, u32x4* qw,
+                             u32x4* kl) {
   const int s = blk % P.S_d;
   const int ig = blk / P.S_d;
   const int gam = ig % P.g, i = ig / P.g;
-  const int total = P.len_offset + clamp_len(P.lens, i, P.m_d_max);
-  const int k0 = s * P.dec_keys;
-  const int k1 = min(total, k0 + P.dec_keys);
+  const int kbeg = s * P.dec_keys;
+  const int kcap = min(P.dec_rows, kbeg + P.dec_keys);  // the chunk within the cache capacity
   const size_t cache = (size_t)(i * P.g + gam) * P.dec_rows * D;
+  const __amdgpu_buffer_rsrc_t rk = rows_rsrc<D>(P.Kd + cache, kcap);
+  const __amdgpu_buffer_rsrc_t rv = rows_rsrc<D>(P.Vd + cache, kcap);
+  const int k0 = kbeg + wave * kTileKeys;
+  TileRegs<D> A;
+  A.load(rk, rv, k0, lane);  // first tile in flight before the length is known
+  const int total = P.len_offset + clamp_len(P.lens, i, P.m_d_max);
+  const int k1 = min(total, kcap);
   const uint16_t* qbase = P.q + ((size_t)i * P.h + (size_t)gam * P.p) * D;
   const int p = P.p;
   stage_q<D, NT>(qw, [&](int r) -> const uint16_t* { return r < p ? qbase + (size_t)r * D : nullptr; },
                  lane);
   RowState<D, NT> st;
   st.init();
-  stream_keys<D, NT>(st, qw, P.Kd + cache, P.Vd + cache, k0 + wave * kTileKeys, k1,
-                     kWaves * kTileKeys, P.scale_log2, lane);
+  stream_keys<D, NT>(st, qw, kl, rk, rv, A, k0, k1, kWaves * kTileKeys, P.scale_log2, lane);
   const size_t prow = ((size_t)blk * kWaves + wave) * P.p;
   store_partials<D, NT>(st, p, P.dec_acc + prow * D, P.dec_ml + prow, lane);
 }
@@ -423,9 +481,14 @@ template <int D, int NT> struct MergeLds {
 // waves' states merge in LDS into the split's partial.
 template <int D, int NT>
 __device__ void ctx_small_block(const PartialsParams& P, int blk, int wave, int lane, u32x4* qw,
-                                float* merge_lds) {
+                                u32x4* kl, float* merge_lds) {
   const int s = blk % P.S_c, gam = blk / P.S_c;
   const size_t cache = (size_t)gam * P.m_c * D;
+  const __amdgpu_buffer_rsrc_t rk = rows_rsrc<D>(P.Kc + cache, P.m_c);
+  const __amdgpu_buffer_rsrc_t rv = rows_rsrc<D>(P.Vc + cache, P.m_c);
+  const int k0 = (s * kWaves + wave) * kTileKeys;
+  TileRegs<D> A;
+  A.load(rk, rv, k0, lane);  // first tile in flight while Q is staged
   const int M = P.M, p = P.p, h = P.h;
   const uint16_t* q = P.q;
   stage_q<D, NT>(qw, [&](int r) -> const uint16_t* {
@@ -435,9 +498,10 @@ __device__ void ctx_small_block(const PartialsParams& P, int blk, int wave, int 
   }, lane);
   RowState<D, NT> st;
   st.init();
-  stream_keys<D, NT>(st, qw, P.Kc + cache, P.Vc + cache, (s * kWaves + wave) * kTileKeys, P.m_c,
-                     P.S_c * kWaves * kTileKeys, P.scale_log2, lane);
+  stream_keys<D, NT>(st, qw, kl, rk, rv, A, k0, P.m_c, P.S_c * kWaves * kTileKeys, P.scale_log2,
+                     lane);
   const size_t prow = (size_t)blk * P.M;
+  __syncthreads();  // the merge buffer overlays the waves' K tiles
   merge_waves_and_store<D, NT>(st, merge_lds, M, P.ctx_acc + prow * D, P.ctx_ml + prow, wave, lane);
 }
 
@@ -495,7 +559,7 @@ __device__ void ctx_large_block(const PartialsParams& P, int blk, float* lds) {
     }
 #pragma unroll
     for (int c = 0; c < 2; ++c) {
-      const int key = 8 * G + 2 * wave + c;
+      const int key = 4 * (2 * wave + c) + G;
       vst[c] = key < nvalid ? VSlice<D>::load(Vb + (size_t)(key0 + key) * D + DV * r)
                             : VSlice<D>::zero();
     }
@@ -503,7 +567,7 @@ __device__ void ctx_large_block(const PartialsParams& P, int blk, float* lds) {
   auto stage = [&](int buf) {
 #pragma unroll
     for (int c = 0; c < KPW; ++c) slot(buf, wave * KPW + c)[lane] = kst[c];
-    // word `wave` of V^T operand t = keys (8G + 2*wave, 8G + 2*wave + 1) at dim DV*r + t
+    // word `wave` of V^T operand t = keys 4(2*wave) + G, 4(2*wave+1) + G at dim DV*r + t
 #pragma unroll
     for (int t = 0; t < DV; ++t)
       reinterpret_cast<uint32_t*>(slot(buf, KOPS + t) + lane)[wave] =
@@ -519,13 +583,9 @@ __device__ void ctx_large_block(const PartialsParams& P, int blk, float* lds) {
   for (int it = 0; it < ntiles; ++it) {
     const int buf = it & 1;
     if (it + 1 < ntiles) fetch(k0 + (it + 1) * kTileKeys);
-    u32x4 kop[2][KS];
-#pragma unroll
-    for (int a = 0; a < 2; ++a)
-#pragma unroll
-      for (int ss = 0; ss < KS; ++ss) kop[a][ss] = slot(buf, a * KS + ss)[lane];
     const int nvalid = min(kTileKeys, k1 - (k0 + it * kTileKeys));
-    tile_update<D, NT>(st, kop, [&](int t) { return slot(buf, KOPS + t)[lane]; },
+    tile_update<D, NT>(st, [&](int a, int ss) { return slot(buf, a * KS + ss)[lane]; },
+                       [&](int t) { return slot(buf, KOPS + t)[lane]; },
                        [&](int nt, int ss) { return qop[nt][ss]; }, nvalid, P.scale_log2, lane);
     if (it + 1 < ntiles) stage(buf ^ 1);
     __syncthreads();
@@ -573,8 +633,10 @@ __device__ __forceinline__ void partials_body(const PartialsParams& P) {
   constexpr int NTC = kSmall ? CTX : 1;
   constexpr int NTQ = NTC > NTD ? NTC : NTD;
   constexpr int QSLOTS = kWaves * NTQ * (D / 32) * 64;  // u32x4 slots for Q^T operands
-  constexpr int MERGE = kSmall ? (MergeLds<D, NTC>::bytes + 15) / 16 : 0;
-  constexpr int LDS = CTX == kCtxLarge ? cmax(LargeLds<D>::bytes / 16, QSLOTS) : QSLOTS + MERGE;
+  constexpr int KSLOTS = kWaves * kTileKeys * D / 8;      // one staged K tile per wave
+  constexpr int MERGE = kSmall ? (MergeLds<D, NTC>::bytes + 15) / 16 : 0;  // overlays the K tiles
+  constexpr int LDS = CTX == kCtxLarge ? cmax(LargeLds<D>::bytes / 16, QSLOTS + KSLOTS)
+                                       : QSLOTS + cmax(KSLOTS, MERGE);
   __shared__ __attribute__((aligned(16))) u32x4 lds[LDS];
   const int bid = blockIdx.x;
   if constexpr (CTX == kCtxLarge) {
@@ -585,12 +647,13 @@ __device__ __forceinline__ void partials_body(const PartialsParams& P) {
   }
   const int lane = threadIdx.x & 63, wave = wave_id();
   u32x4* qw = lds + wave * NTQ * (D / 32) * 64;
+  u32x4* kl = lds + QSLOTS + wave * (kTileKeys * D / 8);
   const int blk = bid - P.n_ctx_blocks;
   if (blk < P.n_ctx_small_blocks) {
     if constexpr (kSmall)
-      ctx_small_block<D, NTC>(P, blk, wave, lane, qw, reinterpret_cast<float*>(lds + QSLOTS));
+      ctx_small_block<D, NTC>(P, blk, wave, lane, qw, kl, reinterpret_cast<float*>(lds + QSLOTS));
   } else if (blk - P.n_ctx_small_blocks < P.n_dec_blocks) {
-    decode_block<D, NTD>(P, blk - P.n_ctx_small_blocks, wave, lane, qw);
+    decode_block<D, NTD>(P, blk - P.n_ctx_small_blocks, wave, lane, qw, kl);
   }
 }
 
@@ -621,7 +684,7 @@ constexpr bool fits_two_waves() {
 template <int D>
 __global__ __launch_bounds__(256) void combine_kernel(CombineParams C) {
   constexpr int PER = D / 64;
-  constexpr int BATCH = 8;
+  constexpr int BATCH = 16;
   const int lane = threadIdx.x & 63, wave = wave_id();
   const int row = blockIdx.x * 4 + wave;
   if (row >= C.b * C.h) return;
@@ -631,7 +694,7 @@ __global__ __launch_bounds__(256) void combine_kernel(CombineParams C) {
     const int raw = C.lens[i];
     if (raw < 0 || raw > C.m_d_max) atomicOr(C.status, kStatusLens);
   }
-  const int np = C.S_c + C.S_d;  // every decode item wrote a partial (maybe empty)
+  const int np = C.S_c + C.S_d;  // every decode wave wrote a partial (maybe empty)
   const size_t cbase = (size_t)gam * C.S_c * C.M + (size_t)i * C.p + jp;  // + k*M
   const size_t dbase = ((size_t)(i * C.g + gam) * C.S_d) * C.p + jp;      // + k*p
   auto idx = [&](int k) -> size_t {
@@ -646,6 +709,16 @@ __global__ __launch_bounds__(256) void combine_kernel(CombineParams C) {
   float L = 0.f;
   float mx = kNegInf;
   for (int k0 = 0; k0 < np; k0 += 64) {  // running max over chunks of 64 partials
+    const int kn = min(64, np - k0);
+    // Issue the first batch of value rows together with the statistics, so
+    // a chunk of up to BATCH partials costs one memory round trip.
+    float v[BATCH][PER];
+#pragma unroll
+    for (int u = 0; u < BATCH; ++u) {
+      const float* a = accp(k0 + min(u, kn - 1));
+#pragma unroll
+      for (int e = 0; e < PER; ++e) v[u][e] = a[e];
+    }
     const int k = k0 + lane;
     const float2 ml = k < np ? (k < C.S_c ? C.ctx_ml[idx(k)] : C.dec_ml[idx(k)])
                              : float2{kNegInf, 0.f};
@@ -664,18 +737,18 @@ __global__ __launch_bounds__(256) void combine_kernel(CombineParams C) {
 #pragma unroll
     for (int o = 32; o > 0; o >>= 1) lw += __shfl_xor(lw, o);
     L += lw;
-    const int kn = min(64, np - k0);
     for (int kb = 0; kb < kn; kb += BATCH) {
-      float v[BATCH][PER];
+      if (kb > 0) {
 #pragma unroll
-      for (int u = 0; u < BATCH; ++u) {
-        const float* a = accp(k0 + min(kb + u, kn - 1));
+        for (int u = 0; u < BATCH; ++u) {
+          const float* a = accp(k0 + min(kb + u, kn - 1));
 #pragma unroll
-        for (int e = 0; e < PER; ++e) v[u][e] = a[e];
+          for (int e = 0; e < PER; ++e) v[u][e] = a[e];
+        }
       }
 #pragma unroll
       for (int u = 0; u < BATCH; ++u) {
-        const float wu = __shfl(w, kb + u);
+        const float wu = __shfl(w, min(kb + u, 63));
         if (kb + u < kn) {
 #pragma unroll
           for (int e = 0; e < PER; ++e) acc[e] += wu * v[u][e];
