@@ -92,6 +92,98 @@ def cpu_baseline(x, w, min_seconds):
                       f"{per * 1e3:.1f} ms per step"}
 
 
+COPY_BYTES = 1 << 30
+
+
+def calibrate_copy(reps: int = 5):
+    """A copy-equivalent elementwise kernel over COPY_BYTES (torch.neg on
+    float32: reads COPY_BYTES, writes COPY_BYTES), the reference for the HBM
+    counters: FETCH_SIZE and WRITE_SIZE should each read COPY_BYTES per
+    dispatch. A kernel of its own name, so that it is not confused with the
+    blit kernels of host uploads."""
+    import torch
+    a = torch.ones(COPY_BYTES // 4, dtype=torch.float32, device="cuda")
+    b = torch.empty_like(a)
+    for _ in range(reps):
+        torch.neg(a, out=b)
+    torch.cuda.synchronize()
+    del a, b
+    log(f"[bench] copy-equivalent kernel over {COPY_BYTES} bytes, {reps} times")
+
+
+def summarize_profile(stats_dir: str, fetch_dir: str, write_dir: str, workload: str, out_dir: str,
+                      warmup: int, steps: int):
+    """Turn rocprofv3 outputs into the committed summary: the kernel-trace
+    statistics, and the partial kernel's HBM traffic per launch from the two
+    counter runs, each scaled by what the same counter reads for the plain
+    copy of COPY_BYTES."""
+    import csv
+    import glob
+
+    def rows(d, pattern):
+        files = glob.glob(os.path.join(d, "**", pattern), recursive=True)
+        if not files:
+            raise SystemExit(f"no {pattern} under {d}")
+        return list(csv.DictReader(open(files[0])))
+
+    stats = rows(stats_dir, "*kernel_stats.csv")
+    # The partial kernel's launches in dispatch order: warmup, value loop,
+    # event-timed loop, warm loop, ...; average the event-timed ones.
+    trace = [r for r in rows(stats_dir, "*kernel_trace.csv") if "partials_kernel" in r["Kernel_Name"]]
+    trace.sort(key=lambda r: int(r["Start_Timestamp"]))
+    timed = trace[warmup + steps: warmup + 2 * steps]
+    timed_us = sum(int(r["End_Timestamp"]) - int(r["Start_Timestamp"]) for r in timed) / len(timed) / 1e3
+
+    def per_kernel(d, counter):
+        acc = {}
+        for r in rows(d, "*counter_collection.csv"):
+            if r.get("Counter_Name") != counter:
+                continue
+            acc.setdefault(r["Kernel_Name"], []).append(float(r["Counter_Value"]))
+        return acc
+
+    fetch, write = per_kernel(fetch_dir, "FETCH_SIZE"), per_kernel(write_dir, "WRITE_SIZE")
+
+    def pick(acc, key):
+        for name, vals in acc.items():
+            if key(name):
+                return name, sum(vals) / len(vals), len(vals)
+        raise SystemExit(f"kernel not found in counters: {list(acc)}")
+
+    is_copy = lambda n: "neg" in n.lower()
+    is_part = lambda n: "partials_kernel" in n
+    _, copy_fetch_kib, _ = pick(fetch, is_copy)
+    _, copy_write_kib, _ = pick(write, is_copy)
+    pname, part_fetch_kib, nf = pick(fetch, is_part)
+    _, part_write_kib, nw = pick(write, is_part)
+    f_scale = COPY_BYTES / (copy_fetch_kib * 1024.0)
+    w_scale = COPY_BYTES / (copy_write_kib * 1024.0)
+    fetch_b = part_fetch_kib * 1024.0 * f_scale
+    write_b = part_write_kib * 1024.0 * w_scale
+    rec = {"workload": workload, "kernel": pname, "kernel_source_sha256_16": kernel_source_hash(),
+           "fetch_size_kib_per_dispatch": part_fetch_kib, "write_size_kib_per_dispatch": part_write_kib,
+           "dispatches": [nf, nw], "copy_fetch_kib": copy_fetch_kib, "copy_write_kib": copy_write_kib,
+           "copy_bytes": COPY_BYTES, "fetch_scale": f_scale, "write_scale": w_scale,
+           "hbm_fetch_bytes_per_launch": fetch_b, "hbm_write_bytes_per_launch": write_b,
+           "hbm_bytes_per_launch": fetch_b + write_b,
+           "trace_avg_us_event_timed_launches": timed_us}
+    os.makedirs(out_dir, exist_ok=True)
+    json.dump(rec, open(os.path.join(out_dir, f"traffic_partials_{workload}.json"), "w"), indent=1)
+    lines = [f"# rocprofv3 kernel statistics, {workload}", "",
+             "| kernel | calls | avg us | min us | max us | % time |", "|---|---|---|---|---|---|"]
+    for r in stats:
+        lines.append(f"| {r['Name'][:90]} | {r['Calls']} | {float(r['AverageNs']) / 1e3:.2f} | "
+                     f"{float(r['MinNs']) / 1e3:.2f} | {float(r['MaxNs']) / 1e3:.2f} | "
+                     f"{float(r['Percentage']):.2f} |")
+    lines += ["", f"`{pname}` over the {len(timed)} launches that bench.py times with HIP events "
+              f"(dispatches {warmup + steps}..{warmup + 2 * steps - 1}): average {timed_us:.2f} us."]
+    lines += ["", f"HBM traffic of `{pname}` per launch (FETCH_SIZE / WRITE_SIZE, scaled by a "
+              f"{COPY_BYTES}-byte copy: fetch x{f_scale:.4f}, write x{w_scale:.4f}): "
+              f"{fetch_b / 1e6:.2f} MB read, {write_b / 1e6:.2f} MB written."]
+    print("\n".join(lines))
+    return lines
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -101,7 +193,15 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-ablation", action="store_true")
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="first run the 1 GiB copy-equivalent kernel that scales HBM counters")
+    ap.add_argument("--summarize-profile", nargs=4, metavar=("STATS", "FETCH", "WRITE", "OUT"),
+                    help="summarize rocprofv3 outputs of the workload into OUT")
     args = ap.parse_args()
+    if args.summarize_profile:
+        summarize_profile(*args.summarize_profile[:3], args.workload, args.summarize_profile[3],
+                          args.warmup, args.steps)
+        return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU: the bifurcated decode step runs on a single MI355X "
               "(see DESIGN.md for how it would shard); --gpus must be 1.", file=sys.stderr)
@@ -110,6 +210,8 @@ def main():
     import torch
     import paper_2403_08845_amd as bif
 
+    if args.calibrate_copy:
+        calibrate_copy()
     w = workloads.WORKLOADS[args.workload]
     log(f"[bench] generating {w.name}")
     x = workloads.make_workload_inputs(w)

@@ -33,6 +33,7 @@ SMALL_CASES = [
     (3, 6, 3, 64, 1, 3, True),            # single context key
     (2, 4, 2, 128, 96, 0, False),         # no decode cache
     (40, 32, 1, 128, 2000, 64, True),     # M = 1280 -> 5 row blocks, ragged last block
+    (100, 6, 2, 64, 300, 40, True),       # p = 3, M = 300: a sample's rows straddle two row blocks
 ]
 
 
@@ -157,3 +158,35 @@ def test_timing_api_counts_calls():
         n, ms = bif.bifattn_plan_read_timing(plan)
         assert n == 3 and 0 < ms < 1000
         bif.bifattn_plan_set_timing(plan, bif.KERNEL_PARTIALS, 0)
+
+
+@pytest.mark.parametrize("case", [(32, 32, 32, 128, 3000, 300, True), (12, 64, 2, 128, 900, 200, True),
+                                  (8, 32, 8, 64, 1500, 90, True)],
+                         ids=lambda c: "b%d_h%d_g%d_d%d_mc%d_md%d" % c[:6])
+def test_workspace_reuse_over_many_calls(case):
+    """One plan, inputs alternating between two problems for 40 calls: every
+    output equals the first result for its input bit for bit (no partial of
+    a previous call can leak into the next one)."""
+    import torch
+    b, h, g, d, m_c, m_d, ragged = case
+    xs = [workloads.make_inputs(b, h, g, d, m_c, m_d, seed=80 + k, ragged=ragged) for k in range(2)]
+    devs = [to_device(x) for x in xs]
+    with bif.Plan(b, h, g, d, m_c, m_d) as plan:
+        refs = []
+        for dv in devs:
+            out = torch.empty((b, h, d), dtype=torch.float32, device="cuda")
+            bif.bifattn_decode(plan, dv["q"], dv["Kc"], dv["Vc"], dv["Kd"], dv["Vd"], dv["lens"], out)
+            refs.append(out)
+        torch.cuda.synchronize()
+        assert_parity(refs[0].cpu().double().numpy(), oracle.attention(**xs[0]), "first call")
+        outs = [torch.empty((b, h, d), dtype=torch.float32, device="cuda") for _ in range(2)]
+        for it in range(40):
+            k = it % 2
+            dv = devs[k]
+            bif.bifattn_decode(plan, dv["q"], dv["Kc"], dv["Vc"], dv["Kd"], dv["Vd"], dv["lens"],
+                               outs[k])
+            if k == 1:
+                torch.cuda.synchronize()
+                for kk in range(2):
+                    assert torch.equal(outs[kk], refs[kk]), f"call {it}: input {kk} differs"
+        assert bif.bifattn_plan_status(plan) == bif.OK
