@@ -60,7 +60,8 @@ extern "C" {
 typedef enum {
   BIFATTN_OK = 0,
   BIFATTN_EINVAL = -1,       /* null pointer, non-positive size, h % g != 0, ... */
-  BIFATTN_EUNSUPPORTED = -2, /* valid but not built: d not in {64,128}, p > 64 */
+  BIFATTN_EUNSUPPORTED = -2, /* valid but not built: d not in {64,128}, p > 64,
+                                (m_c + m_d_max) * d * 2 > 2^31 - 1 */
   BIFATTN_EALIGN = -3,       /* a tensor pointer not 16-byte aligned */
   BIFATTN_ENOMEM = -4,       /* workspace or event allocation failed */
   BIFATTN_EHIP = -5,         /* a HIP runtime call or kernel launch failed */
@@ -104,8 +105,9 @@ typedef enum {
  * Validate dims and allocate the plan and its workspace on the current HIP
  * device. On success *plan is set; on failure *plan is left NULL.
  * Errors: EINVAL (null argument, b/h/g/m_c < 1, m_d_max < 0, h % g != 0,
- * sizes whose byte counts overflow), EUNSUPPORTED (d not 64 or 128, or
- * h/g > 64), ENOMEM (device allocation failed), EHIP (no usable device).
+ * sizes whose byte counts overflow), EUNSUPPORTED (d not 64 or 128,
+ * h/g > 64, or one sample's cache rows (m_c + m_d_max) * d * 2 bytes beyond
+ * 2^31 - 1), ENOMEM (device allocation failed), EHIP (no usable device).
  */
 bifattn_status_t bifattn_plan_create(const bifattn_dims_t *dims, bifattn_plan_t *plan);
 

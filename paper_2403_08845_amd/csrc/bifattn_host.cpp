@@ -82,11 +82,12 @@ bifattn_status_t plan_splits(bifattn_plan_s* P) {
     P->ctx_keys = keys;
     P->ctx_row_blocks = 1;
   } else {
-    // Many rows: work-groups of 256 rows share each staged K_c/V_c tile;
-    // about one work-group per CU.
+    // Many rows: work-groups of 128 rows share each staged K_c/V_c tile;
+    // about two work-groups per CU, so that one computes while the other
+    // waits on its loads and barriers.
     P->ctx_mode = kCtxLarge;
     P->ctx_row_blocks = (int)ceil_div(M, kLargeRowsPerBlock);
-    int64_t splits = ceil_div(kCUs, (int64_t)d.g * P->ctx_row_blocks);
+    int64_t splits = ceil_div(2 * kCUs, (int64_t)d.g * P->ctx_row_blocks);
     if (splits < 1) splits = 1;
     const int64_t ck = round_up(ceil_div(d.m_c, splits), kTileKeys);
     P->ctx_keys = (int)round_up(env_int("BIFATTN_CTX_KEYS", (int)ck), kTileKeys);
@@ -108,10 +109,10 @@ bifattn_status_t plan_splits(bifattn_plan_s* P) {
                               kTileKeys);
   P->S_r = (int)ceil_div(rep_rows, P->rep_keys);
   P->n_rep_blocks = (int)(units * P->S_r);
-  // One launch for both parts when their waves have the same register
-  // footprint; the many-row context path runs as its own launch.
-  // BIFATTN_LAUNCH=1 forces one launch, 2 forces two.
-  const int launch = env_int("BIFATTN_LAUNCH", P->ctx_mode == kCtxLarge ? 2 : 1);
+  // Context and decode work-groups share one launch, so that the decode
+  // part's HBM streaming overlaps the context part (compute-bound when many
+  // rows share it). BIFATTN_LAUNCH=2 splits them into two launches.
+  const int launch = env_int("BIFATTN_LAUNCH", 1);
   P->fused = launch == 1 ? 1 : 0;
   if ((int64_t)P->n_ctx_blocks + P->n_ctx_small_blocks + P->n_dec_blocks > INT32_MAX / 2 ||
       units * P->S_r > INT32_MAX / 2)
@@ -134,6 +135,9 @@ bifattn_status_t check_dims(const bifattn_dims_t* d) {
     return BIFATTN_EINVAL;
   if ((double)d->b * d->h > INT32_MAX / 2 || (double)d->b * d->g > INT32_MAX / 2)
     return BIFATTN_EINVAL;
+  // Kernels address one cache (a group's context, a sample's decode rows, or
+  // both in the replicated ablation) with 32-bit byte offsets.
+  if (((double)d->m_c + d->m_d_max) * dd * 2 > INT32_MAX) return BIFATTN_EUNSUPPORTED;
   return BIFATTN_OK;
 }
 
@@ -178,7 +182,10 @@ PartialsParams base_params(const bifattn_plan_s* P, const void* q, const int32_t
   K.M = P->M;
   K.m_c = P->dims.m_c;
   K.m_d_max = P->dims.m_d_max;
-  K.scale_log2 = P->scale * 1.4426950408889634f;
+  // scale * (q . k) = |scale| * ((-q) . k): a negative scale negates q, which
+  // is exact in bf16, so the kernels only ever see a positive scale.
+  K.scale_log2 = std::fabs(P->scale) * 1.4426950408889634f;
+  K.q_sign = P->scale < 0.f ? 0x80008000u : 0u;
   return K;
 }
 

@@ -16,7 +16,7 @@ constexpr int kTileKeys = 32;
 // Query rows per MFMA N-tile.
 constexpr int kRowsPerTile = 16;
 // Context path with many query rows per group: query tiles per wave.
-constexpr int kLargeTilesPerWave = 4;
+constexpr int kLargeTilesPerWave = 2;
 constexpr int kLargeRowsPerBlock = kWaves * kLargeTilesPerWave * kRowsPerTile;  // 256
 // Largest group size the per-sample decode path holds in registers.
 constexpr int kMaxP = 64;
@@ -56,7 +56,8 @@ struct PartialsParams {
   int n_ctx_blocks;       // work-groups of the many-row context path
   int n_ctx_small_blocks; // work-groups of the few-row context path (g * S_c)
   int n_dec_blocks;       // decode work-groups (b * g * S_d); 4 partials each
-  float scale_log2;       // scale * log2(e)
+  float scale_log2;       // |scale| * log2(e)
+  uint32_t q_sign;        // 0x80008000 when scale < 0 (q enters negated, exactly), else 0
 };
 
 struct CombineParams {

@@ -51,6 +51,56 @@ __device__ __forceinline__ uint32_t pack_bf16(float lo, float hi) {
 
 __device__ __forceinline__ float exp2_fast(float x) { return __builtin_amdgcn_exp2f(x); }
 
+// Cross-row exchanges without a trip through LDS: v_permlane16_swap and
+// v_permlane32_swap of a register with itself return, in their two results,
+// the lane's own value and the value of lane l^16 (l^32), in an order that
+// depends on the row; max / sum of the two is the same in every lane. The
+// two vector elements are copied to scalars before the float reinterpret:
+// __builtin_bit_cast applied to an element of the result vector reads
+// element 0 whatever the index.
+template <bool kWide>
+__device__ __forceinline__ void swap_halves(float x, float& a, float& b) {
+  const unsigned u = __float_as_uint(x);
+  const auto r = kWide ? __builtin_amdgcn_permlane32_swap(u, u, false, false)
+                       : __builtin_amdgcn_permlane16_swap(u, u, false, false);
+  const unsigned r0 = r[0], r1 = r[1];
+  a = __uint_as_float(r0);
+  b = __uint_as_float(r1);
+}
+__device__ __forceinline__ float xor16_max(float x) {
+  float a, b;
+  swap_halves<false>(x, a, b);
+  return fmaxf(a, b);
+}
+__device__ __forceinline__ float xor32_max(float x) {
+  float a, b;
+  swap_halves<true>(x, a, b);
+  return fmaxf(a, b);
+}
+__device__ __forceinline__ float xor16_sum(float x) {
+  float a, b;
+  swap_halves<false>(x, a, b);
+  return a + b;
+}
+__device__ __forceinline__ float xor32_sum(float x) {
+  float a, b;
+  swap_halves<true>(x, a, b);
+  return a + b;
+}
+// Whole-wave reductions: permlane swaps across rows, then shuffles in a row.
+__device__ __forceinline__ float wave_max(float x) {
+  x = xor32_max(xor16_max(x));
+#pragma unroll
+  for (int o = 8; o > 0; o >>= 1) x = fmaxf(x, __shfl_xor(x, o));
+  return x;
+}
+__device__ __forceinline__ float wave_sum(float x) {
+  x = xor32_sum(xor16_sum(x));
+#pragma unroll
+  for (int o = 8; o > 0; o >>= 1) x += __shfl_xor(x, o);
+  return x;
+}
+
 // Wave index within the work-group, as a wave-uniform (scalar) value so that
 // branches on it and on tile bounds derived from it stay scalar.
 __device__ __forceinline__ int wave_id() {
@@ -144,22 +194,26 @@ __device__ __forceinline__ void tile_update(RowState<D, NT>& st, KOp&& k_at, VOp
   u32x4 pb[NT];
 #pragma unroll
   for (int nt = 0; nt < NT; ++nt) {
+    // Raw logits; scale_log2 > 0, so the row max can be taken before scaling
+    // and the scale folds into the exponent's multiply-add.
     float x[8];  // x[e]: key 4e + G
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-      x[j] = sacc[nt][0][j] * scale_log2;
-      x[4 + j] = sacc[nt][1][j] * scale_log2;
+      x[j] = sacc[nt][0][j];
+      x[4 + j] = sacc[nt][1][j];
     }
     if (nvalid < kTileKeys) {
+      // The bound passes through readfirstlane (convergent), so the compiler
+      // cannot hoist these compares out of the branch into every full tile.
+      const int nv = __builtin_amdgcn_readfirstlane(nvalid);
 #pragma unroll
       for (int e = 0; e < 8; ++e)
-        if (4 * e + G >= nvalid) x[e] = kNegInf;
+        if (4 * e + G >= nv) x[e] = kNegInf;
     }
     float tmax = x[0];
 #pragma unroll
     for (int e = 1; e < 8; ++e) tmax = fmaxf(tmax, x[e]);
-    tmax = fmaxf(tmax, __shfl_xor(tmax, 16));
-    tmax = fmaxf(tmax, __shfl_xor(tmax, 32));
+    tmax = xor32_max(xor16_max(tmax)) * scale_log2;
     const bool raise = tmax > st.mref[nt] + kRescaleSlack;
     if (__any(raise)) {
       // Rows that do not raise keep alpha = 1 (and never form -inf - -inf).
@@ -169,14 +223,13 @@ __device__ __forceinline__ void tile_update(RowState<D, NT>& st, KOp&& k_at, VOp
       for (int t = 0; t < DV; ++t) st.acc[nt][t] *= alpha;
       st.mref[nt] = raise ? tmax : st.mref[nt];
     }
-    const float base = st.mref[nt] == kNegInf ? 0.f : st.mref[nt];
+    const float nbase = st.mref[nt] == kNegInf ? 0.f : -st.mref[nt];
     float pr[8];
-    float psum = 0.f;
 #pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      pr[e] = exp2_fast(x[e] - base);
-      psum += pr[e];
-    }
+    for (int e = 0; e < 8; ++e) pr[e] = exp2_fast(__builtin_fmaf(x[e], scale_log2, nbase));
+    float psum = pr[0];
+#pragma unroll
+    for (int e = 1; e < 8; ++e) psum += pr[e];
     st.l[nt] += psum;
 #pragma unroll
     for (int w = 0; w < 4; ++w) pb[nt][w] = pack_bf16(pr[2 * w], pr[2 * w + 1]);
@@ -190,16 +243,18 @@ __device__ __forceinline__ void tile_update(RowState<D, NT>& st, KOp&& k_at, VOp
 }
 
 // Q^T operands of NT query tiles. row_ptr(r) gives the bf16 row of tile row r
-// (r = nt*16 + n) or nullptr when the row is padding.
+// (r = nt*16 + n) or nullptr when the row is padding; `sign` is XORed into
+// every pair of bf16 (0x80008000 negates q for a negative softmax scale).
 template <int D, int NT, typename RowPtr>
-__device__ __forceinline__ void load_q(u32x4 (&qop)[NT][D / 32], RowPtr row_ptr, int lane) {
+__device__ __forceinline__ void load_q(u32x4 (&qop)[NT][D / 32], RowPtr row_ptr, uint32_t sign,
+                                       int lane) {
   const int n = lane & 15, G = lane >> 4;
 #pragma unroll
   for (int nt = 0; nt < NT; ++nt) {
     const uint16_t* qr = row_ptr(nt * kRowsPerTile + n);
 #pragma unroll
     for (int s = 0; s < D / 32; ++s)
-      qop[nt][s] = qr ? load16(qr + s * 32 + G * 8) : u32x4{0, 0, 0, 0};
+      qop[nt][s] = qr ? load16(qr + s * 32 + G * 8) ^ sign : u32x4{0, 0, 0, 0};
   }
 }
 
@@ -287,8 +342,7 @@ template <int D, int NT>
 __device__ __forceinline__ void finish_sums(RowState<D, NT>& st) {
 #pragma unroll
   for (int nt = 0; nt < NT; ++nt) {
-    st.l[nt] += __shfl_xor(st.l[nt], 16);
-    st.l[nt] += __shfl_xor(st.l[nt], 32);
+    st.l[nt] = xor32_sum(xor16_sum(st.l[nt]));
   }
 }
 
@@ -366,10 +420,10 @@ __device__ __forceinline__ void stream_keys(RowState<D, NT>& st, const u32x4* qw
 // row_ptr(r) gives the bf16 row of tile row r (r = nt*16 + n) or nullptr
 // for padding rows.
 template <int D, int NT, typename RowPtr>
-__device__ __forceinline__ void stage_q(u32x4* qw, RowPtr row_ptr, int lane) {
+__device__ __forceinline__ void stage_q(u32x4* qw, RowPtr row_ptr, uint32_t sign, int lane) {
   constexpr int KS = D / 32;
   u32x4 qop[NT][KS];
-  load_q<D, NT>(qop, row_ptr, lane);
+  load_q<D, NT>(qop, row_ptr, sign, lane);
 #pragma unroll
   for (int nt = 0; nt < NT; ++nt)
 #pragma unroll
@@ -408,7 +462,7 @@ __device__ void decode_block(const PartialsParams& P, int blk, int wave, int lan
   const uint16_t* qbase = P.q + ((size_t)i * P.h + (size_t)gam * P.p) * D;
   const int p = P.p;
   stage_q<D, NT>(qw, [&](int r) -> const uint16_t* { return r < p ? qbase + (size_t)r * D : nullptr; },
-                 lane);
+                 P.q_sign, lane);
   RowState<D, NT> st;
   st.init();
   stream_keys<D, NT>(st, qw, kl, rk, rv, A, k0, k1, kWaves * kTileKeys, P.scale_log2, lane);
@@ -495,7 +549,7 @@ __device__ void ctx_small_block(const PartialsParams& P, int blk, int wave, int 
     if (r >= M) return nullptr;
     const int i = r / p, jp = r - i * p;
     return q + ((size_t)i * h + (size_t)gam * p + jp) * D;
-  }, lane);
+  }, P.q_sign, lane);
   RowState<D, NT> st;
   st.init();
   stream_keys<D, NT>(st, qw, kl, rk, rv, A, k0, P.m_c, P.S_c * kWaves * kTileKeys, P.scale_log2,
@@ -506,14 +560,16 @@ __device__ void ctx_small_block(const PartialsParams& P, int blk, int wave, int 
 }
 
 // Context part, many query rows per group: work-group (group gam, key split
-// s, row block rb) of 256 query rows. Each 32-key tile of Kc/Vc is loaded
-// from HBM once per work-group into LDS, already in MFMA operand order (the
-// V^T transpose is done once, on the way in), and all four waves read it for
-// their 64 rows. Double-buffered: the next tile's global loads are in flight
-// while the current one is consumed. Row blocks of one key chunk are
-// scheduled on the same XCD so that they share its L2.
+// s, row block rb) of 128 query rows, 32 per wave, two work-groups per CU.
+// Each 32-key tile of Kc/Vc is loaded from HBM once per work-group into LDS,
+// already in MFMA operand order (the V^T transpose is done once, on the way
+// in), and all four waves read it for their rows. Double-buffered with one
+// barrier per tile: the next tile's global loads are in flight while the
+// current one is consumed, and written to the other buffer after it. Q^T
+// operands stay in registers. Row blocks of one key chunk are scheduled on
+// the same XCD so that they share its L2.
 template <int D>
-__device__ void ctx_large_block(const PartialsParams& P, int blk, float* lds) {
+__device__ void ctx_large_block(const PartialsParams& P, int blk, u32x4* lds) {
   constexpr int KS = D / 32;
   constexpr int DV = D / 16;
   constexpr int NT = kLargeTilesPerWave;
@@ -528,41 +584,30 @@ __device__ void ctx_large_block(const PartialsParams& P, int blk, float* lds) {
   const int k1 = min(P.m_c, k0 + P.ctx_keys);
   const int lane = threadIdx.x & 63, wave = wave_id();
   const int r = lane & 15, G = lane >> 4;
-  const size_t cache = (size_t)gam * P.m_c * D;
-  const uint16_t* Kb = P.Kc + cache;
-  const uint16_t* Vb = P.Vc + cache;
+  // Buffer resources over the chunk's keys [k0, k1): rows past it load as
+  // zero with no memory access and no branch. Offsets count from k0.
+  const size_t chunk = ((size_t)gam * P.m_c + k0) * D;
+  const __amdgpu_buffer_rsrc_t rk = rows_rsrc<D>(P.Kc + chunk, k1 - k0);
+  const __amdgpu_buffer_rsrc_t rv = rows_rsrc<D>(P.Vc + chunk, k1 - k0);
   const int M = P.M, p = P.p, h = P.h;
   const int row0 = rb * kLargeRowsPerBlock + wave * NT * kRowsPerTile;
   const uint16_t* q = P.q;
-  u32x4 qop[NT][KS];
-  load_q<D, NT>(qop, [&](int rr) -> const uint16_t* {
-    const int row = row0 + rr;
-    if (row >= M) return nullptr;
-    const int i = row / p, jp = row - i * p;
-    return q + ((size_t)i * h + (size_t)gam * p + jp) * D;
-  }, lane);
   // LDS: two buffers of OPS operand slots x 64 lanes x 16 B.
-  u32x4* opbuf = reinterpret_cast<u32x4*>(lds);
-  auto slot = [&](int buf, int op) -> u32x4* { return opbuf + ((size_t)buf * OPS + op) * 64; };
+  auto slot = [&](int buf, int op) -> u32x4* { return lds + ((size_t)buf * OPS + op) * 64; };
 
   // Staging registers of the next tile: this wave's K operands and two value rows.
   u32x4 kst[KPW];
   VS vst[2];
   auto fetch = [&](int key0) {
-    const int nvalid = min(kTileKeys, k1 - key0);
 #pragma unroll
     for (int c = 0; c < KPW; ++c) {
       const int op = wave * KPW + c, a = op / KS, ss = op % KS;
-      const int key = qk_key(a, r);
-      kst[c] = key < nvalid ? load16(Kb + (size_t)(key0 + key) * D + ss * 32 + G * 8)
-                            : u32x4{0, 0, 0, 0};
+      kst[c] = __builtin_amdgcn_raw_buffer_load_b128(
+          rk, ((key0 + qk_key(a, r)) * D + ss * 32 + G * 8) * 2, 0, 0);
     }
 #pragma unroll
-    for (int c = 0; c < 2; ++c) {
-      const int key = 4 * (2 * wave + c) + G;
-      vst[c] = key < nvalid ? VSlice<D>::load(Vb + (size_t)(key0 + key) * D + DV * r)
-                            : VSlice<D>::zero();
-    }
+    for (int c = 0; c < 2; ++c)
+      vst[c] = VSlice<D>::load_buf(rv, ((key0 + 4 * (2 * wave + c) + G) * D + DV * r) * 2);
   };
   auto stage = [&](int buf) {
 #pragma unroll
@@ -574,19 +619,28 @@ __device__ void ctx_large_block(const PartialsParams& P, int blk, float* lds) {
           pair_elem(vword(vst[0], t), vword(vst[1], t), t);
   };
 
+  fetch(0);  // first tile in flight while Q is loaded
+  u32x4 qop[NT][KS];
+  load_q<D, NT>(qop, [&](int rr) -> const uint16_t* {
+    const int row = row0 + rr;
+    if (row >= M) return nullptr;
+    const int i = row / p, jp = row - i * p;
+    return q + ((size_t)i * h + (size_t)gam * p + jp) * D;
+  }, P.q_sign, lane);
   RowState<D, NT> st;
   st.init();
   const int ntiles = (k1 - k0 + kTileKeys - 1) / kTileKeys;
-  fetch(k0);
   stage(0);
   __syncthreads();
   for (int it = 0; it < ntiles; ++it) {
     const int buf = it & 1;
-    if (it + 1 < ntiles) fetch(k0 + (it + 1) * kTileKeys);
+    if (it + 1 < ntiles) fetch((it + 1) * kTileKeys);
     const int nvalid = min(kTileKeys, k1 - (k0 + it * kTileKeys));
     tile_update<D, NT>(st, [&](int a, int ss) { return slot(buf, a * KS + ss)[lane]; },
                        [&](int t) { return slot(buf, KOPS + t)[lane]; },
                        [&](int nt, int ss) { return qop[nt][ss]; }, nvalid, P.scale_log2, lane);
+    // The other buffer was last read in the previous iteration, before the
+    // barrier that ended it.
     if (it + 1 < ntiles) stage(buf ^ 1);
     __syncthreads();
   }
@@ -609,7 +663,7 @@ __device__ void ctx_large_block(const PartialsParams& P, int blk, float* lds) {
   }
 }
 
-template <int D> struct LargeLds {
+template <int D> struct LargeLds {  // two operand tiles
   static constexpr int bytes = 2 * (2 * (D / 32) + D / 16) * 64 * 16;
 };
 constexpr int cmax(int a, int b) { return a > b ? a : b; }
@@ -641,7 +695,7 @@ __device__ __forceinline__ void partials_body(const PartialsParams& P) {
   const int bid = blockIdx.x;
   if constexpr (CTX == kCtxLarge) {
     if (bid < P.n_ctx_blocks) {
-      ctx_large_block<D>(P, xcd_logical(bid, P.n_ctx_blocks), reinterpret_cast<float*>(lds));
+      ctx_large_block<D>(P, xcd_logical(bid, P.n_ctx_blocks), lds);
       return;
     }
   }
@@ -671,7 +725,7 @@ __global__ __launch_bounds__(kThreads) void partials_kernel(PartialsParams P) {
 }
 template <int D, int CTX, int NTD>
 constexpr bool fits_two_waves() {
-  return CTX != kCtxLarge && CTX != kCtxSmall4 && NTD <= 2;
+  return CTX != kCtxSmall4 && NTD <= 2;
 }
 
 // Combine (the joint softmax of Eq. 3-4): one wave per output row (i, j)
@@ -723,8 +777,7 @@ __global__ __launch_bounds__(256) void combine_kernel(CombineParams C) {
     const float2 ml = k < np ? (k < C.S_c ? C.ctx_ml[idx(k)] : C.dec_ml[idx(k)])
                              : float2{kNegInf, 0.f};
     float cm = ml.x;
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) cm = fmaxf(cm, __shfl_xor(cm, o));
+    cm = wave_max(cm);
     const float mnew = fmaxf(mx, cm);
     const float base = mnew == kNegInf ? 0.f : mnew;
     const float rescale = exp2_fast(mx - base);  // 0 on the first chunk
@@ -734,8 +787,7 @@ __global__ __launch_bounds__(256) void combine_kernel(CombineParams C) {
     mx = mnew;
     const float w = exp2_fast(ml.x - base);      // 0 for padding lanes
     float lw = w * ml.y;
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) lw += __shfl_xor(lw, o);
+    lw = wave_sum(lw);
     L += lw;
     for (int kb = 0; kb < kn; kb += BATCH) {
       if (kb > 0) {

@@ -57,6 +57,8 @@ def _create(L, *dims):
     ((4, 4, 4, 96, 128, 16, 0.0), bif.EUNSUPPORTED),  # d not 64/128
     ((4, 128, 1, 128, 128, 16, 0.0), bif.EUNSUPPORTED),  # p = 128 > 64
     ((2**30, 2**30, 2**30, 128, 128, 16, 0.0), bif.EINVAL),  # overflowing sizes
+    ((1, 32, 32, 128, 2**23, 0, 0.0), bif.EUNSUPPORTED),    # one cache past 2^31 bytes
+    ((1, 32, 32, 128, 2**23 - 64, 64, 0.0), bif.EUNSUPPORTED),  # context + decode rows
 ])
 def test_plan_create_rejects_bad_dims_without_a_device(L, dims, expect):
     st, handle = _create(L, *dims)

@@ -107,12 +107,17 @@ def test_b1_equivalence_on_gpu():
         assert_parity(single[0], full[i], f"b=1 sample {i}")
 
 
-def test_explicit_scale():
-    b, h, g, d, m_c, m_d = 3, 8, 4, 64, 200, 40
+@pytest.mark.parametrize("scale", [0.05, -0.08])
+@pytest.mark.parametrize("shape", [(3, 8, 4, 64, 200, 40), (4, 32, 1, 128, 300, 50)],
+                         ids=["few_rows", "many_rows"])
+def test_explicit_scale(shape, scale):
+    """A caller-given scale, including a negative one (the kernels then negate
+    q, exactly), on the few-row and the many-row context paths."""
+    b, h, g, d, m_c, m_d = shape
     x = workloads.make_inputs(b, h, g, d, m_c, m_d, seed=74, ragged=True)
-    out = run_decode(x, scale=0.05)
-    ref = oracle.attention(**x, scale=0.05)
-    assert_parity(out, ref, "scale 0.05")
+    out = run_decode(x, scale=scale)
+    ref = oracle.attention(**x, scale=scale)
+    assert_parity(out, ref, f"scale {scale}")
 
 
 def test_out_of_range_lengths_are_clamped_and_flagged():
