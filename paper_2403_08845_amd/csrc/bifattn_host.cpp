@@ -4,6 +4,7 @@
 
 #include <hip/hip_runtime_api.h>
 
+#include <algorithm>
 #include <cmath>
 #include <cstdint>
 #include <cstdlib>
@@ -76,9 +77,13 @@ bifattn_status_t plan_splits(bifattn_plan_s* P) {
   const int64_t units = (int64_t)d.b * d.g;
   if (M <= 64) {
     // Few rows per group: S_c work-groups per group, interleaved over the
-    // group's tiles; 1024 keys each by default (twice a decode work-group).
+    // group's tiles; about four of them, each with 1024..2048 keys (2-4
+    // decode work-groups' worth): fewer, longer context work-groups leave
+    // fewer partials to merge, too few stop covering the decode part's time.
     P->ctx_mode = M <= 16 ? kCtxSmall1 : (M <= 32 ? kCtxSmall2 : kCtxSmall4);
-    const int keys = (int)round_up(env_int("BIFATTN_CTX_KEYS", 1024), kWaves * kTileKeys);
+    const int64_t quarter = round_up(ceil_div(d.m_c, 4), kWaves * kTileKeys);
+    const int def_keys = (int)std::min<int64_t>(2048, std::max<int64_t>(1024, quarter));
+    const int keys = (int)round_up(env_int("BIFATTN_CTX_KEYS", def_keys), kWaves * kTileKeys);
     P->ctx_keys = keys;
     P->ctx_row_blocks = 1;
   } else {

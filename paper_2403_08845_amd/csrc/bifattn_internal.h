@@ -17,7 +17,7 @@ constexpr int kTileKeys = 32;
 constexpr int kRowsPerTile = 16;
 // Context path with many query rows per group: query tiles per wave.
 constexpr int kLargeTilesPerWave = 2;
-constexpr int kLargeRowsPerBlock = kWaves * kLargeTilesPerWave * kRowsPerTile;  // 256
+constexpr int kLargeRowsPerBlock = kWaves * kLargeTilesPerWave * kRowsPerTile;  // 128
 // Largest group size the per-sample decode path holds in registers.
 constexpr int kMaxP = 64;
 // Lazy softmax rescaling: the running reference maximum is only raised when a
