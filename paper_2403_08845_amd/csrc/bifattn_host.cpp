@@ -60,8 +60,18 @@ int env_int(const char* name, int fallback) {
 
 bool aligned(const void* ptr, uintptr_t a) { return ((uintptr_t)ptr & (a - 1)) == 0; }
 
-// Keys one decode (or replicated) work-group reads: `start` by default,
-// halved (down to 128) while fewer than two work-groups per CU would exist.
+// Keys one decode work-group reads: the whole decode cache up to 1024 keys
+// (each work-group writes partials for p rows per wave, so short chunks
+// multiply that traffic, and ragged lengths leave short chunks nearly empty),
+// halved (down to 128) only while fewer than half as many work-groups as
+// CUs would exist.
+int dec_chunk_keys(int64_t units, int64_t rows) {
+  int keys = (int)std::min<int64_t>(1024, std::max<int64_t>(128, round_up(rows, 128)));
+  while (keys > 128 && units * ceil_div(rows, keys) < kCUs / 2) keys /= 2;
+  return keys;
+}
+// Keys one replicated-ablation work-group reads: `start` by default, halved
+// (down to 128) while fewer than two work-groups per CU would exist.
 int seq_keys(int64_t units, int64_t rows, int start) {
   int keys = start;
   while (keys > 128 && units * ceil_div(rows, keys) < 2 * kCUs) keys /= 2;
@@ -87,9 +97,8 @@ bifattn_status_t plan_splits(bifattn_plan_s* P) {
     P->ctx_keys = keys;
     P->ctx_row_blocks = 1;
   } else {
-    // Many rows: work-groups of 128 rows share each staged K_c/V_c tile;
-    // about two work-groups per CU, so that one computes while the other
-    // waits on its loads and barriers.
+    // Many rows: eight-wave work-groups of 128 rows share each staged
+    // K_c/V_c tile; about two work-groups per CU (four waves per SIMD).
     P->ctx_mode = kCtxLarge;
     P->ctx_row_blocks = (int)ceil_div(M, kLargeRowsPerBlock);
     int64_t splits = ceil_div(2 * kCUs, (int64_t)d.g * P->ctx_row_blocks);
@@ -101,7 +110,7 @@ bifattn_status_t plan_splits(bifattn_plan_s* P) {
   P->n_ctx_blocks = P->ctx_mode == kCtxLarge ? d.g * P->S_c * P->ctx_row_blocks : 0;
   P->n_ctx_small_blocks = P->ctx_mode == kCtxLarge ? 0 : d.g * P->S_c;
   if (d.m_d_max > 0) {
-    P->dec_keys = (int)round_up(env_int("BIFATTN_DEC_KEYS", seq_keys(units, d.m_d_max, 512)),
+    P->dec_keys = (int)round_up(env_int("BIFATTN_DEC_KEYS", dec_chunk_keys(units, d.m_d_max)),
                                 kTileKeys);
     P->S_d = (int)ceil_div(d.m_d_max, P->dec_keys);
   } else {
@@ -114,11 +123,12 @@ bifattn_status_t plan_splits(bifattn_plan_s* P) {
                               kTileKeys);
   P->S_r = (int)ceil_div(rep_rows, P->rep_keys);
   P->n_rep_blocks = (int)(units * P->S_r);
-  // Context and decode work-groups share one launch, so that the decode
-  // part's HBM streaming overlaps the context part (compute-bound when many
-  // rows share it). BIFATTN_LAUNCH=2 splits them into two launches.
+  // Few-row context and decode work-groups share one launch (the context
+  // part then overlaps the decode part's streaming); BIFATTN_LAUNCH=2 splits
+  // them into two launches. The many-row context path has a kernel of its
+  // own (eight-wave work-groups), launched before the decode work-groups.
   const int launch = env_int("BIFATTN_LAUNCH", 1);
-  P->fused = launch == 1 ? 1 : 0;
+  P->fused = launch == 1 && P->ctx_mode != kCtxLarge ? 1 : 0;
   if ((int64_t)P->n_ctx_blocks + P->n_ctx_small_blocks + P->n_dec_blocks > INT32_MAX / 2 ||
       units * P->S_r > INT32_MAX / 2)
     return BIFATTN_EINVAL;
@@ -335,21 +345,27 @@ bifattn_status_t bifattn_decode(bifattn_plan_t P, const void* q, const void* Kc,
   K.S_d = P->S_d;
   TimedSection whole(P, BIFATTN_KERNEL_CALL, stream);
   TimedSection part(P, BIFATTN_KERNEL_PARTIALS, stream);
-  hipError_t e;
-  K.n_ctx_blocks = P->n_ctx_blocks;
-  K.n_ctx_small_blocks = P->n_ctx_small_blocks;
-  if (P->fused) {
+  hipError_t e = hipSuccess;
+  K.n_ctx_blocks = 0;
+  K.n_ctx_small_blocks = 0;
+  K.n_dec_blocks = 0;
+  if (P->ctx_mode == kCtxLarge) {
+    // The many-row context kernel, then the decode work-groups.
+    K.n_ctx_blocks = P->n_ctx_blocks;
+    e = launch_ctx_large(K, P->dims.d, stream);
+    K.n_ctx_blocks = 0;
+    K.n_dec_blocks = P->n_dec_blocks;
+    if (e == hipSuccess) e = launch_partials(K, P->dims.d, kCtxNone, P->dec_tiles, stream);
+  } else if (P->fused) {
+    K.n_ctx_small_blocks = P->n_ctx_small_blocks;
     K.n_dec_blocks = P->n_dec_blocks;
     e = launch_partials(K, P->dims.d, P->ctx_mode, P->dec_tiles, stream);
   } else {
-    K.n_dec_blocks = 0;
+    K.n_ctx_small_blocks = P->n_ctx_small_blocks;
     e = launch_partials(K, P->dims.d, P->ctx_mode, P->dec_tiles, stream);
-    if (e == hipSuccess && P->n_dec_blocks) {
-      K.n_ctx_blocks = 0;
-      K.n_ctx_small_blocks = 0;
-      K.n_dec_blocks = P->n_dec_blocks;
-      e = launch_partials(K, P->dims.d, kCtxNone, P->dec_tiles, stream);
-    }
+    K.n_ctx_small_blocks = 0;
+    K.n_dec_blocks = P->n_dec_blocks;
+    if (e == hipSuccess) e = launch_partials(K, P->dims.d, kCtxNone, P->dec_tiles, stream);
   }
   part.end();
   if (e != hipSuccess) return BIFATTN_EHIP;

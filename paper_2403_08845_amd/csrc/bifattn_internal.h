@@ -15,9 +15,11 @@ constexpr int kThreads = 64 * kWaves;
 constexpr int kTileKeys = 32;
 // Query rows per MFMA N-tile.
 constexpr int kRowsPerTile = 16;
-// Context path with many query rows per group: query tiles per wave.
-constexpr int kLargeTilesPerWave = 2;
-constexpr int kLargeRowsPerBlock = kWaves * kLargeTilesPerWave * kRowsPerTile;  // 128
+// Context path with many query rows per group: work-groups of eight waves,
+// one 16-row query tile each.
+constexpr int kLargeWaves = 8;
+constexpr int kLargeThreads = 64 * kLargeWaves;
+constexpr int kLargeRowsPerBlock = kLargeWaves * kRowsPerTile;  // 128
 // Largest group size the per-sample decode path holds in registers.
 constexpr int kMaxP = 64;
 // Lazy softmax rescaling: the running reference maximum is only raised when a
@@ -81,5 +83,7 @@ enum CtxMode { kCtxNone = 0, kCtxSmall1 = 1, kCtxSmall2 = 2, kCtxSmall4 = 4, kCt
 hipError_t launch_partials(const PartialsParams& P, int d, int ctx_mode, int dec_tiles,
                            hipStream_t stream);
 hipError_t launch_combine(const CombineParams& C, int d, hipStream_t stream);
+// Launch the many-row context kernel over n_ctx_blocks work-groups.
+hipError_t launch_ctx_large(const PartialsParams& P, int d, hipStream_t stream);
 
 }  // namespace bifattn

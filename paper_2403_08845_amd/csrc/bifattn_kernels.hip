@@ -191,16 +191,18 @@ __device__ __forceinline__ void tile_update(RowState<D, NT>& st, KOp&& k_at, VOp
       sacc[nt][1] = mfma_bf16(k1, qo, sacc[nt][1]);
     }
   }
-  u32x4 pb[NT];
+  // Row maxima of every query tile (raw logits; scale_log2 > 0, so the max
+  // can be taken before scaling and the scale folds into the exponent's
+  // multiply-add), then one rescale branch for the whole tile.
+  float x[NT][8];  // x[nt][e]: key 4e + G
+  float tmax[NT];
+  bool raise_any = false;
 #pragma unroll
   for (int nt = 0; nt < NT; ++nt) {
-    // Raw logits; scale_log2 > 0, so the row max can be taken before scaling
-    // and the scale folds into the exponent's multiply-add.
-    float x[8];  // x[e]: key 4e + G
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-      x[j] = sacc[nt][0][j];
-      x[4 + j] = sacc[nt][1][j];
+      x[nt][j] = sacc[nt][0][j];
+      x[nt][4 + j] = sacc[nt][1][j];
     }
     if (nvalid < kTileKeys) {
       // The bound passes through readfirstlane (convergent), so the compiler
@@ -208,37 +210,77 @@ __device__ __forceinline__ void tile_update(RowState<D, NT>& st, KOp&& k_at, VOp
       const int nv = __builtin_amdgcn_readfirstlane(nvalid);
 #pragma unroll
       for (int e = 0; e < 8; ++e)
-        if (4 * e + G >= nv) x[e] = kNegInf;
+        if (4 * e + G >= nv) x[nt][e] = kNegInf;
     }
-    float tmax = x[0];
+    float m = x[nt][0];
 #pragma unroll
-    for (int e = 1; e < 8; ++e) tmax = fmaxf(tmax, x[e]);
-    tmax = xor32_max(xor16_max(tmax)) * scale_log2;
-    const bool raise = tmax > st.mref[nt] + kRescaleSlack;
-    if (__any(raise)) {
+    for (int e = 1; e < 8; ++e) m = fmaxf(m, x[nt][e]);
+    tmax[nt] = xor32_max(xor16_max(m)) * scale_log2;
+    raise_any |= tmax[nt] > st.mref[nt] + kRescaleSlack;
+  }
+  if (__any(raise_any)) {
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) {
       // Rows that do not raise keep alpha = 1 (and never form -inf - -inf).
-      const float alpha = raise ? exp2_fast(st.mref[nt] - tmax) : 1.f;  // 0 when mref = -inf
+      const bool raise = tmax[nt] > st.mref[nt] + kRescaleSlack;
+      const float alpha = raise ? exp2_fast(st.mref[nt] - tmax[nt]) : 1.f;  // 0 when mref = -inf
       st.l[nt] *= alpha;
 #pragma unroll
       for (int t = 0; t < DV; ++t) st.acc[nt][t] *= alpha;
-      st.mref[nt] = raise ? tmax : st.mref[nt];
+      st.mref[nt] = raise ? tmax[nt] : st.mref[nt];
     }
+  }
+  auto weights = [&](int nt) -> u32x4 {  // bf16 P^T operand of query tile nt; adds to l
     const float nbase = st.mref[nt] == kNegInf ? 0.f : -st.mref[nt];
     float pr[8];
 #pragma unroll
-    for (int e = 0; e < 8; ++e) pr[e] = exp2_fast(__builtin_fmaf(x[e], scale_log2, nbase));
+    for (int e = 0; e < 8; ++e) pr[e] = exp2_fast(__builtin_fmaf(x[nt][e], scale_log2, nbase));
     float psum = pr[0];
 #pragma unroll
     for (int e = 1; e < 8; ++e) psum += pr[e];
     st.l[nt] += psum;
+    u32x4 pb;
 #pragma unroll
-    for (int w = 0; w < 4; ++w) pb[nt][w] = pack_bf16(pr[2 * w], pr[2 * w + 1]);
-  }
+    for (int w = 0; w < 4; ++w) pb[w] = pack_bf16(pr[2 * w], pr[2 * w + 1]);
+    return pb;
+  };
+  if constexpr (NT == 2) {
+    // O^T += V^T P^T query tile by query tile, the V^T operands held. Tile
+    // 1's weights do not depend on tile 0's products: they are scheduled
+    // between them, so the exponentials issue while the matrix cores run
+    // (sched_barrier fences the regions; group masks: 0x2 VALU, 0x8 MFMA).
+    u32x4 vo[DV];
 #pragma unroll
-  for (int t = 0; t < DV; ++t) {
-    const u32x4 v = vop_at(t);
+    for (int t = 0; t < DV; ++t) vo[t] = vop_at(t);
+    const u32x4 pb0 = weights(0);
+    __builtin_amdgcn_sched_barrier(0);
+    const u32x4 pb1 = weights(1);
 #pragma unroll
-    for (int nt = 0; nt < NT; ++nt) st.acc[nt][t] = mfma_bf16(v, pb[nt], st.acc[nt][t]);
+    for (int t = 0; t < DV; ++t) st.acc[0][t] = mfma_bf16(vo[t], pb0, st.acc[0][t]);
+#pragma unroll
+    for (int t = 0; t < DV; ++t) {
+      __builtin_amdgcn_sched_group_barrier(0x8, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x2, 4, 0);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int t = 0; t < DV; ++t) st.acc[1][t] = mfma_bf16(vo[t], pb1, st.acc[1][t]);
+  } else if constexpr (NT == 1) {
+    const u32x4 pb = weights(0);
+#pragma unroll
+    for (int t = 0; t < DV; ++t) st.acc[0][t] = mfma_bf16(vop_at(t), pb, st.acc[0][t]);
+  } else {
+    // Many query tiles: registers are short, so each V^T operand is formed
+    // once and used for every tile.
+    u32x4 pb[NT];
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) pb[nt] = weights(nt);
+#pragma unroll
+    for (int t = 0; t < DV; ++t) {
+      const u32x4 v = vop_at(t);
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt) st.acc[nt][t] = mfma_bf16(v, pb[nt], st.acc[nt][t]);
+    }
   }
 }
 
@@ -559,115 +601,6 @@ __device__ void ctx_small_block(const PartialsParams& P, int blk, int wave, int 
   merge_waves_and_store<D, NT>(st, merge_lds, M, P.ctx_acc + prow * D, P.ctx_ml + prow, wave, lane);
 }
 
-// Context part, many query rows per group: work-group (group gam, key split
-// s, row block rb) of 128 query rows, 32 per wave, two work-groups per CU.
-// Each 32-key tile of Kc/Vc is loaded from HBM once per work-group into LDS,
-// already in MFMA operand order (the V^T transpose is done once, on the way
-// in), and all four waves read it for their rows. Double-buffered with one
-// barrier per tile: the next tile's global loads are in flight while the
-// current one is consumed, and written to the other buffer after it. Q^T
-// operands stay in registers. Row blocks of one key chunk are scheduled on
-// the same XCD so that they share its L2.
-template <int D>
-__device__ void ctx_large_block(const PartialsParams& P, int blk, u32x4* lds) {
-  constexpr int KS = D / 32;
-  constexpr int DV = D / 16;
-  constexpr int NT = kLargeTilesPerWave;
-  constexpr int KOPS = 2 * KS;             // K operands per tile
-  constexpr int KPW = KOPS / kWaves;       // K operands each wave stages
-  constexpr int OPS = KOPS + DV;           // operands per tile (16 B per lane each)
-  typedef typename VSlice<D>::type VS;
-  const int rb = blk % P.ctx_row_blocks;
-  const int sg = blk / P.ctx_row_blocks;
-  const int s = sg % P.S_c, gam = sg / P.S_c;
-  const int k0 = s * P.ctx_keys;
-  const int k1 = min(P.m_c, k0 + P.ctx_keys);
-  const int lane = threadIdx.x & 63, wave = wave_id();
-  const int r = lane & 15, G = lane >> 4;
-  // Buffer resources over the chunk's keys [k0, k1): rows past it load as
-  // zero with no memory access and no branch. Offsets count from k0.
-  const size_t chunk = ((size_t)gam * P.m_c + k0) * D;
-  const __amdgpu_buffer_rsrc_t rk = rows_rsrc<D>(P.Kc + chunk, k1 - k0);
-  const __amdgpu_buffer_rsrc_t rv = rows_rsrc<D>(P.Vc + chunk, k1 - k0);
-  const int M = P.M, p = P.p, h = P.h;
-  const int row0 = rb * kLargeRowsPerBlock + wave * NT * kRowsPerTile;
-  const uint16_t* q = P.q;
-  // LDS: two buffers of OPS operand slots x 64 lanes x 16 B.
-  auto slot = [&](int buf, int op) -> u32x4* { return lds + ((size_t)buf * OPS + op) * 64; };
-
-  // Staging registers of the next tile: this wave's K operands and two value rows.
-  u32x4 kst[KPW];
-  VS vst[2];
-  auto fetch = [&](int key0) {
-#pragma unroll
-    for (int c = 0; c < KPW; ++c) {
-      const int op = wave * KPW + c, a = op / KS, ss = op % KS;
-      kst[c] = __builtin_amdgcn_raw_buffer_load_b128(
-          rk, ((key0 + qk_key(a, r)) * D + ss * 32 + G * 8) * 2, 0, 0);
-    }
-#pragma unroll
-    for (int c = 0; c < 2; ++c)
-      vst[c] = VSlice<D>::load_buf(rv, ((key0 + 4 * (2 * wave + c) + G) * D + DV * r) * 2);
-  };
-  auto stage = [&](int buf) {
-#pragma unroll
-    for (int c = 0; c < KPW; ++c) slot(buf, wave * KPW + c)[lane] = kst[c];
-    // word `wave` of V^T operand t = keys 4(2*wave) + G, 4(2*wave+1) + G at dim DV*r + t
-#pragma unroll
-    for (int t = 0; t < DV; ++t)
-      reinterpret_cast<uint32_t*>(slot(buf, KOPS + t) + lane)[wave] =
-          pair_elem(vword(vst[0], t), vword(vst[1], t), t);
-  };
-
-  fetch(0);  // first tile in flight while Q is loaded
-  u32x4 qop[NT][KS];
-  load_q<D, NT>(qop, [&](int rr) -> const uint16_t* {
-    const int row = row0 + rr;
-    if (row >= M) return nullptr;
-    const int i = row / p, jp = row - i * p;
-    return q + ((size_t)i * h + (size_t)gam * p + jp) * D;
-  }, P.q_sign, lane);
-  RowState<D, NT> st;
-  st.init();
-  const int ntiles = (k1 - k0 + kTileKeys - 1) / kTileKeys;
-  stage(0);
-  __syncthreads();
-  for (int it = 0; it < ntiles; ++it) {
-    const int buf = it & 1;
-    if (it + 1 < ntiles) fetch((it + 1) * kTileKeys);
-    const int nvalid = min(kTileKeys, k1 - (k0 + it * kTileKeys));
-    tile_update<D, NT>(st, [&](int a, int ss) { return slot(buf, a * KS + ss)[lane]; },
-                       [&](int t) { return slot(buf, KOPS + t)[lane]; },
-                       [&](int nt, int ss) { return qop[nt][ss]; }, nvalid, P.scale_log2, lane);
-    // The other buffer was last read in the previous iteration, before the
-    // barrier that ended it.
-    if (it + 1 < ntiles) stage(buf ^ 1);
-    __syncthreads();
-  }
-  finish_sums(st);
-  const size_t pbase = ((size_t)gam * P.S_c + s) * P.M;
-#pragma unroll
-  for (int nt = 0; nt < NT; ++nt) {
-    const int row = row0 + nt * kRowsPerTile + r;
-    if (row < M) {
-      float* dst = P.ctx_acc + (pbase + row) * D + 4 * DV * G;
-#pragma unroll
-      for (int j = 0; j < 4; ++j)
-#pragma unroll
-        for (int t4 = 0; t4 < DV; t4 += 4)
-          *reinterpret_cast<f32x4*>(dst + DV * j + t4) =
-              f32x4{st.acc[nt][t4][j], st.acc[nt][t4 + 1][j], st.acc[nt][t4 + 2][j],
-                    st.acc[nt][t4 + 3][j]};
-      if (G == 0) P.ctx_ml[pbase + row] = float2{st.mref[nt], st.l[nt]};
-    }
-  }
-}
-
-template <int D> struct LargeLds {  // two operand tiles
-  static constexpr int bytes = 2 * (2 * (D / 32) + D / 16) * 64 * 16;
-};
-constexpr int cmax(int a, int b) { return a > b ? a : b; }
-
 // XCD-aware order for the large context path: the hardware hands work-group
 // ids to the 8 XCDs round robin, so logical ids that must share an L2 (the
 // row blocks of one key chunk) are spread with stride 8 in dispatch order.
@@ -678,31 +611,176 @@ __device__ __forceinline__ int xcd_logical(int bid, int n) {
   return (bid % X) * per + bid / X;
 }
 
-// Grid: n_ctx_blocks work-groups of the many-row context path, then
-// n_ctx_small_blocks of the few-row context path, then n_dec_blocks decode
-// work-groups.
+// Value-slice half: the HW = d/32 dimensions DV*r + vh*HW .. + HW of a value
+// row that one wave of the many-row context kernel stages per lane.
+template <int D> struct VHalf;
+template <> struct VHalf<128> {
+  typedef u32x2 type;
+  static __device__ __forceinline__ type load(__amdgpu_buffer_rsrc_t r, int off) {
+    return __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, 0);
+  }
+  static __device__ __forceinline__ uint32_t word(const type& v, int t) { return v[t >> 1]; }
+};
+template <> struct VHalf<64> {
+  typedef uint32_t type;
+  static __device__ __forceinline__ type load(__amdgpu_buffer_rsrc_t r, int off) {
+    return __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, 0);
+  }
+  static __device__ __forceinline__ uint32_t word(const type& v, int) { return v; }
+};
+
+// Context part, many query rows per group: work-group (group gam, key split
+// s, row block rb) of 128 query rows, eight waves with one 16-row query
+// tile each, two work-groups per CU (four waves per SIMD, so one wave's
+// softmax arithmetic overlaps another's matrix products and waits).
+// Each 32-key tile of Kc/Vc is loaded from HBM once per work-group into LDS,
+// already in MFMA operand order (the V^T transpose is done once, on the way
+// in), and all eight waves read it. Each wave stages one eighth of a tile:
+// one K operand (d = 128; the first four waves for d = 64) and one 32-bit
+// word of half of the V^T operands. Tiles are double-buffered in LDS with
+// one barrier per tile, and fetched two tiles ahead into two rotating
+// register sets. Q^T operands stay in registers. Row blocks of one key
+// chunk are scheduled on the same XCD so that they share its L2.
+template <int D>
+__device__ __forceinline__ void ctx_large_body(const PartialsParams& P) {
+  constexpr int KS = D / 32;
+  constexpr int DV = D / 16;
+  constexpr int KOPS = 2 * KS;  // K operands per tile
+  constexpr int OPS = KOPS + DV;  // operands per tile (16 B per lane each)
+  constexpr int HW = DV / 2;      // V^T operands one wave stages a word of
+  typedef typename VHalf<D>::type VH;
+  __shared__ __attribute__((aligned(16))) u32x4 lds[2 * OPS * 64];
+  const int blk = xcd_logical(blockIdx.x, P.n_ctx_blocks);
+  const int rb = blk % P.ctx_row_blocks;
+  const int sg = blk / P.ctx_row_blocks;
+  const int s = sg % P.S_c, gam = sg / P.S_c;
+  const int k0 = s * P.ctx_keys;
+  const int nkeys = min(P.m_c, k0 + P.ctx_keys) - k0;
+  const int lane = threadIdx.x & 63, wave = wave_id();
+  const int r = lane & 15, G = lane >> 4;
+  // Buffer resources over the chunk's keys [k0, k0 + nkeys): rows past it
+  // load as zero with no memory access and no branch. Offsets count from k0.
+  const size_t chunk = ((size_t)gam * P.m_c + k0) * D;
+  const __amdgpu_buffer_rsrc_t rk = rows_rsrc<D>(P.Kc + chunk, nkeys);
+  const __amdgpu_buffer_rsrc_t rv = rows_rsrc<D>(P.Vc + chunk, nkeys);
+  const int M = P.M, p = P.p, h = P.h;
+  const int row0 = rb * kLargeRowsPerBlock + wave * kRowsPerTile;
+  auto slot = [&](int buf, int op) -> u32x4* { return lds + (buf * OPS + op) * 64; };
+  const bool has_k = wave < KOPS;              // wave-uniform
+  const int ka = wave / KS, kss = wave % KS;   // the K operand this wave stages
+  const int vw = wave & 3, vh = wave >> 2;     // its V^T word and operand half
+
+  // Registers of a tile in flight: this wave's K operand and two value-row halves.
+  struct Stage {
+    u32x4 k;
+    VH v[2];
+  };
+  auto fetch = [&](Stage& g, int key0) {  // keys past the chunk load as zero
+    if (has_k)
+      g.k = __builtin_amdgcn_raw_buffer_load_b128(
+          rk, ((key0 + qk_key(ka, r)) * D + kss * 32 + G * 8) * 2, 0, 0);
+#pragma unroll
+    for (int c = 0; c < 2; ++c)
+      g.v[c] = VHalf<D>::load(rv, ((key0 + 4 * (2 * vw + c) + G) * D + DV * r + vh * HW) * 2);
+  };
+  auto stage = [&](const Stage& g, int buf) {
+    if (has_k) slot(buf, wave)[lane] = g.k;
+    // word vw of V^T operand vh*HW + t = keys 4(2vw) + G, 4(2vw+1) + G at dim DV*r + vh*HW + t
+#pragma unroll
+    for (int t = 0; t < HW; ++t)
+      reinterpret_cast<uint32_t*>(slot(buf, KOPS + vh * HW + t) + lane)[vw] =
+          pair_elem(VHalf<D>::word(g.v[0], t), VHalf<D>::word(g.v[1], t), t);
+  };
+
+  // Q first, then the first two tiles: the wait for the first tile then also
+  // covers Q, so no wait inside the loop reaches past the set in flight.
+  u32x4 qop[1][KS];
+  load_q<D, 1>(qop, [&](int rr) -> const uint16_t* {
+    const int row = row0 + rr;
+    if (row >= M) return nullptr;
+    const int i = row / p, jp = row - i * p;
+    return P.q + ((size_t)i * h + (size_t)gam * p + jp) * D;
+  }, P.q_sign, lane);
+  Stage A, B;
+  fetch(A, 0);
+  fetch(B, kTileKeys);
+  RowState<D, 1> st;
+  st.init();
+  const bool rows = row0 < M;  // wave-uniform: waves past the last row only stage
+  stage(A, 0);
+  __syncthreads();
+  // Tile `key` (in LDS buffer buf) is consumed while the next tile is in
+  // flight in one register set and the one after that is issued into the
+  // other; fetches past the chunk are unconditional (they read zeros), so
+  // every wait covers exactly one set. The loop runs while two more tiles
+  // follow (a single exit at the bottom keeps the waits exact); the last one
+  // or two tiles are the tail.
+  auto step = [&](int key, int buf, Stage& next, Stage& spare, bool stage_next) {
+    fetch(spare, key + 2 * kTileKeys);
+    if (rows)
+      tile_update<D, 1>(st, [&](int a, int ss) { return slot(buf, a * KS + ss)[lane]; },
+                        [&](int t) { return slot(buf, KOPS + t)[lane]; },
+                        [&](int, int ss) { return qop[0][ss]; }, min(kTileKeys, nkeys - key),
+                        P.scale_log2, lane);
+    if (stage_next) {
+      // The other buffer was last read in the previous step, before the
+      // barrier that ended it.
+      stage(next, buf ^ 1);
+      __syncthreads();
+    }
+  };
+  int key = 0;
+  for (; key + 2 * kTileKeys < nkeys; key += 2 * kTileKeys) {
+    step(key, 0, B, A, true);
+    step(key + kTileKeys, 1, A, B, true);
+  }
+  const bool two = key + kTileKeys < nkeys;
+  step(key, 0, B, A, two);
+  if (two) step(key + kTileKeys, 1, A, B, false);
+
+  finish_sums(st);
+  const int row = row0 + r;
+  if (row < M) {
+    const size_t prow = ((size_t)gam * P.S_c + s) * P.M + row;
+    float* dst = P.ctx_acc + prow * D + 4 * DV * G;
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+      for (int t4 = 0; t4 < DV; t4 += 4)
+        *reinterpret_cast<f32x4*>(dst + DV * j + t4) =
+            f32x4{st.acc[0][t4][j], st.acc[0][t4 + 1][j], st.acc[0][t4 + 2][j],
+                  st.acc[0][t4 + 3][j]};
+    if (G == 0) P.ctx_ml[prow] = float2{st.mref[0], st.l[0]};
+  }
+}
+
+template <int D>
+__global__ __launch_bounds__(kLargeThreads) __attribute__((amdgpu_waves_per_eu(4))) void
+ctx_large_kernel(PartialsParams P) {
+  ctx_large_body<D>(P);
+}
+
+constexpr int cmax(int a, int b) { return a > b ? a : b; }
+
+
+// Grid: n_ctx_small_blocks work-groups of the few-row context path, then
+// n_dec_blocks decode work-groups (the many-row context path has a kernel of
+// its own).
 template <int D, int CTX, int NTD>
 __device__ __forceinline__ void partials_body(const PartialsParams& P) {
-  constexpr bool kSmall = CTX != kCtxNone && CTX != kCtxLarge;
+  constexpr bool kSmall = CTX != kCtxNone;
   constexpr int NTC = kSmall ? CTX : 1;
   constexpr int NTQ = NTC > NTD ? NTC : NTD;
   constexpr int QSLOTS = kWaves * NTQ * (D / 32) * 64;  // u32x4 slots for Q^T operands
   constexpr int KSLOTS = kWaves * kTileKeys * D / 8;      // one staged K tile per wave
   constexpr int MERGE = kSmall ? (MergeLds<D, NTC>::bytes + 15) / 16 : 0;  // overlays the K tiles
-  constexpr int LDS = CTX == kCtxLarge ? cmax(LargeLds<D>::bytes / 16, QSLOTS + KSLOTS)
-                                       : QSLOTS + cmax(KSLOTS, MERGE);
+  constexpr int LDS = QSLOTS + cmax(KSLOTS, MERGE);
   __shared__ __attribute__((aligned(16))) u32x4 lds[LDS];
   const int bid = blockIdx.x;
-  if constexpr (CTX == kCtxLarge) {
-    if (bid < P.n_ctx_blocks) {
-      ctx_large_block<D>(P, xcd_logical(bid, P.n_ctx_blocks), lds);
-      return;
-    }
-  }
   const int lane = threadIdx.x & 63, wave = wave_id();
   u32x4* qw = lds + wave * NTQ * (D / 32) * 64;
   u32x4* kl = lds + QSLOTS + wave * (kTileKeys * D / 8);
-  const int blk = bid - P.n_ctx_blocks;
+  const int blk = bid;
   if (blk < P.n_ctx_small_blocks) {
     if constexpr (kSmall)
       ctx_small_block<D, NTC>(P, blk, wave, lane, qw, kl, reinterpret_cast<float*>(lds + QSLOTS));
@@ -816,7 +894,7 @@ __global__ __launch_bounds__(256) void combine_kernel(CombineParams C) {
 
 template <int D, int CTX>
 hipError_t launch_partials_ctx(const PartialsParams& P, int dec_tiles, hipStream_t stream) {
-  const int grid = P.n_ctx_blocks + P.n_ctx_small_blocks + P.n_dec_blocks;
+  const int grid = P.n_ctx_small_blocks + P.n_dec_blocks;
   if (grid == 0) return hipSuccess;
   switch (dec_tiles) {
     case 1:
@@ -845,13 +923,22 @@ hipError_t launch_partials_d(const PartialsParams& P, int ctx_mode, int dec_tile
     case kCtxSmall1: return launch_partials_ctx<D, kCtxSmall1>(P, dec_tiles, stream);
     case kCtxSmall2: return launch_partials_ctx<D, kCtxSmall2>(P, dec_tiles, stream);
     case kCtxSmall4: return launch_partials_ctx<D, kCtxSmall4>(P, dec_tiles, stream);
-    case kCtxLarge: return launch_partials_ctx<D, kCtxLarge>(P, dec_tiles, stream);
     default: return hipErrorInvalidValue;
   }
 }
 
 }  // namespace
 
+hipError_t launch_ctx_large(const PartialsParams& P, int d, hipStream_t stream) {
+  if (P.n_ctx_blocks == 0) return hipSuccess;
+  if (d == 128)
+    ctx_large_kernel<128><<<P.n_ctx_blocks, kLargeThreads, 0, stream>>>(P);
+  else if (d == 64)
+    ctx_large_kernel<64><<<P.n_ctx_blocks, kLargeThreads, 0, stream>>>(P);
+  else
+    return hipErrorInvalidValue;
+  return hipGetLastError();
+}
 hipError_t launch_partials(const PartialsParams& P, int d, int ctx_mode, int dec_tiles,
                            hipStream_t stream) {
   if (d == 128) return launch_partials_d<128>(P, ctx_mode, dec_tiles, stream);
