@@ -154,12 +154,14 @@ __device__ __forceinline__ uint32_t pair_elem(uint32_t even_w, uint32_t odd_w, i
 template <int D, int NT> struct RowState {
   static constexpr int DV = D / 16;
   float mref[NT];       // reference maximum (log2 units), uniform over the row's 4 lanes
+  float thr[NT];        // raw-logit threshold: a logit above it calls for a higher mref
   float l[NT];          // this lane's share of the row sum
   f32x4 acc[NT][DV];    // O^T accumulators
   __device__ __forceinline__ void init() {
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) {
       mref[nt] = kNegInf;
+      thr[nt] = kNegInf;
       l[nt] = 0.f;
 #pragma unroll
       for (int t = 0; t < DV; ++t) acc[nt][t] = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -191,11 +193,14 @@ __device__ __forceinline__ void tile_update(RowState<D, NT>& st, KOp&& k_at, VOp
       sacc[nt][1] = mfma_bf16(k1, qo, sacc[nt][1]);
     }
   }
-  // Row maxima of every query tile (raw logits; scale_log2 > 0, so the max
-  // can be taken before scaling and the scale folds into the exponent's
-  // multiply-add), then one rescale branch for the whole tile.
+  // Raw logits; scale_log2 > 0, so maxima can be taken before scaling and
+  // the scale folds into the exponent's multiply-add. The reference maximum
+  // only has to bound the row's logits to within 2^kRescaleSlack (the same
+  // reference scales its weights, sum and values): each lane compares its
+  // own maximum with the threshold, and only when some lane exceeds it does
+  // the wave form exact row maxima across lanes and rescale.
   float x[NT][8];  // x[nt][e]: key 4e + G
-  float tmax[NT];
+  float lmax[NT];
   bool raise_any = false;
 #pragma unroll
   for (int nt = 0; nt < NT; ++nt) {
@@ -215,19 +220,21 @@ __device__ __forceinline__ void tile_update(RowState<D, NT>& st, KOp&& k_at, VOp
     float m = x[nt][0];
 #pragma unroll
     for (int e = 1; e < 8; ++e) m = fmaxf(m, x[nt][e]);
-    tmax[nt] = xor32_max(xor16_max(m)) * scale_log2;
-    raise_any |= tmax[nt] > st.mref[nt] + kRescaleSlack;
+    lmax[nt] = m;
+    raise_any |= m > st.thr[nt];
   }
   if (__any(raise_any)) {
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) {
+      const float tmax = xor32_max(xor16_max(lmax[nt])) * scale_log2;  // exact row maximum
       // Rows that do not raise keep alpha = 1 (and never form -inf - -inf).
-      const bool raise = tmax[nt] > st.mref[nt] + kRescaleSlack;
-      const float alpha = raise ? exp2_fast(st.mref[nt] - tmax[nt]) : 1.f;  // 0 when mref = -inf
+      const bool raise = tmax > st.mref[nt] + kRescaleSlack;
+      const float alpha = raise ? exp2_fast(st.mref[nt] - tmax) : 1.f;  // 0 when mref = -inf
       st.l[nt] *= alpha;
 #pragma unroll
       for (int t = 0; t < DV; ++t) st.acc[nt][t] *= alpha;
-      st.mref[nt] = raise ? tmax[nt] : st.mref[nt];
+      st.mref[nt] = raise ? tmax : st.mref[nt];
+      st.thr[nt] = (st.mref[nt] + kRescaleSlack) / scale_log2;
     }
   }
   auto weights = [&](int nt) -> u32x4 {  // bf16 P^T operand of query tile nt; adds to l
@@ -383,9 +390,7 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t rows_rsrc(const uint16_t* base
 template <int D, int NT>
 __device__ __forceinline__ void finish_sums(RowState<D, NT>& st) {
 #pragma unroll
-  for (int nt = 0; nt < NT; ++nt) {
-    st.l[nt] = xor32_sum(xor16_sum(st.l[nt]));
-  }
+  for (int nt = 0; nt < NT; ++nt) st.l[nt] = xor32_sum(xor16_sum(st.l[nt]));
 }
 
 // Write the wave's partials of rows row0 + nt*16 + n < nrows: lane (n, G)
