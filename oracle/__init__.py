@@ -51,12 +51,12 @@ def _load():
         i32 = ctypes.POINTER(ctypes.c_int32)
         f64 = ctypes.POINTER(ctypes.c_double)
         ci = ctypes.c_int
-        lib.oracle_attention_fp64.argtypes = [ci, ci, ci, ci, ci, ci, ctypes.c_double,
+        lib.oracle_attention_fp64.argtypes = [ci, ci, ci, ci, ci, ci, ci, ctypes.c_double,
                                               u16, u16, u16, u16, u16, i32, f64, ci]
         lib.oracle_attention_fp64.restype = ci
-        lib.oracle_attention_rows_fp64.argtypes = [ci, ci, ci, ci, ci, ci, ctypes.c_double,
+        lib.oracle_attention_rows_fp64.argtypes = [ci, ci, ci, ci, ci, ci, ci, ctypes.c_double,
                                                    u16, u16, u16, u16, u16, i32, ci, i32, i32,
-                                                   f64, ci]
+                                                   i32, f64, ci]
         lib.oracle_attention_rows_fp64.restype = ci
         lib.oracle_max_threads.restype = ci
         _lib = lib
@@ -68,15 +68,20 @@ def _ptr(a, ctype):
 
 
 def _prep(q, Kc, Vc, Kd, Vd, lens):
+    """q is [b, h, d] (one new token per sample) or [b, h, n, d] (n new tokens)."""
     q, Kc, Vc, Kd, Vd = (np.ascontiguousarray(x, dtype=np.uint16) for x in (q, Kc, Vc, Kd, Vd))
     lens = np.ascontiguousarray(lens, dtype=np.int32)
-    b, h, d = q.shape
+    if q.ndim == 3:
+        b, h, d = q.shape
+        n = 1
+    else:
+        b, h, n, d = q.shape
     g, m_c, d2 = Kc.shape
     b2, g2, m_d_max, d3 = Kd.shape
     if not (d == d2 == d3 and b == b2 and g == g2 and Vc.shape == Kc.shape
             and Vd.shape == Kd.shape and lens.shape == (b,)):
         raise ValueError("inconsistent shapes")
-    return (q, Kc, Vc, Kd, Vd, lens), (b, h, g, d, m_c, m_d_max)
+    return (q, Kc, Vc, Kd, Vd, lens), (b, h, g, d, m_c, m_d_max, n)
 
 
 def default_scale(d: int) -> float:
@@ -86,12 +91,14 @@ def default_scale(d: int) -> float:
 
 
 def attention(q, Kc, Vc, Kd, Vd, lens, scale=None, nthreads=0):
-    """Full fp64 output [b, h, d] (inputs are bf16 bit patterns, uint16)."""
-    arrs, (b, h, g, d, m_c, m_d_max) = _prep(q, Kc, Vc, Kd, Vd, lens)
+    """Full fp64 output, shaped like q: [b, h, d] or [b, h, n, d] (inputs are
+    bf16 bit patterns, uint16). With n tokens per sample, token r sees the
+    first max(0, len_i - n + r + 1) decode rows."""
+    arrs, (b, h, g, d, m_c, m_d_max, n) = _prep(q, Kc, Vc, Kd, Vd, lens)
     scale = default_scale(d) if scale is None else float(scale)
-    out = np.empty((b, h, d), dtype=np.float64)
+    out = np.empty(arrs[0].shape, dtype=np.float64)
     q, Kc, Vc, Kd, Vd, lens = arrs
-    rc = _load().oracle_attention_fp64(b, h, g, d, m_c, m_d_max, scale,
+    rc = _load().oracle_attention_fp64(b, h, g, d, m_c, m_d_max, n, scale,
                                        _ptr(q, ctypes.c_uint16), _ptr(Kc, ctypes.c_uint16),
                                        _ptr(Vc, ctypes.c_uint16), _ptr(Kd, ctypes.c_uint16),
                                        _ptr(Vd, ctypes.c_uint16), _ptr(lens, ctypes.c_int32),
@@ -101,23 +108,25 @@ def attention(q, Kc, Vc, Kd, Vd, lens, scale=None, nthreads=0):
     return out
 
 
-def attention_rows(q, Kc, Vc, Kd, Vd, lens, rows_i, rows_j, scale=None, nthreads=0):
-    """fp64 output rows (sample rows_i[r], head rows_j[r]) -> [nrows, d]."""
-    arrs, (b, h, g, d, m_c, m_d_max) = _prep(q, Kc, Vc, Kd, Vd, lens)
+def attention_rows(q, Kc, Vc, Kd, Vd, lens, rows_i, rows_j, scale=None, nthreads=0, rows_t=None):
+    """fp64 output rows (sample rows_i[r], head rows_j[r], token rows_t[r]
+    (default 0)) -> [nrows, d]."""
+    arrs, (b, h, g, d, m_c, m_d_max, n) = _prep(q, Kc, Vc, Kd, Vd, lens)
     scale = default_scale(d) if scale is None else float(scale)
     ri = np.ascontiguousarray(rows_i, dtype=np.int32)
     rj = np.ascontiguousarray(rows_j, dtype=np.int32)
-    if ri.shape != rj.shape or ri.ndim != 1:
-        raise ValueError("rows_i and rows_j must be 1-D and equally long")
+    rt = np.zeros_like(ri) if rows_t is None else np.ascontiguousarray(rows_t, dtype=np.int32)
+    if ri.shape != rj.shape or rt.shape != ri.shape or ri.ndim != 1:
+        raise ValueError("rows_i, rows_j and rows_t must be 1-D and equally long")
     out = np.empty((ri.size, d), dtype=np.float64)
     q, Kc, Vc, Kd, Vd, lens = arrs
-    rc = _load().oracle_attention_rows_fp64(b, h, g, d, m_c, m_d_max, scale,
+    rc = _load().oracle_attention_rows_fp64(b, h, g, d, m_c, m_d_max, n, scale,
                                             _ptr(q, ctypes.c_uint16), _ptr(Kc, ctypes.c_uint16),
                                             _ptr(Vc, ctypes.c_uint16), _ptr(Kd, ctypes.c_uint16),
                                             _ptr(Vd, ctypes.c_uint16), _ptr(lens, ctypes.c_int32),
                                             int(ri.size), _ptr(ri, ctypes.c_int32),
-                                            _ptr(rj, ctypes.c_int32), _ptr(out, ctypes.c_double),
-                                            int(nthreads))
+                                            _ptr(rj, ctypes.c_int32), _ptr(rt, ctypes.c_int32),
+                                            _ptr(out, ctypes.c_double), int(nthreads))
     if rc:
         raise ValueError(f"oracle: {_ERRORS.get(rc, rc)}")
     return out

@@ -1,7 +1,9 @@
 """Bifurcated attention evaluated as the paper writes it -- TEST INFRASTRUCTURE ONLY.
 
 numpy fp64, following Section 4.2 step by step (notation ``b g p n k``,
-``n = 1`` for incremental decoding, ``k`` = head dimension):
+``n`` new tokens per sample -- 1 for incremental decoding, ``n_g`` draft
+tokens for the speculative decoding of the appendix -- and ``k`` = head
+dimension):
 
 1. Eq. 3, context logits: einsum(bgpnk, g m_c k -> bgpn m_c); the context
    cache has no ``b`` axis because it is shared by all samples.
@@ -24,11 +26,16 @@ from . import default_scale, widen_bf16
 
 
 def bifurcated_attention(q, Kc, Vc, Kd, Vd, lens, scale=None):
+    """q [b, h, k] or [b, h, n, k]; the output has q's shape."""
     qf = widen_bf16(q)
     Kcf, Vcf = widen_bf16(Kc), widen_bf16(Vc)
     Kdf, Vdf = widen_bf16(Kd), widen_bf16(Vd)
     lens = np.asarray(lens, dtype=np.int64)
-    b, h, k = qf.shape
+    if qf.ndim == 3:
+        b, h, k = qf.shape
+        n = 1
+    else:
+        b, h, n, k = qf.shape
     g, m_c, _ = Kcf.shape
     m_d = Kdf.shape[2]
     p = h // g
@@ -39,14 +46,17 @@ def bifurcated_attention(q, Kc, Vc, Kd, Vd, lens, scale=None):
     # they hold (NaN included) cannot reach the sums.
     Kdf = np.where(valid[:, None, :, None], Kdf, 0.0)
     Vdf = np.where(valid[:, None, :, None], Vdf, 0.0)
-    q5 = qf.reshape(b, g, p, 1, k)                                    # bgpnk, n = 1
+    # Token r of n sees decode positions < len_i - n + r + 1.
+    seen = (np.arange(m_d)[None, None, :]
+            < (lens[:, None, None] - n + np.arange(n)[None, :, None] + 1))  # [b, n, m_d]
+    q5 = qf.reshape(b, g, p, n, k)                                    # bgpnk
     logits_c = np.einsum("bgpnk,gmk->bgpnm", q5, Kcf)                 # Eq. 3, context part
     logits_d = np.einsum("bgpnk,bgmk->bgpnm", q5, Kdf)                # Eq. 3, decode part
     logits = np.concatenate([logits_c, logits_d], axis=-1) * scale
-    logits[..., m_c:] = np.where(valid[:, None, None, None, :], logits[..., m_c:], -np.inf)
+    logits[..., m_c:] = np.where(seen[:, None, None, :, :], logits[..., m_c:], -np.inf)
     mu = logits.max(axis=-1, keepdims=True)
     w = np.exp(logits - mu)
     w /= w.sum(axis=-1, keepdims=True)
     o = np.einsum("bgpnm,gmk->bgpnk", w[..., :m_c], Vcf) \
         + np.einsum("bgpnm,bgmk->bgpnk", w[..., m_c:], Vdf)           # Eq. 4
-    return o.reshape(b, h, k)
+    return o.reshape(qf.shape)

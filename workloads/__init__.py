@@ -40,6 +40,7 @@ class Workload:
     m_d_max: int
     ragged: bool
     seed: int
+    n: int = 1  # new tokens per sample (draft tokens verified together when > 1)
 
     @property
     def p(self) -> int:
@@ -49,7 +50,8 @@ class Workload:
 # The five synthetic layers: a tiny MHA layer; 7B-shaped MHA layers (32 heads
 # of 128) at 16 and 32 samples over an 8k context; an MQA layer with 128
 # samples over 16k; and a GQA layer (8 KV groups) with 256 samples over 32k
-# and ragged decode lengths uniform in [1, 1024].
+# and ragged decode lengths uniform in [1, 1024]. Then the 32-sample MHA layer
+# verifying 4 draft tokens per sample in one step (speculative decoding).
 WORKLOADS = {
     w.name: w
     for w in (
@@ -58,6 +60,7 @@ WORKLOADS = {
         Workload("mha7b_b32_mc8k_md512", 32, 32, 32, 128, 8192, 512, False, 1003),
         Workload("mqa_b128_mc16k_md512", 128, 32, 1, 128, 16384, 512, False, 1004),
         Workload("gqa8_b256_mc32k_ragged1024", 256, 32, 8, 128, 32768, 1024, True, 1005),
+        Workload("mha7b_b32_mc8k_md512_draft4", 32, 32, 32, 128, 8192, 512, False, 1006, 4),
     )
 }
 WORKLOAD_ORDER = list(WORKLOADS)
@@ -87,24 +90,26 @@ def _normal_bf16(rng: np.random.Generator, shape) -> np.ndarray:
 
 
 def make_inputs(b, h, g, d, m_c, m_d_max, *, seed, ragged=False, lens=None,
-                poison_tail=False, with_decode_tail=True):
+                poison_tail=False, with_decode_tail=True, n=1):
     """Draw one problem instance.
 
     ``lens`` overrides the drawn lengths (it is applied after all draws, so the
     tensors stay identical). ``poison_tail`` fills decode rows ``t >= len_i``
-    with bf16 NaN, so any read of them shows up in the output.
+    with bf16 NaN, so any read of them shows up in the output. With ``n > 1``
+    new tokens per sample, q is [b, h, n, d] and ragged lengths are drawn in
+    [n, m_d_max] (the n tokens are the last n valid decode rows).
     """
     if h % g:
         raise ValueError("h must be a multiple of g")
     rng = np.random.Generator(np.random.PCG64(seed))
-    q = _normal_bf16(rng, (b, h, d))
+    q = _normal_bf16(rng, (b, h, d) if n == 1 else (b, h, n, d))
     Kc = _normal_bf16(rng, (g, m_c, d))
     Vc = _normal_bf16(rng, (g, m_c, d))
     Kd = _normal_bf16(rng, (b, g, m_d_max, d))
     Vd = _normal_bf16(rng, (b, g, m_d_max, d))
     if ragged:
-        drawn = rng.integers(1, m_d_max + 1, size=b).astype(np.int32) if m_d_max > 0 \
-            else np.zeros(b, np.int32)
+        drawn = rng.integers(min(n, m_d_max) if m_d_max > 0 else 0, m_d_max + 1,
+                             size=b).astype(np.int32) if m_d_max > 0 else np.zeros(b, np.int32)
     else:
         drawn = np.full(b, m_d_max, dtype=np.int32)
     if lens is not None:
@@ -119,7 +124,7 @@ def make_inputs(b, h, g, d, m_c, m_d_max, *, seed, ragged=False, lens=None,
 def make_workload_inputs(w: Workload, *, seed=None, poison_tail=False):
     return make_inputs(w.b, w.h, w.g, w.d, w.m_c, w.m_d_max,
                        seed=w.seed if seed is None else seed, ragged=w.ragged,
-                       poison_tail=poison_tail)
+                       poison_tail=poison_tail, n=w.n)
 
 
 def kv_bytes(g, d, m_c, lens) -> int:
@@ -133,7 +138,10 @@ def replicated_kv_bytes(b, g, d, m_c, lens) -> int:
     return 2 * 2 * g * d * (b * int(m_c) + int(np.sum(lens, dtype=np.int64)))
 
 
-def attention_flops(h, d, b, m_c, lens) -> int:
+def attention_flops(h, d, b, m_c, lens, n=1) -> int:
     """Multiply-adds of QK^T and PV counted as 2 flops each: identical for the
-    bifurcated and the standard formulation (Section 4.2)."""
-    return 4 * h * d * (b * int(m_c) + int(np.sum(lens, dtype=np.int64)))
+    bifurcated and the standard formulation (Section 4.2). With n tokens per
+    sample, token r sees m_c + max(0, len_i - n + r + 1) keys."""
+    lens = np.asarray(lens, dtype=np.int64)
+    seen = sum(int(np.maximum(lens - n + r + 1, 0).sum()) for r in range(n))
+    return 4 * h * d * (n * b * int(m_c) + seen)
