@@ -216,14 +216,14 @@ def main():
     log(f"[bench] generating {w.name}")
     x = workloads.make_workload_inputs(w)
     B_kv = workloads.kv_bytes(w.g, w.d, w.m_c, x["lens"])
-    flops = workloads.attention_flops(w.h, w.d, w.b, w.m_c, x["lens"])
+    flops = workloads.attention_flops(w.h, w.d, w.b, w.m_c, x["lens"], n=w.n)
     torch.cuda.set_device(0)
     dev0 = to_device(x)
     # Rotate over device copies so each step's KV is cold in the Infinity Cache.
     copies = max(3, -(-4 * MALL_BYTES // B_kv))
     devs = [dev0] + [{k: v.clone() for k, v in dev0.items()} for _ in range(copies - 1)]
-    out = torch.empty((w.b, w.h, w.d), dtype=torch.float32, device="cuda")
-    plan = bif.Plan(w.b, w.h, w.g, w.d, w.m_c, w.m_d_max)
+    out = torch.empty(tuple(x["q"].shape), dtype=torch.float32, device="cuda")
+    plan = bif.Plan(w.b, w.h, w.g, w.d, w.m_c, w.m_d_max, n=w.n)
     info = plan.info()
     log(f"[bench] plan {info}, {copies} input copies")
 
@@ -326,7 +326,8 @@ def main():
         "dtype": "bf16",
         "data": "synthetic",
         "config": {"workload": w.name, "b": w.b, "h": w.h, "g": w.g, "d": w.d, "m_c": w.m_c,
-                   "m_d": w.m_d_max, "decode_lens": "ragged" if w.ragged else "uniform",
+                   "m_d": w.m_d_max, "new_tokens": w.n,
+                   "decode_lens": "ragged" if w.ragged else "uniform",
                    "parallelism": "single GPU"},
         "roofline": {"kernel": "partials_kernel (context + decode partials)", "bound": "hbm",
                      "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",

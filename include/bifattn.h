@@ -13,18 +13,24 @@
  * Notation (Section 3.1): b samples, h query heads, g KV groups with
  * p = h/g query heads per group (g = h: multi-head, g = 1: multi-query),
  * d head dimension (the paper's k), m_c context length, m_d_max capacity of
- * each sample's decode cache, len_i <= m_d_max its valid rows. Query length
- * is 1 (one new token per sample).
+ * each sample's decode cache, len_i <= m_d_max its valid rows, n new tokens
+ * per sample: 1 in incremental decoding, n_g > 1 when draft tokens are
+ * verified in one step (the appendix on speculative decoding, where n_g
+ * replaces the query length n of Eq. 3-4).
  *
  * Layouts (all row-major, all device memory, bf16 = 16-bit brain float):
- *   q       bf16 [b][h][d]          head j of sample i at (i*h + j)*d
+ *   q       bf16 [b][h][n][d]       token r of head j of sample i at ((i*h + j)*n + r)*d
+ *                                   ([b][h][d] when n = 1)
  *   Kc, Vc  bf16 [g][m_c][d]        one shared copy of the context cache
  *   Kd, Vd  bf16 [b][g][m_d_max][d] per-sample decode cache
  *   decode_lens int32 [b]           valid decode rows per sample
- *   out     fp32 [b][h][d]
+ *   out     fp32 [b][h][n][d]
  * Head j reads KV group j / p (group-major, the bgpnk order of Eq. 1).
  * Decode rows t >= len_i are never read into arithmetic: they may hold
- * anything, NaN included. Arithmetic: bf16 products, fp32 logits, softmax
+ * anything, NaN included. With n > 1 the n new tokens are the last n of the
+ * len_i valid decode rows, and token r attends to the context and to decode
+ * rows t < len_i - n + r + 1 (the rows up to and including itself); rows it
+ * does not see get weight 0 (they must be finite, like all valid rows). Arithmetic: bf16 products, fp32 logits, softmax
  * statistics and accumulators; softmax weights enter the weighted sum over
  * values rounded to bf16. Softmax scale: dims.scale, or 1/sqrt(d) when 0.
  *
@@ -55,12 +61,12 @@
 extern "C" {
 #endif
 
-#define BIFATTN_VERSION 1
+#define BIFATTN_VERSION 2
 
 typedef enum {
   BIFATTN_OK = 0,
   BIFATTN_EINVAL = -1,       /* null pointer, non-positive size, h % g != 0, ... */
-  BIFATTN_EUNSUPPORTED = -2, /* valid but not built: d not in {64,128}, p > 64,
+  BIFATTN_EUNSUPPORTED = -2, /* valid but not built: d not in {64,128}, p*n > 64,
                                 (m_c + m_d_max) * d * 2 > 2^31 - 1 */
   BIFATTN_EALIGN = -3,       /* a tensor pointer not 16-byte aligned */
   BIFATTN_ENOMEM = -4,       /* workspace or event allocation failed */
@@ -77,6 +83,7 @@ typedef struct {
   int32_t m_c;     /* context length, >= 1 */
   int32_t m_d_max; /* decode cache capacity per sample, >= 0 */
   float scale;     /* softmax scale on q.k; 0 selects 1/sqrt(d) */
+  int32_t n;       /* new tokens per sample, >= 1 (0 is taken as 1) */
 } bifattn_dims_t;
 
 typedef struct bifattn_plan_s *bifattn_plan_t;
@@ -104,10 +111,11 @@ typedef enum {
 /*
  * Validate dims and allocate the plan and its workspace on the current HIP
  * device. On success *plan is set; on failure *plan is left NULL.
- * Errors: EINVAL (null argument, b/h/g/m_c < 1, m_d_max < 0, h % g != 0,
- * sizes whose byte counts overflow), EUNSUPPORTED (d not 64 or 128,
- * h/g > 64, or one sample's cache rows (m_c + m_d_max) * d * 2 bytes beyond
- * 2^31 - 1), ENOMEM (device allocation failed), EHIP (no usable device).
+ * Errors: EINVAL (null argument, b/h/g/m_c < 1, m_d_max < 0, n < 0,
+ * h % g != 0, sizes whose byte counts overflow), EUNSUPPORTED (d not 64 or
+ * 128, (h/g)*n > 64, or one sample's cache rows (m_c + m_d_max) * d * 2
+ * bytes beyond 2^31 - 1), ENOMEM (device allocation failed), EHIP (no
+ * usable device).
  */
 bifattn_status_t bifattn_plan_create(const bifattn_dims_t *dims, bifattn_plan_t *plan);
 
@@ -120,8 +128,8 @@ bifattn_status_t bifattn_plan_get_info(bifattn_plan_t plan, bifattn_plan_info_t 
 
 /*
  * One bifurcated decode-attention step (Section 4.2, Eq. 3-4):
- *   out[i, j, :] = softmax_t( scale * q[i,j,:] . K_i[t,:] ) @ V_i
- * with K_i = Kc[j/p] (+) Kd[i, j/p, 0:len_i] and V_i likewise. Enqueues on
+ *   out[i, j, r, :] = softmax_t( scale * q[i,j,r,:] . K_i[t,:] ) @ V_i
+ * with K_i = Kc[j/p] (+) Kd[i, j/p, 0:len_i - n + r + 1] and V_i likewise. Enqueues on
  * `stream` (a) context partials: each work-group stages a chunk of Kc/Vc of
  * one group once and applies it to all b*p query rows of the group; (b)
  * decode partials: per sample and group over its own Kd/Vd; (c) the combine,

@@ -35,7 +35,7 @@ class BifattnError(RuntimeError):
 class Dims(ctypes.Structure):
     _fields_ = [("b", ctypes.c_int32), ("h", ctypes.c_int32), ("g", ctypes.c_int32),
                 ("d", ctypes.c_int32), ("m_c", ctypes.c_int32), ("m_d_max", ctypes.c_int32),
-                ("scale", ctypes.c_float)]
+                ("scale", ctypes.c_float), ("n", ctypes.c_int32)]
 
 
 class PlanInfo(ctypes.Structure):
@@ -93,10 +93,11 @@ def _check(status: int, what: str):
 
 
 class Plan:
-    """A bifattn_plan_t: problem dimensions plus the workspace it owns."""
+    """A bifattn_plan_t: problem dimensions plus the workspace it owns
+    (n = new tokens per sample)."""
 
-    def __init__(self, b, h, g, d, m_c, m_d_max, scale=0.0):
-        self.dims = Dims(b, h, g, d, m_c, m_d_max, scale)
+    def __init__(self, b, h, g, d, m_c, m_d_max, scale=0.0, n=1):
+        self.dims = Dims(b, h, g, d, m_c, m_d_max, scale, n)
         handle = ctypes.c_void_p()
         _check(lib().bifattn_plan_create(ctypes.byref(self.dims), ctypes.byref(handle)),
                "bifattn_plan_create")
@@ -125,8 +126,8 @@ class Plan:
         return info.as_dict()
 
 
-def bifattn_plan_create(b, h, g, d, m_c, m_d_max, scale=0.0) -> Plan:
-    return Plan(b, h, g, d, m_c, m_d_max, scale)
+def bifattn_plan_create(b, h, g, d, m_c, m_d_max, scale=0.0, n=1) -> Plan:
+    return Plan(b, h, g, d, m_c, m_d_max, scale, n)
 
 
 def bifattn_plan_destroy(plan: Plan):
@@ -145,13 +146,16 @@ def _stream_ptr(stream):
 
 
 def _tensor(t, shape, dtype, device, name):
+    """shape: one shape, or a list of accepted shapes."""
     import torch
     if not isinstance(t, torch.Tensor):
         raise TypeError(f"{name} must be a torch.Tensor")
     if t.dtype != dtype:
         raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
-    if tuple(t.shape) != tuple(shape):
-        raise ValueError(f"{name} must have shape {tuple(shape)}, got {tuple(t.shape)}")
+    shapes = [tuple(x) for x in shape] if isinstance(shape, list) else [tuple(shape)]
+    if tuple(t.shape) not in shapes:
+        raise ValueError(f"{name} must have shape {' or '.join(map(str, shapes))}, "
+                         f"got {tuple(t.shape)}")
     if not t.is_cuda or (device is not None and t.device != device):
         raise ValueError(f"{name} must live on {device or 'the GPU'}")
     if not t.is_contiguous():
@@ -159,23 +163,33 @@ def _tensor(t, shape, dtype, device, name):
     return ctypes.c_void_p(t.data_ptr())
 
 
+def _query_shapes(D):
+    """[b, h, n, d], or [b, h, d] too when n = 1."""
+    n = max(1, D.n)
+    shapes = [(D.b, D.h, n, D.d)]
+    if n == 1:
+        shapes.append((D.b, D.h, D.d))
+    return shapes
+
+
 def bifattn_decode(plan: Plan, q, Kc, Vc, Kd, Vd, decode_lens, out, stream=None):
     """Enqueue one bifurcated decode step (see include/bifattn.h).
 
-    q bf16 [b,h,d]; Kc, Vc bf16 [g,m_c,d]; Kd, Vd bf16 [b,g,m_d_max,d];
-    decode_lens int32 [b]; out fp32 [b,h,d]; all on the same GPU.
+    q bf16 [b,h,n,d] ([b,h,d] when n = 1); Kc, Vc bf16 [g,m_c,d];
+    Kd, Vd bf16 [b,g,m_d_max,d]; decode_lens int32 [b]; out fp32 shaped like
+    q; all on the same GPU.
     """
     import torch
     D = plan.dims
     dev = q.device
     args = [
-        _tensor(q, (D.b, D.h, D.d), torch.bfloat16, dev, "q"),
+        _tensor(q, _query_shapes(D), torch.bfloat16, dev, "q"),
         _tensor(Kc, (D.g, D.m_c, D.d), torch.bfloat16, dev, "Kc"),
         _tensor(Vc, (D.g, D.m_c, D.d), torch.bfloat16, dev, "Vc"),
         _tensor(Kd, (D.b, D.g, D.m_d_max, D.d), torch.bfloat16, dev, "Kd"),
         _tensor(Vd, (D.b, D.g, D.m_d_max, D.d), torch.bfloat16, dev, "Vd"),
         _tensor(decode_lens, (D.b,), torch.int32, dev, "decode_lens"),
-        _tensor(out, (D.b, D.h, D.d), torch.float32, dev, "out"),
+        _tensor(out, [tuple(q.shape)], torch.float32, dev, "out"),
     ]
     _check(lib().bifattn_decode(plan.handle, *args, _stream_ptr(stream)), "bifattn_decode")
 
@@ -188,11 +202,11 @@ def bifattn_decode_replicated(plan: Plan, q, K, V, decode_lens, out, stream=None
     dev = q.device
     rows = D.m_c + D.m_d_max
     args = [
-        _tensor(q, (D.b, D.h, D.d), torch.bfloat16, dev, "q"),
+        _tensor(q, _query_shapes(D), torch.bfloat16, dev, "q"),
         _tensor(K, (D.b, D.g, rows, D.d), torch.bfloat16, dev, "K"),
         _tensor(V, (D.b, D.g, rows, D.d), torch.bfloat16, dev, "V"),
         _tensor(decode_lens, (D.b,), torch.int32, dev, "decode_lens"),
-        _tensor(out, (D.b, D.h, D.d), torch.float32, dev, "out"),
+        _tensor(out, [tuple(q.shape)], torch.float32, dev, "out"),
     ]
     _check(lib().bifattn_decode_replicated(plan.handle, *args, _stream_ptr(stream)),
            "bifattn_decode_replicated")

@@ -18,7 +18,8 @@ using namespace bifattn;
 struct bifattn_plan_s {
   bifattn_dims_t dims{};
   float scale = 0.f;
-  int p = 0, M = 0;
+  int p = 0, M = 0;  // query rows per (sample, group) unit (heads x tokens), rows per group
+  int ntok = 1;
   int ctx_mode = kCtxNone;
   int dec_tiles = 1;
   int ctx_keys = 0, S_c = 0, ctx_row_blocks = 1, n_ctx_blocks = 0, n_ctx_small_blocks = 0;
@@ -80,7 +81,10 @@ int seq_keys(int64_t units, int64_t rows, int start) {
 
 bifattn_status_t plan_splits(bifattn_plan_s* P) {
   const bifattn_dims_t& d = P->dims;
-  P->p = d.h / d.g;
+  P->ntok = d.n > 0 ? d.n : 1;
+  // The n tokens of a head are consecutive rows of q and out, so a unit's
+  // query rows are its p heads times n tokens.
+  P->p = d.h / d.g * P->ntok;
   P->M = d.b * P->p;
   P->dec_tiles = P->p <= 16 ? 1 : (P->p <= 32 ? 2 : 4);
   const int64_t M = P->M;
@@ -137,18 +141,20 @@ bifattn_status_t plan_splits(bifattn_plan_s* P) {
 
 bifattn_status_t check_dims(const bifattn_dims_t* d) {
   if (!d) return BIFATTN_EINVAL;
-  if (d->b < 1 || d->h < 1 || d->g < 1 || d->m_c < 1 || d->m_d_max < 0) return BIFATTN_EINVAL;
+  if (d->b < 1 || d->h < 1 || d->g < 1 || d->m_c < 1 || d->m_d_max < 0 || d->n < 0)
+    return BIFATTN_EINVAL;
   if (d->h % d->g) return BIFATTN_EINVAL;
   if (!(std::isfinite(d->scale))) return BIFATTN_EINVAL;
   if (d->d != 64 && d->d != 128) return BIFATTN_EUNSUPPORTED;
-  if (d->h / d->g > kMaxP) return BIFATTN_EUNSUPPORTED;
+  const double ntok = d->n > 0 ? d->n : 1;
+  if ((double)(d->h / d->g) * ntok > kMaxP) return BIFATTN_EUNSUPPORTED;
   // element counts of the largest tensors must stay far from 2^62
   const double lim = 4.0e18;
   const double dd = d->d;
-  if ((double)d->b * d->h * dd > lim || (double)d->g * d->m_c * dd > lim ||
+  if ((double)d->b * d->h * ntok * dd > lim || (double)d->g * d->m_c * dd > lim ||
       (double)d->b * d->g * ((double)d->m_c + d->m_d_max) * dd > lim)
     return BIFATTN_EINVAL;
-  if ((double)d->b * d->h > INT32_MAX / 2 || (double)d->b * d->g > INT32_MAX / 2)
+  if ((double)d->b * d->h * ntok > INT32_MAX / 2 || (double)d->b * d->g > INT32_MAX / 2)
     return BIFATTN_EINVAL;
   // Kernels address one cache (a group's context, a sample's decode rows, or
   // both in the replicated ablation) with 32-bit byte offsets.
@@ -191,10 +197,11 @@ PartialsParams base_params(const bifattn_plan_s* P, const void* q, const int32_t
   K.dec_ml = P->dec_ml;
   K.status = P->status;
   K.b = P->dims.b;
-  K.h = P->dims.h;
+  K.h = P->dims.h * P->ntok;
   K.g = P->dims.g;
   K.p = P->p;
   K.M = P->M;
+  K.ntok = P->ntok;
   K.m_c = P->dims.m_c;
   K.m_d_max = P->dims.m_d_max;
   // scale * (q . k) = |scale| * ((-q) . k): a negative scale negates q, which
@@ -214,7 +221,7 @@ CombineParams combine_params(const bifattn_plan_s* P, const int32_t* lens, float
   C.out = out;
   C.status = P->status;
   C.b = P->dims.b;
-  C.h = P->dims.h;
+  C.h = P->dims.h * P->ntok;
   C.g = P->dims.g;
   C.p = P->p;
   C.M = P->M;

@@ -45,7 +45,8 @@ struct PartialsParams {
   float* dec_acc;         // [b][g][S_d][4 waves][p][d]
   float2* dec_ml;         // [b][g][S_d][4 waves][p]
   int* status;
-  int b, h, g, p, M;      // M = b*p query rows per group
+  int b, h, g, p, M;      // h, p count query rows (heads x tokens); M = b*p rows per group
+  int ntok;               // new tokens per sample (rows of a unit: head*ntok + token)
   int m_c;
   int m_d_max;            // clamp bound for lens
   int dec_rows;           // row capacity of one (sample, group) decode cache
@@ -70,7 +71,7 @@ struct CombineParams {
   const int32_t* lens;
   float* out;
   int* status;
-  int b, h, g, p, M;
+  int b, h, g, p, M;      // h, p count query rows (heads x tokens)
   int m_d_max;
   int S_c;
   int S_d;

@@ -173,10 +173,15 @@ template <int D, int NT> struct RowState {
 // with lazy rescaling, O^T += V^T P^T on MFMA. k_at(a, s) yields this lane's
 // K operand of sub-tile a and k-step s, vop_at(t) its V^T operand of
 // dimension block t (built on demand, so only one is live at a time),
-// q_at(nt, s) its Q^T operands. Keys >= nvalid are masked.
+// q_at(nt, s) its Q^T operands. `rem` counts the keys from the tile's first
+// to the end of the range. With ntok tokens per (sample, group) unit (rows
+// r = head*ntok + token), row r sees keys < rem - (ntok - 1) + r % ntok:
+// the range ends at the last token's limit and earlier tokens stop earlier
+// (ntok = 1 masks keys >= rem).
 template <int D, int NT, typename KOp, typename VOp, typename QOp>
 __device__ __forceinline__ void tile_update(RowState<D, NT>& st, KOp&& k_at, VOp&& vop_at,
-                                            QOp&& q_at, int nvalid, float scale_log2, int lane) {
+                                            QOp&& q_at, int rem, int ntok, float scale_log2,
+                                            int lane) {
   constexpr int KS = D / 32;
   constexpr int DV = D / 16;
   const int G = lane >> 4;
@@ -209,13 +214,14 @@ __device__ __forceinline__ void tile_update(RowState<D, NT>& st, KOp&& k_at, VOp
       x[nt][j] = sacc[nt][0][j];
       x[nt][4 + j] = sacc[nt][1][j];
     }
-    if (nvalid < kTileKeys) {
+    if (rem < kTileKeys + ntok - 1) {
       // The bound passes through readfirstlane (convergent), so the compiler
       // cannot hoist these compares out of the branch into every full tile.
-      const int nv = __builtin_amdgcn_readfirstlane(nvalid);
+      const int nv = __builtin_amdgcn_readfirstlane(rem) - (ntok - 1);
+      const int lim = ntok == 1 ? nv : nv + (nt * kRowsPerTile + (lane & 15)) % ntok;
 #pragma unroll
       for (int e = 0; e < 8; ++e)
-        if (4 * e + G >= nv) x[nt][e] = kNegInf;
+        if (4 * e + G >= lim) x[nt][e] = kNegInf;
     }
     float m = x[nt][0];
 #pragma unroll
@@ -427,12 +433,14 @@ __device__ __forceinline__ void store_partials(RowState<D, NT>& st, int nrows, f
 // into A (before anything else, so that they overlap the set-up). The waves
 // that share a segment start at neighbouring tiles, so together they sweep
 // one window of it. qw: this wave's Q^T operands in LDS, [NT][d/32][64
-// lanes]; kl: this wave's LDS K tile (32*d*2 bytes).
+// lanes]; kl: this wave's LDS K tile (32*d*2 bytes). kend: the end of the
+// sequence the tokens' causal limits count from (ntok tokens per unit; k1
+// when ntok = 1).
 template <int D, int NT>
 __device__ __forceinline__ void stream_keys(RowState<D, NT>& st, const u32x4* qw, u32x4* kl,
                                             __amdgpu_buffer_rsrc_t rk, __amdgpu_buffer_rsrc_t rv,
-                                            TileRegs<D>& A, int k0, int k1, int stride,
-                                            float scale_log2, int lane) {
+                                            TileRegs<D>& A, int k0, int k1, int kend, int stride,
+                                            int ntok, float scale_log2, int lane) {
   constexpr int KS = D / 32;
   if (k0 >= k1) return;
   // Volatile: a real LDS read at each use, not a register copy kept alive
@@ -451,14 +459,16 @@ __device__ __forceinline__ void stream_keys(RowState<D, NT>& st, const u32x4* qw
     const int nv0 = min(kTileKeys, k1 - key);
     if (nv0 < kTileKeys) A.mask_v(nv0, lane);
     A.stage_k(kl, lane);
-    tile_update<D, NT>(st, k_at, [&](int t) { return A.vop(t); }, q_at, nv0, scale_log2, lane);
+    tile_update<D, NT>(st, k_at, [&](int t) { return A.vop(t); }, q_at, kend - key, ntok,
+                       scale_log2, lane);
     if (key1 >= k1) break;
     const int key2 = key1 + stride;
     A.load(rk, rv, key2, lane);
     const int nv1 = min(kTileKeys, k1 - key1);
     if (nv1 < kTileKeys) B.mask_v(nv1, lane);
     B.stage_k(kl, lane);
-    tile_update<D, NT>(st, k_at, [&](int t) { return B.vop(t); }, q_at, nv1, scale_log2, lane);
+    tile_update<D, NT>(st, k_at, [&](int t) { return B.vop(t); }, q_at, kend - key1, ntok,
+                       scale_log2, lane);
     if (key2 >= k1) break;
   }
 }
@@ -512,7 +522,10 @@ __device__ void decode_block(const PartialsParams& P, int blk, int wave, int lan
                  P.q_sign, lane);
   RowState<D, NT> st;
   st.init();
-  stream_keys<D, NT>(st, qw, kl, rk, rv, A, k0, k1, kWaves * kTileKeys, P.scale_log2, lane);
+  // Keys [k0, k1) of this chunk; the causal limits of the tokens count from
+  // the end of the sequence (total), which may lie in a later chunk.
+  stream_keys<D, NT>(st, qw, kl, rk, rv, A, k0, k1, total, kWaves * kTileKeys, P.ntok,
+                     P.scale_log2, lane);
   const size_t prow = ((size_t)blk * kWaves + wave) * P.p;
   store_partials<D, NT>(st, p, P.dec_acc + prow * D, P.dec_ml + prow, lane);
 }
@@ -599,8 +612,8 @@ __device__ void ctx_small_block(const PartialsParams& P, int blk, int wave, int 
   }, P.q_sign, lane);
   RowState<D, NT> st;
   st.init();
-  stream_keys<D, NT>(st, qw, kl, rk, rv, A, k0, P.m_c, P.S_c * kWaves * kTileKeys, P.scale_log2,
-                     lane);
+  stream_keys<D, NT>(st, qw, kl, rk, rv, A, k0, P.m_c, P.m_c, P.S_c * kWaves * kTileKeys, 1,
+                     P.scale_log2, lane);
   const size_t prow = (size_t)blk * P.M;
   __syncthreads();  // the merge buffer overlays the waves' K tiles
   merge_waves_and_store<D, NT>(st, merge_lds, M, P.ctx_acc + prow * D, P.ctx_ml + prow, wave, lane);
@@ -725,8 +738,8 @@ __device__ __forceinline__ void ctx_large_body(const PartialsParams& P) {
     if (rows)
       tile_update<D, 1>(st, [&](int a, int ss) { return slot(buf, a * KS + ss)[lane]; },
                         [&](int t) { return slot(buf, KOPS + t)[lane]; },
-                        [&](int, int ss) { return qop[0][ss]; }, min(kTileKeys, nkeys - key),
-                        P.scale_log2, lane);
+                        [&](int, int ss) { return qop[0][ss]; }, nkeys - key, 1, P.scale_log2,
+                        lane);
     if (stage_next) {
       // The other buffer was last read in the previous step, before the
       // barrier that ended it.

@@ -15,10 +15,16 @@ def to_device(x):
 
 
 def dims_of(x):
-    b, h, d = x["q"].shape
+    """(b, h, g, d, m_c, m_d_max); q is [b, h, d] or [b, h, n, d]."""
+    q = x["q"]
+    b, h, d = q.shape[0], q.shape[1], q.shape[-1]
     g, m_c, _ = x["Kc"].shape
     m_d_max = x["Kd"].shape[2]
     return b, h, g, d, m_c, m_d_max
+
+
+def tokens_of(x):
+    return 1 if x["q"].ndim == 3 else x["q"].shape[2]
 
 
 def run_decode(x, scale=0.0, plan=None, dev=None, check_status=True):
@@ -27,10 +33,10 @@ def run_decode(x, scale=0.0, plan=None, dev=None, check_status=True):
     b, h, g, d, m_c, m_d_max = dims_of(x)
     own = plan is None
     if own:
-        plan = bif.Plan(b, h, g, d, m_c, m_d_max, scale)
+        plan = bif.Plan(b, h, g, d, m_c, m_d_max, scale, n=tokens_of(x))
     try:
         dev = dev or to_device(x)
-        out = torch.full((b, h, d), float("nan"), dtype=torch.float32, device="cuda")
+        out = torch.full(tuple(x["q"].shape), float("nan"), dtype=torch.float32, device="cuda")
         bif.bifattn_decode(plan, dev["q"], dev["Kc"], dev["Vc"], dev["Kd"], dev["Vd"],
                            dev["lens"], out)
         st = bif.bifattn_plan_status(plan)
@@ -54,11 +60,11 @@ def run_replicated(x, scale=0.0):
     import torch
     b, h, g, d, m_c, m_d_max = dims_of(x)
     K, V = replicate(x)
-    with bif.Plan(b, h, g, d, m_c, m_d_max, scale) as plan:
+    with bif.Plan(b, h, g, d, m_c, m_d_max, scale, n=tokens_of(x)) as plan:
         dev = to_device(x)
         Kt = torch.from_numpy(K.view(np.int16)).view(torch.bfloat16).cuda()
         Vt = torch.from_numpy(V.view(np.int16)).view(torch.bfloat16).cuda()
-        out = torch.full((b, h, d), float("nan"), dtype=torch.float32, device="cuda")
+        out = torch.full(tuple(x["q"].shape), float("nan"), dtype=torch.float32, device="cuda")
         bif.bifattn_decode_replicated(plan, dev["q"], Kt, Vt, dev["lens"], out)
         assert bif.bifattn_plan_status(plan) == bif.OK
         return out.cpu().double().numpy()

@@ -35,7 +35,7 @@ def test_every_declared_symbol_is_exported(L):
 
 
 def test_version_and_status_strings(L):
-    assert bif.bifattn_version() == 1
+    assert bif.bifattn_version() == 2
     for code in (bif.OK, bif.EINVAL, bif.EUNSUPPORTED, bif.EALIGN, bif.ENOMEM, bif.EHIP, bif.ELENS):
         assert bif.status_string(code)
     assert bif.status_string(12345) == "unknown status"
@@ -59,6 +59,8 @@ def _create(L, *dims):
     ((2**30, 2**30, 2**30, 128, 128, 16, 0.0), bif.EINVAL),  # overflowing sizes
     ((1, 32, 32, 128, 2**23, 0, 0.0), bif.EUNSUPPORTED),    # one cache past 2^31 bytes
     ((1, 32, 32, 128, 2**23 - 64, 64, 0.0), bif.EUNSUPPORTED),  # context + decode rows
+    ((2, 4, 2, 64, 128, 16, 0.0, -1), bif.EINVAL),          # negative token count
+    ((2, 32, 1, 64, 128, 16, 0.0, 3), bif.EUNSUPPORTED),    # p * n = 96 query rows per unit
 ])
 def test_plan_create_rejects_bad_dims_without_a_device(L, dims, expect):
     st, handle = _create(L, *dims)

@@ -7,7 +7,7 @@ import oracle
 import paper_2403_08845_amd as bif
 import workloads
 
-from .gpu_util import dims_of, run_decode, run_replicated, sample_rows, to_device
+from .gpu_util import dims_of, run_decode, run_replicated, sample_rows, to_device, tokens_of
 from .parity import assert_parity
 
 pytestmark = pytest.mark.gpu
@@ -70,8 +70,15 @@ def test_workload_sampled_rows(name):
     out = run_decode(x)
     assert np.all(np.isfinite(out))
     ri, rj = sample_rows(w.b, w.h, x["lens"], 48, seed=w.seed)
-    ref = oracle.attention_rows(**x, rows_i=ri, rows_j=rj)
-    _report(name, *assert_parity(out[ri, rj], ref, name))
+    if w.n == 1:
+        ref = oracle.attention_rows(**x, rows_i=ri, rows_j=rj)
+        got = out[ri, rj]
+    else:  # every token of the sampled rows
+        rt = np.tile(np.arange(w.n, dtype=np.int32), ri.size)
+        ri, rj = np.repeat(ri, w.n), np.repeat(rj, w.n)
+        ref = oracle.attention_rows(**x, rows_i=ri, rows_j=rj, rows_t=rt)
+        got = out[ri, rj, rt]
+    _report(name, *assert_parity(got, ref, name))
 
 
 def test_masked_tail_is_never_read():
@@ -195,3 +202,38 @@ def test_workspace_reuse_over_many_calls(case):
                 for kk in range(2):
                     assert torch.equal(outs[kk], refs[kk]), f"call {it}: input {kk} differs"
         assert bif.bifattn_plan_status(plan) == bif.OK
+
+
+# n new tokens per sample (draft tokens verified in one step): MHA / GQA / MQA,
+# both head dims, the few-row and the many-row context paths, ragged lengths
+# including lengths below n and zero.
+DRAFT_CASES = [
+    # b, h, g, d, m_c, m_d_max, n, lens (None: drawn in [n, m_d_max])
+    (4, 8, 8, 128, 700, 90, 4, None),
+    (3, 8, 2, 64, 333, 70, 3, [70, 2, 0]),
+    (5, 16, 1, 128, 517, 45, 2, None),       # MQA, p*n = 32
+    (2, 4, 4, 128, 1000, 300, 8, [300, 5]),  # n = 8 across two 32-key tiles
+    (40, 32, 32, 128, 600, 64, 4, None),     # M = 160 rows per group: many-row context path
+    (6, 8, 1, 64, 200, 33, 8, None),         # MQA, p*n = 64
+]
+
+
+@pytest.mark.parametrize("case", DRAFT_CASES, ids=lambda c: "b%d_h%d_g%d_d%d_mc%d_md%d_n%d" % c[:7])
+def test_draft_tokens_full_output(case):
+    b, h, g, d, m_c, m_d, n, lens = case
+    x = workloads.make_inputs(b, h, g, d, m_c, m_d, seed=600 + n, ragged=lens is None, lens=lens, n=n)
+    print(f"[case] {case} lens={x['lens'].tolist()[:8]}", flush=True)
+    out = run_decode(x)
+    assert out.shape == (b, h, n, d)
+    _report(str(case), *assert_parity(out, oracle.attention(**x), str(case)))
+
+
+def test_draft_tokens_masked_tail_and_replicated():
+    """Rows past each sample's length stay unread with n tokens, and the
+    replicated ablation applies the same causal rule."""
+    b, h, g, d, m_c, m_d, n = 4, 8, 2, 128, 300, 80, 4
+    x = workloads.make_inputs(b, h, g, d, m_c, m_d, seed=650, ragged=True, n=n)
+    y = workloads.make_inputs(b, h, g, d, m_c, m_d, seed=650, ragged=True, n=n, poison_tail=True)
+    a = run_decode(x)
+    assert np.array_equal(a, run_decode(y))
+    assert_parity(run_replicated(x), oracle.attention(**x), "replicated, n = 4")
