@@ -156,9 +156,27 @@ bifattn_status_t bifattn_decode_replicated(bifattn_plan_t plan, const void *q, c
                                            float *out, hipStream_t stream);
 
 /*
+ * Append one decoding step's keys and values to the decode cache (the decode
+ * cache holds the keys and values of the previous decoding steps, Section
+ * 3.1), so that a generation loop runs append then decode each step:
+ *   Kd[i, gam, len_i + r, :] = k_new[i, gam, r, :]   (r < n; Vd likewise)
+ *   decode_lens[i] += n
+ * k_new, v_new bf16 [b][g][n][d] (the step's n new tokens per sample, n from
+ * the plan); Kd, Vd, decode_lens as in bifattn_decode, updated in place on
+ * `stream`. Rows that would pass m_d_max are dropped (the length stops at
+ * m_d_max), a length outside [0, m_d_max] is clamped first; both raise the
+ * device-side flag that bifattn_plan_status reports as BIFATTN_ELENS.
+ * Errors: EINVAL (null argument, m_d_max = 0), EALIGN (a tensor not 16-byte
+ * aligned, decode_lens not 4-byte aligned), EHIP (launch failure).
+ */
+bifattn_status_t bifattn_append_kv(bifattn_plan_t plan, const void *k_new, const void *v_new,
+                                   void *Kd, void *Vd, int32_t *decode_lens, hipStream_t stream);
+
+/*
  * Synchronise `stream`, then report and clear the plan's device-side flag:
  * BIFATTN_ELENS if any call since the last check saw a decode length outside
- * [0, m_d_max] (the call used the clamped length), else BIFATTN_OK.
+ * [0, m_d_max] (the call used the clamped length) or an append ran out of
+ * capacity, else BIFATTN_OK.
  * EHIP if the stream reports an error.
  */
 bifattn_status_t bifattn_plan_status(bifattn_plan_t plan, hipStream_t stream);

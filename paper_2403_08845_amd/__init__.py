@@ -21,7 +21,7 @@ KERNEL_PARTIALS, KERNEL_COMBINE, KERNEL_CALL = 0, 1, 2
 
 EXPORTED = (
     "bifattn_plan_create", "bifattn_plan_destroy", "bifattn_plan_get_info", "bifattn_decode",
-    "bifattn_decode_replicated", "bifattn_plan_status", "bifattn_plan_set_timing",
+    "bifattn_decode_replicated", "bifattn_append_kv", "bifattn_plan_status", "bifattn_plan_set_timing",
     "bifattn_plan_read_timing", "bifattn_status_string", "bifattn_version",
 )
 
@@ -66,6 +66,7 @@ def lib() -> ctypes.CDLL:
         L.bifattn_plan_get_info.argtypes = [vp, ctypes.POINTER(PlanInfo)]
         L.bifattn_decode.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp]
         L.bifattn_decode_replicated.argtypes = [vp, vp, vp, vp, vp, vp, vp]
+        L.bifattn_append_kv.argtypes = [vp, vp, vp, vp, vp, vp, vp]
         L.bifattn_plan_status.argtypes = [vp, vp]
         L.bifattn_plan_set_timing.argtypes = [vp, st, i32]
         L.bifattn_plan_read_timing.argtypes = [vp, ctypes.POINTER(i32), ctypes.POINTER(ctypes.c_double)]
@@ -210,6 +211,24 @@ def bifattn_decode_replicated(plan: Plan, q, K, V, decode_lens, out, stream=None
     ]
     _check(lib().bifattn_decode_replicated(plan.handle, *args, _stream_ptr(stream)),
            "bifattn_decode_replicated")
+
+
+def bifattn_append_kv(plan: Plan, k_new, v_new, Kd, Vd, decode_lens, stream=None):
+    """Enqueue the decode-cache append of one step (see include/bifattn.h):
+    k_new, v_new bf16 [b,g,n,d] go to rows decode_lens[i] .. + n - 1 of
+    Kd, Vd bf16 [b,g,m_d_max,d]; decode_lens int32 [b] advances by n."""
+    import torch
+    D = plan.dims
+    dev = Kd.device
+    n = max(1, D.n)
+    args = [
+        _tensor(k_new, (D.b, D.g, n, D.d), torch.bfloat16, dev, "k_new"),
+        _tensor(v_new, (D.b, D.g, n, D.d), torch.bfloat16, dev, "v_new"),
+        _tensor(Kd, (D.b, D.g, D.m_d_max, D.d), torch.bfloat16, dev, "Kd"),
+        _tensor(Vd, (D.b, D.g, D.m_d_max, D.d), torch.bfloat16, dev, "Vd"),
+        _tensor(decode_lens, (D.b,), torch.int32, dev, "decode_lens"),
+    ]
+    _check(lib().bifattn_append_kv(plan.handle, *args, _stream_ptr(stream)), "bifattn_append_kv")
 
 
 def bifattn_plan_status(plan: Plan, stream=None) -> int:

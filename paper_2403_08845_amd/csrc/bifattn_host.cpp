@@ -421,6 +421,27 @@ bifattn_status_t bifattn_decode_replicated(bifattn_plan_t P, const void* q, cons
   return e == hipSuccess ? BIFATTN_OK : BIFATTN_EHIP;
 }
 
+bifattn_status_t bifattn_append_kv(bifattn_plan_t P, const void* k_new, const void* v_new,
+                                   void* Kd, void* Vd, int32_t* decode_lens, hipStream_t stream) {
+  if (!P || !k_new || !v_new || !Kd || !Vd || !decode_lens || P->dims.m_d_max < 1)
+    return BIFATTN_EINVAL;
+  if (!aligned(k_new, 16) || !aligned(v_new, 16) || !aligned(Kd, 16) || !aligned(Vd, 16) ||
+      !aligned(decode_lens, 4))
+    return BIFATTN_EALIGN;
+  AppendParams A{};
+  A.k_new = static_cast<const uint16_t*>(k_new);
+  A.v_new = static_cast<const uint16_t*>(v_new);
+  A.Kd = static_cast<uint16_t*>(Kd);
+  A.Vd = static_cast<uint16_t*>(Vd);
+  A.lens = decode_lens;
+  A.status = P->status;
+  A.b = P->dims.b;
+  A.g = P->dims.g;
+  A.n = P->ntok;
+  A.m_d_max = P->dims.m_d_max;
+  return launch_append(A, P->dims.d, stream) == hipSuccess ? BIFATTN_OK : BIFATTN_EHIP;
+}
+
 bifattn_status_t bifattn_plan_status(bifattn_plan_t P, hipStream_t stream) {
   if (!P) return BIFATTN_EINVAL;
   if (hipStreamSynchronize(stream) != hipSuccess) return BIFATTN_EHIP;

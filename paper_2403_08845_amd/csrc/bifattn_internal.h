@@ -77,6 +77,17 @@ struct CombineParams {
   int S_d;
 };
 
+// Decode-cache append: the n new rows of every (sample, group).
+struct AppendParams {
+  const uint16_t* k_new;  // [b][g][n][d]
+  const uint16_t* v_new;
+  uint16_t* Kd;           // [b][g][m_d_max][d]
+  uint16_t* Vd;
+  int32_t* lens;          // [b], advanced by n (capped at m_d_max)
+  int* status;
+  int b, g, n, m_d_max;
+};
+
 enum CtxMode { kCtxNone = 0, kCtxSmall1 = 1, kCtxSmall2 = 2, kCtxSmall4 = 4, kCtxLarge = 8 };
 
 // Launch the partial kernel over n_ctx_blocks + n_ctx_small_blocks +
@@ -84,6 +95,8 @@ enum CtxMode { kCtxNone = 0, kCtxSmall1 = 1, kCtxSmall2 = 2, kCtxSmall4 = 4, kCt
 hipError_t launch_partials(const PartialsParams& P, int d, int ctx_mode, int dec_tiles,
                            hipStream_t stream);
 hipError_t launch_combine(const CombineParams& C, int d, hipStream_t stream);
+// Launch the decode-cache append (one work-group per sample).
+hipError_t launch_append(const AppendParams& A, int d, hipStream_t stream);
 // Launch the many-row context kernel over n_ctx_blocks work-groups.
 hipError_t launch_ctx_large(const PartialsParams& P, int d, hipStream_t stream);
 

@@ -945,8 +945,48 @@ hipError_t launch_partials_d(const PartialsParams& P, int ctx_mode, int dec_tile
   }
 }
 
+// Decode-cache append (the decode cache holds the keys and values of the
+// previous decoding steps, Section 3.1): work-group i copies sample i's n new
+// rows of every group to rows len_i .. len_i + n - 1 of its decode cache and
+// then advances len_i by n. One work-group per sample, so every thread reads
+// len_i before thread 0 rewrites it. Rows past the capacity are dropped; a
+// length outside [0, m_d_max] is clamped; both raise the status flag.
+template <int D>
+__global__ __launch_bounds__(256) void append_kernel(AppendParams A) {
+  constexpr int CH = D / 8;  // 16-byte chunks per row
+  const int i = blockIdx.x;
+  const int raw = A.lens[i];
+  const int len = raw < 0 ? 0 : (raw > A.m_d_max ? A.m_d_max : raw);
+  const int room = min(A.n, A.m_d_max - len);  // new rows that fit
+  const int total = A.g * room * CH;
+  for (int idx = threadIdx.x; idx < total; idx += blockDim.x) {
+    const int c = idx % CH;
+    const int r = (idx / CH) % room;
+    const int gam = idx / CH / room;
+    const size_t unit = (size_t)i * A.g + gam;
+    const size_t src = (unit * A.n + r) * D + c * 8;
+    const size_t dst = (unit * A.m_d_max + len + r) * D + c * 8;
+    *reinterpret_cast<u32x4*>(A.Kd + dst) = *reinterpret_cast<const u32x4*>(A.k_new + src);
+    *reinterpret_cast<u32x4*>(A.Vd + dst) = *reinterpret_cast<const u32x4*>(A.v_new + src);
+  }
+  __syncthreads();  // every thread has read len_i
+  if (threadIdx.x == 0) {
+    if (raw != len || room < A.n) atomicOr(A.status, kStatusLens);
+    A.lens[i] = len + room;
+  }
+}
+
 }  // namespace
 
+hipError_t launch_append(const AppendParams& A, int d, hipStream_t stream) {
+  if (d == 128)
+    append_kernel<128><<<A.b, 256, 0, stream>>>(A);
+  else if (d == 64)
+    append_kernel<64><<<A.b, 256, 0, stream>>>(A);
+  else
+    return hipErrorInvalidValue;
+  return hipGetLastError();
+}
 hipError_t launch_ctx_large(const PartialsParams& P, int d, hipStream_t stream) {
   if (P.n_ctx_blocks == 0) return hipSuccess;
   if (d == 128)
