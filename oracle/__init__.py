@@ -15,6 +15,11 @@ Two independent evaluations of the same quantity:
 
 Their agreement to ~1e-12 is the paper's exactness claim (Section 4.2,
 Appendix E.1), checked in ``tests/test_oracle_pins.py``.
+
+Caches may hold 8-bit codes (``kv="fp8_e4m3"`` or ``kv="int8"``, arrays of
+uint8 bit patterns) with per-group fp32 ``k_scale`` / ``v_scale`` [g]: the
+key of a row is ``k_scale[gam]`` times the code's value (the FAQ on
+attention quantization; the reading is spelled out in ``oracle.c``).
 """
 from __future__ import annotations
 
@@ -31,6 +36,9 @@ _lib = None
 
 _ERRORS = {-1: "invalid dimensions or row index", -4: "out of memory",
            -6: "decode length outside [0, m_d_max]"}
+
+#: Cache element types: name -> (code of oracle.c, numpy dtype of the stored bits).
+KV_TYPES = {"bf16": (0, np.uint16), "fp8_e4m3": (1, np.uint8), "int8": (2, np.uint8)}
 
 
 def build(force: bool = False) -> str:
@@ -50,14 +58,18 @@ def _load():
         u16 = ctypes.POINTER(ctypes.c_uint16)
         i32 = ctypes.POINTER(ctypes.c_int32)
         f64 = ctypes.POINTER(ctypes.c_double)
+        f32 = ctypes.POINTER(ctypes.c_float)
+        vp = ctypes.c_void_p
         ci = ctypes.c_int
-        lib.oracle_attention_fp64.argtypes = [ci, ci, ci, ci, ci, ci, ci, ctypes.c_double,
-                                              u16, u16, u16, u16, u16, i32, f64, ci]
-        lib.oracle_attention_fp64.restype = ci
-        lib.oracle_attention_rows_fp64.argtypes = [ci, ci, ci, ci, ci, ci, ci, ctypes.c_double,
-                                                   u16, u16, u16, u16, u16, i32, ci, i32, i32,
-                                                   i32, f64, ci]
-        lib.oracle_attention_rows_fp64.restype = ci
+        lib.oracle_attention_kv_fp64.argtypes = [ci, ci, ci, ci, ci, ci, ci, ctypes.c_double, ci,
+                                                 u16, vp, vp, vp, vp, i32, f32, f32, f64, ci]
+        lib.oracle_attention_kv_fp64.restype = ci
+        lib.oracle_attention_kv_rows_fp64.argtypes = [ci, ci, ci, ci, ci, ci, ci, ctypes.c_double,
+                                                      ci, u16, vp, vp, vp, vp, i32, f32, f32, ci,
+                                                      i32, i32, i32, f64, ci]
+        lib.oracle_attention_kv_rows_fp64.restype = ci
+        lib.oracle_code_value.argtypes = [ci, ci]
+        lib.oracle_code_value.restype = ctypes.c_double
         lib.oracle_max_threads.restype = ci
         _lib = lib
     return _lib
@@ -67,9 +79,19 @@ def _ptr(a, ctype):
     return a.ctypes.data_as(ctypes.POINTER(ctype))
 
 
-def _prep(q, Kc, Vc, Kd, Vd, lens):
+def _prep(q, Kc, Vc, Kd, Vd, lens, kv="bf16", k_scale=None, v_scale=None):
     """q is [b, h, d] (one new token per sample) or [b, h, n, d] (n new tokens)."""
-    q, Kc, Vc, Kd, Vd = (np.ascontiguousarray(x, dtype=np.uint16) for x in (q, Kc, Vc, Kd, Vd))
+    if kv not in KV_TYPES:
+        raise ValueError(f"unknown cache type {kv!r}")
+    code, dt = KV_TYPES[kv]
+    q = np.ascontiguousarray(q, dtype=np.uint16)
+    caches = []
+    for x in (Kc, Vc, Kd, Vd):
+        x = np.ascontiguousarray(x)
+        if x.dtype.itemsize != np.dtype(dt).itemsize or x.dtype.kind not in "ui":
+            raise ValueError(f"{kv} caches are {np.dtype(dt).itemsize}-byte bit patterns")
+        caches.append(x.view(dt))
+    Kc, Vc, Kd, Vd = caches
     lens = np.ascontiguousarray(lens, dtype=np.int32)
     if q.ndim == 3:
         b, h, d = q.shape
@@ -81,7 +103,22 @@ def _prep(q, Kc, Vc, Kd, Vd, lens):
     if not (d == d2 == d3 and b == b2 and g == g2 and Vc.shape == Kc.shape
             and Vd.shape == Kd.shape and lens.shape == (b,)):
         raise ValueError("inconsistent shapes")
-    return (q, Kc, Vc, Kd, Vd, lens), (b, h, g, d, m_c, m_d_max, n)
+    scales = []
+    for sc in (k_scale, v_scale):
+        if sc is not None:
+            sc = np.ascontiguousarray(sc, dtype=np.float32)
+            if sc.shape != (g,):
+                raise ValueError("scales must be [g]")
+        scales.append(sc)
+    return (q, Kc, Vc, Kd, Vd, lens), (b, h, g, d, m_c, m_d_max, n), code, scales
+
+
+def _vp(a):
+    return ctypes.c_void_p(a.ctypes.data)
+
+
+def _fp(a):
+    return None if a is None else _ptr(a, ctypes.c_float)
 
 
 def default_scale(d: int) -> float:
@@ -90,28 +127,32 @@ def default_scale(d: int) -> float:
     return 1.0 / np.sqrt(float(d))
 
 
-def attention(q, Kc, Vc, Kd, Vd, lens, scale=None, nthreads=0):
-    """Full fp64 output, shaped like q: [b, h, d] or [b, h, n, d] (inputs are
-    bf16 bit patterns, uint16). With n tokens per sample, token r sees the
-    first max(0, len_i - n + r + 1) decode rows."""
-    arrs, (b, h, g, d, m_c, m_d_max, n) = _prep(q, Kc, Vc, Kd, Vd, lens)
+def attention(q, Kc, Vc, Kd, Vd, lens, scale=None, nthreads=0, kv="bf16", k_scale=None,
+              v_scale=None):
+    """Full fp64 output, shaped like q: [b, h, d] or [b, h, n, d] (q is bf16
+    bit patterns, uint16; caches bf16 bits or 8-bit codes as ``kv`` says).
+    With n tokens per sample, token r sees the first max(0, len_i - n + r + 1)
+    decode rows."""
+    arrs, (b, h, g, d, m_c, m_d_max, n), code, (ks, vs) = _prep(q, Kc, Vc, Kd, Vd, lens, kv,
+                                                               k_scale, v_scale)
     scale = default_scale(d) if scale is None else float(scale)
     out = np.empty(arrs[0].shape, dtype=np.float64)
     q, Kc, Vc, Kd, Vd, lens = arrs
-    rc = _load().oracle_attention_fp64(b, h, g, d, m_c, m_d_max, n, scale,
-                                       _ptr(q, ctypes.c_uint16), _ptr(Kc, ctypes.c_uint16),
-                                       _ptr(Vc, ctypes.c_uint16), _ptr(Kd, ctypes.c_uint16),
-                                       _ptr(Vd, ctypes.c_uint16), _ptr(lens, ctypes.c_int32),
-                                       _ptr(out, ctypes.c_double), int(nthreads))
+    rc = _load().oracle_attention_kv_fp64(b, h, g, d, m_c, m_d_max, n, scale, code,
+                                          _ptr(q, ctypes.c_uint16), _vp(Kc), _vp(Vc), _vp(Kd),
+                                          _vp(Vd), _ptr(lens, ctypes.c_int32), _fp(ks), _fp(vs),
+                                          _ptr(out, ctypes.c_double), int(nthreads))
     if rc:
         raise ValueError(f"oracle: {_ERRORS.get(rc, rc)}")
     return out
 
 
-def attention_rows(q, Kc, Vc, Kd, Vd, lens, rows_i, rows_j, scale=None, nthreads=0, rows_t=None):
+def attention_rows(q, Kc, Vc, Kd, Vd, lens, rows_i, rows_j, scale=None, nthreads=0, rows_t=None,
+                   kv="bf16", k_scale=None, v_scale=None):
     """fp64 output rows (sample rows_i[r], head rows_j[r], token rows_t[r]
     (default 0)) -> [nrows, d]."""
-    arrs, (b, h, g, d, m_c, m_d_max, n) = _prep(q, Kc, Vc, Kd, Vd, lens)
+    arrs, (b, h, g, d, m_c, m_d_max, n), code, (ks, vs) = _prep(q, Kc, Vc, Kd, Vd, lens, kv,
+                                                               k_scale, v_scale)
     scale = default_scale(d) if scale is None else float(scale)
     ri = np.ascontiguousarray(rows_i, dtype=np.int32)
     rj = np.ascontiguousarray(rows_j, dtype=np.int32)
@@ -120,16 +161,21 @@ def attention_rows(q, Kc, Vc, Kd, Vd, lens, rows_i, rows_j, scale=None, nthreads
         raise ValueError("rows_i, rows_j and rows_t must be 1-D and equally long")
     out = np.empty((ri.size, d), dtype=np.float64)
     q, Kc, Vc, Kd, Vd, lens = arrs
-    rc = _load().oracle_attention_rows_fp64(b, h, g, d, m_c, m_d_max, n, scale,
-                                            _ptr(q, ctypes.c_uint16), _ptr(Kc, ctypes.c_uint16),
-                                            _ptr(Vc, ctypes.c_uint16), _ptr(Kd, ctypes.c_uint16),
-                                            _ptr(Vd, ctypes.c_uint16), _ptr(lens, ctypes.c_int32),
-                                            int(ri.size), _ptr(ri, ctypes.c_int32),
-                                            _ptr(rj, ctypes.c_int32), _ptr(rt, ctypes.c_int32),
-                                            _ptr(out, ctypes.c_double), int(nthreads))
+    rc = _load().oracle_attention_kv_rows_fp64(b, h, g, d, m_c, m_d_max, n, scale, code,
+                                               _ptr(q, ctypes.c_uint16), _vp(Kc), _vp(Vc),
+                                               _vp(Kd), _vp(Vd), _ptr(lens, ctypes.c_int32),
+                                               _fp(ks), _fp(vs), int(ri.size),
+                                               _ptr(ri, ctypes.c_int32), _ptr(rj, ctypes.c_int32),
+                                               _ptr(rt, ctypes.c_int32),
+                                               _ptr(out, ctypes.c_double), int(nthreads))
     if rc:
         raise ValueError(f"oracle: {_ERRORS.get(rc, rc)}")
     return out
+
+
+def code_value(kv: str, code: int) -> float:
+    """The C oracle's decoded value of one cache code (unscaled)."""
+    return float(_load().oracle_code_value(KV_TYPES[kv][0], int(code)))
 
 
 def max_threads() -> int:
@@ -140,3 +186,21 @@ def widen_bf16(bits) -> np.ndarray:
     """bf16 bit patterns (uint16) -> exact fp64 values."""
     u = np.asarray(bits, dtype=np.uint16).astype(np.uint32) << np.uint32(16)
     return u.view(np.float32).astype(np.float64)
+
+
+def widen_codes(codes, kv: str) -> np.ndarray:
+    """Cache codes -> exact unscaled fp64 values (numpy; independent of
+    oracle.c's decoder). fp8 e4m3 follows the OCP definition: bias 7,
+    exponent 0 subnormal, S.1111.111 NaN, no infinities."""
+    if kv == "bf16":
+        return widen_bf16(codes)
+    c = np.asarray(codes).view(np.uint8)
+    if kv == "int8":
+        return c.view(np.int8).astype(np.float64)
+    if kv != "fp8_e4m3":
+        raise ValueError(f"unknown cache type {kv!r}")
+    e = ((c >> 3) & 15).astype(np.int64)
+    m = (c & 7).astype(np.float64)
+    mag = np.where(e == 0, m / 8.0 * 2.0 ** -6, (1.0 + m / 8.0) * np.exp2(e - 7.0))
+    mag = np.where((e == 15) & (m == 7), np.nan, mag)
+    return np.where(c >= 128, -mag, mag)

@@ -15,6 +15,10 @@ dimension):
 4. Eq. 4: split the weights at ``m_c`` and sum
    einsum(bgpn m_c, g m_c k -> bgpnk) + einsum(bgpn m_d, b g m_d k -> bgpnk).
 
+With 8-bit caches (the FAQ on attention quantization) every cache is first
+widened to its values: code value times the per-group scale of keys or
+values (``widen_codes``, a numpy decoder of its own).
+
 This module shares no code with ``oracle.c``; the two agree only because the
 bifurcated method is exact (Appendix E.1).
 """
@@ -22,14 +26,20 @@ from __future__ import annotations
 
 import numpy as np
 
-from . import default_scale, widen_bf16
+from . import default_scale, widen_bf16, widen_codes
 
 
-def bifurcated_attention(q, Kc, Vc, Kd, Vd, lens, scale=None):
+def bifurcated_attention(q, Kc, Vc, Kd, Vd, lens, scale=None, kv="bf16", k_scale=None,
+                         v_scale=None):
     """q [b, h, k] or [b, h, n, k]; the output has q's shape."""
     qf = widen_bf16(q)
-    Kcf, Vcf = widen_bf16(Kc), widen_bf16(Vc)
-    Kdf, Vdf = widen_bf16(Kd), widen_bf16(Vd)
+    g = np.asarray(Kc).shape[0]
+    ks = np.ones(g) if k_scale is None else np.asarray(k_scale, np.float32).astype(np.float64)
+    vs = np.ones(g) if v_scale is None else np.asarray(v_scale, np.float32).astype(np.float64)
+    Kcf = widen_codes(Kc, kv) * ks[:, None, None]
+    Vcf = widen_codes(Vc, kv) * vs[:, None, None]
+    Kdf = widen_codes(Kd, kv) * ks[None, :, None, None]
+    Vdf = widen_codes(Vd, kv) * vs[None, :, None, None]
     lens = np.asarray(lens, dtype=np.int64)
     if qf.ndim == 3:
         b, h, k = qf.shape

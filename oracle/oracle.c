@@ -35,9 +35,25 @@
  * including itself. All sums run sequentially in index order in fp64. Rows
  * a token does not see are never read. Outputs are fp64.
  *
+ * Quantized caches (the FAQ on attention quantization: 8-bit KV halves the
+ * KV bytes and leaves the method unchanged). Reading: a cache may hold 8-bit
+ * codes instead of bf16, with one fp32 scale per KV group for keys and one
+ * for values, shared by the context and decode caches of that group (the
+ * decode cache continues the context's sequence, so one static scale serves
+ * both). The key (value) of a row is k_scale[gam] (v_scale[gam]) times the
+ * code's value:
+ *   int8      two's complement integer in [-128, 127]
+ *   fp8 e4m3  OCP 8-bit float E4M3 (sign, 4-bit exponent with bias 7, 3-bit
+ *             mantissa; exponent 0 is subnormal, m/8 * 2^-6; all-ones
+ *             exponent and mantissa is NaN; no infinities; largest 448)
+ * The scaled values are formed exactly in fp64 (a float times an 8-bit value
+ * fits in 53 bits) and the attention above runs on them unchanged. bf16
+ * caches take scales too (NULL means 1).
+ *
  * Parity pins for this file live in tests/test_oracle_pins.py (closed forms,
  * invariants, brute force, and agreement with an independent numpy
- * evaluation of the bifurcated Eq. 3-4).
+ * evaluation of the bifurcated Eq. 3-4) and tests/test_oracle_kvquant.py
+ * (code tables against torch's float8 conversion, scale identities).
  */
 #include <math.h>
 #include <stdint.h>
@@ -52,11 +68,39 @@
 #define ORACLE_ENOMEM -4
 #define ORACLE_ELENS -6
 
+#define KV_BF16 0
+#define KV_FP8_E4M3 1
+#define KV_INT8 2
+
 static double widen_bf16(uint16_t bits) {
   uint32_t u = (uint32_t)bits << 16;
   float f;
   memcpy(&f, &u, sizeof f);
   return (double)f;
+}
+
+/* OCP E4M3: value = (-1)^s * (1 + m/8) * 2^(e-7) for e > 0, (-1)^s * m/8 *
+ * 2^-6 for e = 0; e = 15 with m = 7 is NaN. */
+static double fp8_e4m3_value(uint8_t c) {
+  const int sgn = c >> 7, e = (c >> 3) & 15, m = c & 7;
+  if (e == 15 && m == 7) return NAN;
+  const double mag = e == 0 ? ldexp((double)m, -9) : ldexp(8.0 + m, e - 10);
+  return sgn ? -mag : mag;
+}
+
+/* Unscaled value of element idx of a cache stored as kv_type. */
+static double code_value(int kv_type, const void *base, size_t idx) {
+  switch (kv_type) {
+    case KV_FP8_E4M3: return fp8_e4m3_value(((const uint8_t *)base)[idx]);
+    case KV_INT8: return (double)(int8_t)((const uint8_t *)base)[idx];
+    default: return widen_bf16(((const uint16_t *)base)[idx]);
+  }
+}
+
+/* Decoded value of one code (for the pins of the code tables). */
+double oracle_code_value(int kv_type, int code) {
+  if (kv_type == KV_BF16) return widen_bf16((uint16_t)code);
+  return code_value(kv_type, &(uint8_t){(uint8_t)code}, 0);
 }
 
 /* One output row (sample i, head j): the textbook two-pass softmax over the
@@ -88,9 +132,10 @@ static int visible(int len, int n, int r) {
   return v > 0 ? v : 0;
 }
 
-static int check_dims(int b, int h, int g, int d, int m_c, int m_d_max, int n,
+static int check_dims(int b, int h, int g, int d, int m_c, int m_d_max, int n, int kv_type,
                       const int32_t *lens) {
   if (b < 1 || h < 1 || g < 1 || d < 1 || m_c < 0 || m_d_max < 0 || n < 1) return ORACLE_EINVAL;
+  if (kv_type != KV_BF16 && kv_type != KV_FP8_E4M3 && kv_type != KV_INT8) return ORACLE_EINVAL;
   if (h % g) return ORACLE_EINVAL;
   for (int i = 0; i < b; ++i)
     if (lens[i] < 0 || lens[i] > m_d_max) return ORACLE_ELENS;
@@ -99,16 +144,37 @@ static int check_dims(int b, int h, int g, int d, int m_c, int m_d_max, int n,
   return ORACLE_OK;
 }
 
+/* The first m_c + vis rows of the explicit per-sample cache of (i, gam):
+ * context rows, then the sample's decode rows, scaled values in fp64. */
+static void gather_rows(int g, int d, int m_c, int m_d_max, int kv_type, const void *Kc,
+                        const void *Vc, const void *Kd, const void *Vd, const float *k_scale,
+                        const float *v_scale, int i, int gam, int vis, double *K, double *V) {
+  const double ks = k_scale ? (double)k_scale[gam] : 1.0;
+  const double vs = v_scale ? (double)v_scale[gam] : 1.0;
+  for (int t = 0; t < m_c; ++t)
+    for (int u = 0; u < d; ++u) {
+      size_t src = ((size_t)gam * m_c + t) * d + u;
+      K[(size_t)t * d + u] = ks * code_value(kv_type, Kc, src);
+      V[(size_t)t * d + u] = vs * code_value(kv_type, Vc, src);
+    }
+  for (int t = 0; t < vis; ++t)
+    for (int u = 0; u < d; ++u) {
+      size_t src = (((size_t)i * g + gam) * m_d_max + t) * d + u;
+      K[(size_t)(m_c + t) * d + u] = ks * code_value(kv_type, Kd, src);
+      V[(size_t)(m_c + t) * d + u] = vs * code_value(kv_type, Vd, src);
+    }
+}
+
 /* Rows (sample row_i[r], head row_j[r], token row_t[r]) for r < nrows,
  * written to out[r*d .. r*d+d). Rows are independent; threads split them. */
-int oracle_attention_rows_fp64(int b, int h, int g, int d, int m_c, int m_d_max, int n,
-                               double scale, const uint16_t *q,
-                               const uint16_t *Kc, const uint16_t *Vc,
-                               const uint16_t *Kd, const uint16_t *Vd,
-                               const int32_t *lens, int nrows,
-                               const int32_t *row_i, const int32_t *row_j,
-                               const int32_t *row_t, double *out, int nthreads) {
-  int rc = check_dims(b, h, g, d, m_c, m_d_max, n, lens);
+int oracle_attention_kv_rows_fp64(int b, int h, int g, int d, int m_c, int m_d_max, int n,
+                                  double scale, int kv_type, const uint16_t *q, const void *Kc,
+                                  const void *Vc, const void *Kd, const void *Vd,
+                                  const int32_t *lens, const float *k_scale,
+                                  const float *v_scale, int nrows, const int32_t *row_i,
+                                  const int32_t *row_j, const int32_t *row_t, double *out,
+                                  int nthreads) {
+  int rc = check_dims(b, h, g, d, m_c, m_d_max, n, kv_type, lens);
   if (rc) return rc;
   for (int r = 0; r < nrows; ++r)
     if (row_i[r] < 0 || row_i[r] >= b || row_j[r] < 0 || row_j[r] >= h || row_t[r] < 0 ||
@@ -131,18 +197,8 @@ int oracle_attention_rows_fp64(int b, int h, int g, int d, int m_c, int m_d_max,
     if (!K || !V || !s || !qrow) {
       failed = 1;
     } else {
-      for (int t = 0; t < m_c; ++t)
-        for (int u = 0; u < d; ++u) {
-          size_t src = ((size_t)gam * m_c + t) * d + u;
-          K[(size_t)t * d + u] = widen_bf16(Kc[src]);
-          V[(size_t)t * d + u] = widen_bf16(Vc[src]);
-        }
-      for (int t = 0; t < vis; ++t)
-        for (int u = 0; u < d; ++u) {
-          size_t src = (((size_t)i * g + gam) * m_d_max + t) * d + u;
-          K[(size_t)(m_c + t) * d + u] = widen_bf16(Kd[src]);
-          V[(size_t)(m_c + t) * d + u] = widen_bf16(Vd[src]);
-        }
+      gather_rows(g, d, m_c, m_d_max, kv_type, Kc, Vc, Kd, Vd, k_scale, v_scale, i, gam, vis, K,
+                  V);
       for (int u = 0; u < d; ++u)
         qrow[u] = widen_bf16(q[(((size_t)i * h + j) * n + tok) * d + u]);
       attend_row(d, m_i, scale, qrow, K, V, s, out + (size_t)r * d);
@@ -158,12 +214,12 @@ int oracle_attention_rows_fp64(int b, int h, int g, int d, int m_c, int m_d_max,
 /* Full output [b, h, n, d]. The per-sample cache of each (i, gam) is
  * materialised once (all len_i rows) and reused by the group's p heads and
  * n tokens, each token taking its visible prefix of the decode rows. */
-int oracle_attention_fp64(int b, int h, int g, int d, int m_c, int m_d_max, int n,
-                          double scale, const uint16_t *q, const uint16_t *Kc,
-                          const uint16_t *Vc, const uint16_t *Kd,
-                          const uint16_t *Vd, const int32_t *lens, double *out,
-                          int nthreads) {
-  int rc = check_dims(b, h, g, d, m_c, m_d_max, n, lens);
+int oracle_attention_kv_fp64(int b, int h, int g, int d, int m_c, int m_d_max, int n,
+                             double scale, int kv_type, const uint16_t *q, const void *Kc,
+                             const void *Vc, const void *Kd, const void *Vd,
+                             const int32_t *lens, const float *k_scale, const float *v_scale,
+                             double *out, int nthreads) {
+  int rc = check_dims(b, h, g, d, m_c, m_d_max, n, kv_type, lens);
   if (rc) return rc;
   const int p = h / g;
   int failed = 0;
@@ -181,18 +237,8 @@ int oracle_attention_fp64(int b, int h, int g, int d, int m_c, int m_d_max, int 
     if (!K || !V || !s || !qrow) {
       failed = 1;
     } else {
-      for (int t = 0; t < m_c; ++t)
-        for (int u = 0; u < d; ++u) {
-          size_t src = ((size_t)gam * m_c + t) * d + u;
-          K[(size_t)t * d + u] = widen_bf16(Kc[src]);
-          V[(size_t)t * d + u] = widen_bf16(Vc[src]);
-        }
-      for (int t = 0; t < lens[i]; ++t)
-        for (int u = 0; u < d; ++u) {
-          size_t src = (((size_t)i * g + gam) * m_d_max + t) * d + u;
-          K[(size_t)(m_c + t) * d + u] = widen_bf16(Kd[src]);
-          V[(size_t)(m_c + t) * d + u] = widen_bf16(Vd[src]);
-        }
+      gather_rows(g, d, m_c, m_d_max, kv_type, Kc, Vc, Kd, Vd, k_scale, v_scale, i, gam, lens[i],
+                  K, V);
       for (int r = 0; r < p; ++r) {
         const int j = gam * p + r;
         for (int tok = 0; tok < n; ++tok) {
@@ -208,6 +254,26 @@ int oracle_attention_fp64(int b, int h, int g, int d, int m_c, int m_d_max, int 
     free(qrow);
   }
   return failed ? ORACLE_ENOMEM : ORACLE_OK;
+}
+
+/* bf16 caches, unit scales. */
+int oracle_attention_fp64(int b, int h, int g, int d, int m_c, int m_d_max, int n,
+                          double scale, const uint16_t *q, const uint16_t *Kc,
+                          const uint16_t *Vc, const uint16_t *Kd, const uint16_t *Vd,
+                          const int32_t *lens, double *out, int nthreads) {
+  return oracle_attention_kv_fp64(b, h, g, d, m_c, m_d_max, n, scale, KV_BF16, q, Kc, Vc, Kd,
+                                  Vd, lens, NULL, NULL, out, nthreads);
+}
+
+int oracle_attention_rows_fp64(int b, int h, int g, int d, int m_c, int m_d_max, int n,
+                               double scale, const uint16_t *q, const uint16_t *Kc,
+                               const uint16_t *Vc, const uint16_t *Kd, const uint16_t *Vd,
+                               const int32_t *lens, int nrows, const int32_t *row_i,
+                               const int32_t *row_j, const int32_t *row_t, double *out,
+                               int nthreads) {
+  return oracle_attention_kv_rows_fp64(b, h, g, d, m_c, m_d_max, n, scale, KV_BF16, q, Kc, Vc,
+                                       Kd, Vd, lens, NULL, NULL, nrows, row_i, row_j, row_t, out,
+                                       nthreads);
 }
 
 int oracle_max_threads(void) {

@@ -19,6 +19,16 @@ Layouts (row-major, bf16 stored as uint16 bit patterns):
 Recipe: numpy PCG64 seeded per workload, draws in the order q, Kc, Vc, Kd, Vd,
 each ``standard_normal(float32)`` rounded to bf16 with round-to-nearest-even;
 then ``lens`` (``integers(1, m_d_max + 1)`` when ragged, else all ``m_d_max``).
+
+8-bit caches (``kv="fp8_e4m3"`` or ``"int8"``, stored as uint8 codes): the
+same draws, multiplied by ``qmax / 4.5`` (4.5 standard deviations map to the
+largest code: 448 for OCP fp8 E4M3, 127 for int8), saturated at +-qmax and
+encoded with round-to-nearest-even (fp8 through torch's ``float8_e4m3fn``
+cast, int8 through ``numpy.rint``). After ``lens``, per-group factors
+``c = 2**uniform(-1, 1)`` are drawn for keys, then for values, and the
+scales are ``k_scale = c_k * 4.5 / qmax`` (``v_scale`` likewise), so a
+group's dequantized keys are close to its draws times ``c_k``: heads of
+different magnitude, as in trained models.
 """
 from __future__ import annotations
 
@@ -27,6 +37,13 @@ import dataclasses
 import numpy as np
 
 BF16_NAN = np.uint16(0x7FC0)
+KV_TYPES = ("bf16", "fp8_e4m3", "int8")
+KV_BYTES = {"bf16": 2, "fp8_e4m3": 1, "int8": 1}
+KV_QMAX = {"fp8_e4m3": 448.0, "int8": 127.0}
+KV_CLIP_SIGMA = 4.5
+# A code that poisons rows past a sample's length: NaN in fp8 E4M3, the
+# largest value in int8.
+KV_POISON = {"fp8_e4m3": np.uint8(0x7F), "int8": np.uint8(0x7F)}
 
 
 @dataclasses.dataclass(frozen=True)
@@ -41,6 +58,7 @@ class Workload:
     ragged: bool
     seed: int
     n: int = 1  # new tokens per sample (draft tokens verified together when > 1)
+    kv: str = "bf16"  # cache element type: bf16, or 8-bit codes with per-group scales
 
     @property
     def p(self) -> int:
@@ -51,7 +69,8 @@ class Workload:
 # of 128) at 16 and 32 samples over an 8k context; an MQA layer with 128
 # samples over 16k; and a GQA layer (8 KV groups) with 256 samples over 32k
 # and ragged decode lengths uniform in [1, 1024]. Then the 32-sample MHA layer
-# verifying 4 draft tokens per sample in one step (speculative decoding).
+# verifying 4 draft tokens per sample in one step (speculative decoding), and
+# the 32-sample MHA and the MQA layer with 8-bit KV caches.
 WORKLOADS = {
     w.name: w
     for w in (
@@ -61,6 +80,11 @@ WORKLOADS = {
         Workload("mqa_b128_mc16k_md512", 128, 32, 1, 128, 16384, 512, False, 1004),
         Workload("gqa8_b256_mc32k_ragged1024", 256, 32, 8, 128, 32768, 1024, True, 1005),
         Workload("mha7b_b32_mc8k_md512_draft4", 32, 32, 32, 128, 8192, 512, False, 1006, 4),
+        Workload("mha7b_b32_mc8k_md512_fp8", 32, 32, 32, 128, 8192, 512, False, 1007, 1,
+                 "fp8_e4m3"),
+        Workload("mha7b_b32_mc8k_md512_int8", 32, 32, 32, 128, 8192, 512, False, 1008, 1, "int8"),
+        Workload("mqa_b128_mc16k_md512_fp8", 128, 32, 1, 128, 16384, 512, False, 1009, 1,
+                 "fp8_e4m3"),
     )
 }
 WORKLOAD_ORDER = list(WORKLOADS)
@@ -89,24 +113,51 @@ def _normal_bf16(rng: np.random.Generator, shape) -> np.ndarray:
     return out.reshape(shape)
 
 
+def _encode(y: np.ndarray, kv: str) -> np.ndarray:
+    """float32 values already in code units -> saturated 8-bit codes (RNE)."""
+    qmax = KV_QMAX[kv]
+    y = np.clip(y, -qmax, qmax)
+    if kv == "int8":
+        return np.rint(y).astype(np.int8).view(np.uint8)
+    import torch
+    return torch.from_numpy(np.ascontiguousarray(y)).to(torch.float8_e4m3fn) \
+        .view(torch.uint8).numpy()
+
+
+def _normal_codes(rng: np.random.Generator, shape, kv: str) -> np.ndarray:
+    n = int(np.prod(shape))
+    out = np.empty(n, dtype=np.uint8)
+    mult = np.float32(KV_QMAX[kv] / KV_CLIP_SIGMA)
+    step = 1 << 24
+    for s in range(0, n, step):
+        e = min(n, s + step)
+        out[s:e] = _encode(rng.standard_normal(e - s, dtype=np.float32) * mult, kv)
+    return out.reshape(shape)
+
+
 def make_inputs(b, h, g, d, m_c, m_d_max, *, seed, ragged=False, lens=None,
-                poison_tail=False, with_decode_tail=True, n=1):
+                poison_tail=False, with_decode_tail=True, n=1, kv="bf16"):
     """Draw one problem instance.
 
     ``lens`` overrides the drawn lengths (it is applied after all draws, so the
     tensors stay identical). ``poison_tail`` fills decode rows ``t >= len_i``
     with bf16 NaN, so any read of them shows up in the output. With ``n > 1``
     new tokens per sample, q is [b, h, n, d] and ragged lengths are drawn in
-    [n, m_d_max] (the n tokens are the last n valid decode rows).
+    [n, m_d_max] (the n tokens are the last n valid decode rows). With an
+    8-bit ``kv`` the caches are uint8 codes and the dict also holds ``kv``,
+    ``k_scale`` and ``v_scale`` (float32 [g]).
     """
     if h % g:
         raise ValueError("h must be a multiple of g")
+    if kv not in KV_TYPES:
+        raise ValueError(f"unknown cache type {kv!r}")
     rng = np.random.Generator(np.random.PCG64(seed))
     q = _normal_bf16(rng, (b, h, d) if n == 1 else (b, h, n, d))
-    Kc = _normal_bf16(rng, (g, m_c, d))
-    Vc = _normal_bf16(rng, (g, m_c, d))
-    Kd = _normal_bf16(rng, (b, g, m_d_max, d))
-    Vd = _normal_bf16(rng, (b, g, m_d_max, d))
+    cache = _normal_bf16 if kv == "bf16" else (lambda r, shp: _normal_codes(r, shp, kv))
+    Kc = cache(rng, (g, m_c, d))
+    Vc = cache(rng, (g, m_c, d))
+    Kd = cache(rng, (b, g, m_d_max, d))
+    Vd = cache(rng, (b, g, m_d_max, d))
     if ragged:
         drawn = rng.integers(min(n, m_d_max) if m_d_max > 0 else 0, m_d_max + 1,
                              size=b).astype(np.int32) if m_d_max > 0 else np.zeros(b, np.int32)
@@ -114,28 +165,37 @@ def make_inputs(b, h, g, d, m_c, m_d_max, *, seed, ragged=False, lens=None,
         drawn = np.full(b, m_d_max, dtype=np.int32)
     if lens is not None:
         drawn = np.asarray(lens, dtype=np.int32).reshape(b).copy()
+    scales = {}
+    if kv != "bf16":
+        base = KV_CLIP_SIGMA / KV_QMAX[kv]
+        c_k = np.exp2(rng.uniform(-1.0, 1.0, size=g))
+        c_v = np.exp2(rng.uniform(-1.0, 1.0, size=g))
+        scales = dict(kv=kv, k_scale=(c_k * base).astype(np.float32),
+                      v_scale=(c_v * base).astype(np.float32))
     if poison_tail:
+        poison = BF16_NAN if kv == "bf16" else KV_POISON[kv]
         for i in range(b):
-            Kd[i, :, drawn[i]:, :] = BF16_NAN
-            Vd[i, :, drawn[i]:, :] = BF16_NAN
-    return dict(q=q, Kc=Kc, Vc=Vc, Kd=Kd, Vd=Vd, lens=drawn)
+            Kd[i, :, drawn[i]:, :] = poison
+            Vd[i, :, drawn[i]:, :] = poison
+    return dict(q=q, Kc=Kc, Vc=Vc, Kd=Kd, Vd=Vd, lens=drawn, **scales)
 
 
 def make_workload_inputs(w: Workload, *, seed=None, poison_tail=False):
     return make_inputs(w.b, w.h, w.g, w.d, w.m_c, w.m_d_max,
                        seed=w.seed if seed is None else seed, ragged=w.ragged,
-                       poison_tail=poison_tail, n=w.n)
+                       poison_tail=poison_tail, n=w.n, kv=w.kv)
 
 
-def kv_bytes(g, d, m_c, lens) -> int:
-    """Algorithmic KV bytes of one bifurcated step: one bf16 copy of context
-    K and V plus every sample's valid decode K and V (Section 4.3)."""
-    return 2 * 2 * g * d * (int(m_c) + int(np.sum(lens, dtype=np.int64)))
+def kv_bytes(g, d, m_c, lens, kv="bf16") -> int:
+    """Algorithmic KV bytes of one bifurcated step: one copy of context K and
+    V plus every sample's valid decode K and V (Section 4.3), at the cache's
+    element size (2 bytes bf16, 1 byte for 8-bit codes)."""
+    return 2 * KV_BYTES[kv] * g * d * (int(m_c) + int(np.sum(lens, dtype=np.int64)))
 
 
-def replicated_kv_bytes(b, g, d, m_c, lens) -> int:
+def replicated_kv_bytes(b, g, d, m_c, lens, kv="bf16") -> int:
     """KV bytes when the context is read once per sample (Section 4.3)."""
-    return 2 * 2 * g * d * (b * int(m_c) + int(np.sum(lens, dtype=np.int64)))
+    return 2 * KV_BYTES[kv] * g * d * (b * int(m_c) + int(np.sum(lens, dtype=np.int64)))
 
 
 def attention_flops(h, d, b, m_c, lens, n=1) -> int:
