@@ -5,7 +5,8 @@
 
 A step is one bifattn_decode call (context partials, decode partials and the
 combine) over one batch of seeded synthetic inputs that are already resident
-in HBM. Steps rotate over several device copies of the inputs (about 1.2 GB
+in HBM (bifattn_decode_scaled for the workloads with 8-bit KV caches, whose
+bytes count one per element). Steps rotate over several device copies of the inputs (about 1.2 GB
 or more in total) so that no step finds its KV cache in the 256 MB Infinity
 Cache left behind by the previous one. The timed region is bracketed by
 torch.cuda.synchronize() on both sides.
@@ -65,11 +66,20 @@ def measured_traffic(workload: str):
 
 
 def to_device(x):
+    """q as bf16; caches as bf16, or as uint8 codes with fp32 scales."""
     import torch
+    kv = x.get("kv", "bf16")
     out = {}
     for k in ("q", "Kc", "Vc", "Kd", "Vd"):
-        out[k] = torch.from_numpy(np.ascontiguousarray(x[k]).view(np.int16)).view(torch.bfloat16).cuda()
+        a = np.ascontiguousarray(x[k])
+        if k == "q" or kv == "bf16":
+            out[k] = torch.from_numpy(a.view(np.int16)).view(torch.bfloat16).cuda()
+        else:
+            out[k] = torch.from_numpy(a.view(np.uint8)).cuda()
     out["lens"] = torch.from_numpy(np.ascontiguousarray(x["lens"], dtype=np.int32)).cuda()
+    for k in ("k_scale", "v_scale"):
+        if k in x:
+            out[k] = torch.from_numpy(np.ascontiguousarray(x[k], dtype=np.float32)).cuda()
     return out
 
 
@@ -86,7 +96,7 @@ def cpu_baseline(x, w, min_seconds):
         if el >= min_seconds:
             break
     per = el / reps
-    B = workloads.kv_bytes(w.g, w.d, w.m_c, x["lens"])
+    B = workloads.kv_bytes(w.g, w.d, w.m_c, x["lens"], w.kv)
     return {"value": round(B / per / 1e9, 4), "unit": "GB/s", "cores": threads, "kind": "oracle",
             "sample": f"whole {w.name} step (b={w.b}), fp64, repeated {reps}x over {el:.1f} s; "
                       f"{per * 1e3:.1f} ms per step"}
@@ -215,7 +225,7 @@ def main():
     w = workloads.WORKLOADS[args.workload]
     log(f"[bench] generating {w.name}")
     x = workloads.make_workload_inputs(w)
-    B_kv = workloads.kv_bytes(w.g, w.d, w.m_c, x["lens"])
+    B_kv = workloads.kv_bytes(w.g, w.d, w.m_c, x["lens"], w.kv)
     flops = workloads.attention_flops(w.h, w.d, w.b, w.m_c, x["lens"], n=w.n)
     torch.cuda.set_device(0)
     dev0 = to_device(x)
@@ -223,13 +233,17 @@ def main():
     copies = max(3, -(-4 * MALL_BYTES // B_kv))
     devs = [dev0] + [{k: v.clone() for k, v in dev0.items()} for _ in range(copies - 1)]
     out = torch.empty(tuple(x["q"].shape), dtype=torch.float32, device="cuda")
-    plan = bif.Plan(w.b, w.h, w.g, w.d, w.m_c, w.m_d_max, n=w.n)
+    plan = bif.Plan(w.b, w.h, w.g, w.d, w.m_c, w.m_d_max, n=w.n, kv=w.kv)
     info = plan.info()
     log(f"[bench] plan {info}, {copies} input copies")
 
     def step(k):
         d = devs[k % copies]
-        bif.bifattn_decode(plan, d["q"], d["Kc"], d["Vc"], d["Kd"], d["Vd"], d["lens"], out)
+        if w.kv == "bf16":
+            bif.bifattn_decode(plan, d["q"], d["Kc"], d["Vc"], d["Kd"], d["Vd"], d["lens"], out)
+        else:
+            bif.bifattn_decode_scaled(plan, d["q"], d["Kc"], d["Vc"], d["Kd"], d["Vd"], d["lens"],
+                                      d["k_scale"], d["v_scale"], out)
 
     for k in range(args.warmup):
         step(k)
@@ -279,20 +293,22 @@ def main():
     if not args.no_ablation:
         # Replicated cache built on the device: every sample's own copy of the context.
         rows = w.m_c + w.m_d_max
-        rep_bytes = 2 * w.b * w.g * rows * w.d * 2
+        rep_bytes = 2 * w.b * w.g * rows * w.d * workloads.KV_BYTES[w.kv]
         if rep_bytes < 40e9:
             K = torch.cat([dev0["Kc"].unsqueeze(0).expand(w.b, -1, -1, -1), dev0["Kd"]], dim=2).contiguous()
             V = torch.cat([dev0["Vc"].unsqueeze(0).expand(w.b, -1, -1, -1), dev0["Vd"]], dim=2).contiguous()
             ref_out = out.clone()
-            bif.bifattn_decode_replicated(plan, dev0["q"], K, V, dev0["lens"], out)
+            ks, vs = dev0.get("k_scale"), dev0.get("v_scale")
+            bif.bifattn_decode_replicated_scaled(plan, dev0["q"], K, V, dev0["lens"], ks, vs, out)
             torch.cuda.synchronize()
             rep_steps = max(5, args.steps // 10)
             t0 = time.perf_counter()
             for _ in range(rep_steps):
-                bif.bifattn_decode_replicated(plan, dev0["q"], K, V, dev0["lens"], out)
+                bif.bifattn_decode_replicated_scaled(plan, dev0["q"], K, V, dev0["lens"], ks, vs,
+                                                     out)
             torch.cuda.synchronize()
             rep_us = (time.perf_counter() - t0) * 1e6 / rep_steps
-            B_rep = workloads.replicated_kv_bytes(w.b, w.g, w.d, w.m_c, x["lens"])
+            B_rep = workloads.replicated_kv_bytes(w.b, w.g, w.d, w.m_c, x["lens"], w.kv)
             step(0)
             torch.cuda.synchronize()
             ablation = {"kernel": "bifattn_decode_replicated", "us_per_step": round(rep_us, 3),
@@ -326,7 +342,7 @@ def main():
         "dtype": "bf16",
         "data": "synthetic",
         "config": {"workload": w.name, "b": w.b, "h": w.h, "g": w.g, "d": w.d, "m_c": w.m_c,
-                   "m_d": w.m_d_max, "new_tokens": w.n,
+                   "m_d": w.m_d_max, "new_tokens": w.n, "kv_cache": w.kv,
                    "decode_lens": "ragged" if w.ragged else "uniform",
                    "parallelism": "single GPU"},
         "roofline": {"kernel": "partials_kernel (context + decode partials)", "bound": "hbm",

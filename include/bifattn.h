@@ -21,10 +21,18 @@
  * Layouts (all row-major, all device memory, bf16 = 16-bit brain float):
  *   q       bf16 [b][h][n][d]       token r of head j of sample i at ((i*h + j)*n + r)*d
  *                                   ([b][h][d] when n = 1)
- *   Kc, Vc  bf16 [g][m_c][d]        one shared copy of the context cache
- *   Kd, Vd  bf16 [b][g][m_d_max][d] per-sample decode cache
+ *   Kc, Vc  kv  [g][m_c][d]         one shared copy of the context cache
+ *   Kd, Vd  kv  [b][g][m_d_max][d]  per-sample decode cache
  *   decode_lens int32 [b]           valid decode rows per sample
+ *   k_scale, v_scale fp32 [g]       per-group key / value scales (optional)
  *   out     fp32 [b][h][n][d]
+ * kv is the plan's cache element type (dims.kv_type): bf16, or 8-bit codes
+ * (OCP fp8 E4M3, or two's complement int8), one byte each. The FAQ on
+ * attention quantization notes that 8-bit KV halves the KV bytes and leaves
+ * the method unchanged; here the key of a cache row is k_scale[gam] times
+ * its codes' values and its value v_scale[gam] times its codes' values, the
+ * same scales for the group's context and decode caches (NULL scales mean
+ * 1). Codes are widened to bf16 exactly; the scales enter in fp32.
  * Head j reads KV group j / p (group-major, the bgpnk order of Eq. 1).
  * Decode rows t >= len_i are never read into arithmetic: they may hold
  * anything, NaN included. With n > 1 the n new tokens are the last n of the
@@ -61,7 +69,7 @@
 extern "C" {
 #endif
 
-#define BIFATTN_VERSION 2
+#define BIFATTN_VERSION 3
 
 typedef enum {
   BIFATTN_OK = 0,
@@ -71,8 +79,16 @@ typedef enum {
   BIFATTN_EALIGN = -3,       /* a tensor pointer not 16-byte aligned */
   BIFATTN_ENOMEM = -4,       /* workspace or event allocation failed */
   BIFATTN_EHIP = -5,         /* a HIP runtime call or kernel launch failed */
-  BIFATTN_ELENS = -6         /* a decode length was outside [0, m_d_max] */
+  BIFATTN_ELENS = -6,        /* a decode length was outside [0, m_d_max] */
+  BIFATTN_ESCALE = -7        /* a key or value scale was not a positive normal float */
 } bifattn_status_t;
+
+/* Cache element types (bifattn_dims_t.kv_type). */
+typedef enum {
+  BIFATTN_KV_BF16 = 0,     /* bf16 keys and values */
+  BIFATTN_KV_FP8_E4M3 = 1, /* OCP 8-bit float E4M3 codes (bias 7, no infinities, max 448) */
+  BIFATTN_KV_INT8 = 2      /* two's complement 8-bit integer codes */
+} bifattn_kv_type_t;
 
 /* Problem dimensions (Section 3.1 notation; d is the head dimension). */
 typedef struct {
@@ -84,6 +100,7 @@ typedef struct {
   int32_t m_d_max; /* decode cache capacity per sample, >= 0 */
   float scale;     /* softmax scale on q.k; 0 selects 1/sqrt(d) */
   int32_t n;       /* new tokens per sample, >= 1 (0 is taken as 1) */
+  int32_t kv_type; /* a bifattn_kv_type_t: element type of Kc, Vc, Kd, Vd */
 } bifattn_dims_t;
 
 typedef struct bifattn_plan_s *bifattn_plan_t;
@@ -112,10 +129,10 @@ typedef enum {
  * Validate dims and allocate the plan and its workspace on the current HIP
  * device. On success *plan is set; on failure *plan is left NULL.
  * Errors: EINVAL (null argument, b/h/g/m_c < 1, m_d_max < 0, n < 0,
- * h % g != 0, sizes whose byte counts overflow), EUNSUPPORTED (d not 64 or
- * 128, (h/g)*n > 64, or one sample's cache rows (m_c + m_d_max) * d * 2
- * bytes beyond 2^31 - 1), ENOMEM (device allocation failed), EHIP (no
- * usable device).
+ * h % g != 0, unknown kv_type, sizes whose byte counts overflow),
+ * EUNSUPPORTED (d not 64 or 128, (h/g)*n > 64, or one sample's cache rows
+ * (m_c + m_d_max) * d * (bytes per element) beyond 2^31 - 1), ENOMEM
+ * (device allocation failed), EHIP (no usable device).
  */
 bifattn_status_t bifattn_plan_create(const bifattn_dims_t *dims, bifattn_plan_t *plan);
 
@@ -144,9 +161,27 @@ bifattn_status_t bifattn_decode(bifattn_plan_t plan, const void *q, const void *
                                 const int32_t *decode_lens, float *out, hipStream_t stream);
 
 /*
+ * bifattn_decode with per-group scales (the FAQ on attention quantization):
+ * keys of group gam are k_scale[gam] times the cache entries, values
+ * v_scale[gam] times them, for the context and the decode cache alike. The
+ * key scale folds into the softmax scale of the group's work-groups and the
+ * value scale into the combine, so the cost is that of bifattn_decode.
+ * k_scale, v_scale: device fp32 [g], or NULL for all 1. Scales must be
+ * positive normal floats; a call that finds another value sets the plan's
+ * device-side flag that bifattn_plan_status reports as BIFATTN_ESCALE, and
+ * the output rows of that group are unspecified (NaN possible).
+ * Errors: those of bifattn_decode; EALIGN also for a scale pointer that is
+ * not 4-byte aligned.
+ */
+bifattn_status_t bifattn_decode_scaled(bifattn_plan_t plan, const void *q, const void *Kc,
+                                       const void *Vc, const void *Kd, const void *Vd,
+                                       const int32_t *decode_lens, const float *k_scale,
+                                       const float *v_scale, float *out, hipStream_t stream);
+
+/*
  * Ablation without bifurcation (the baseline of Section 4.1): the same
  * attention, but every sample reads its own physically replicated cache
- *   K, V   bf16 [b][g][m_c + m_d_max][d], rows 0..m_c-1 the context copy,
+ *   K, V   kv [b][g][m_c + m_d_max][d], rows 0..m_c-1 the context copy,
  *          rows m_c..m_c+len_i-1 the sample's decode rows,
  * so the context is read b times. Same partial and combine kernels, no
  * context part. Same errors as bifattn_decode.
@@ -155,14 +190,23 @@ bifattn_status_t bifattn_decode_replicated(bifattn_plan_t plan, const void *q, c
                                            const void *V, const int32_t *decode_lens,
                                            float *out, hipStream_t stream);
 
+/* The replicated ablation with per-group scales, as bifattn_decode_scaled. */
+bifattn_status_t bifattn_decode_replicated_scaled(bifattn_plan_t plan, const void *q,
+                                                  const void *K, const void *V,
+                                                  const int32_t *decode_lens,
+                                                  const float *k_scale, const float *v_scale,
+                                                  float *out, hipStream_t stream);
+
 /*
  * Append one decoding step's keys and values to the decode cache (the decode
  * cache holds the keys and values of the previous decoding steps, Section
  * 3.1), so that a generation loop runs append then decode each step:
  *   Kd[i, gam, len_i + r, :] = k_new[i, gam, r, :]   (r < n; Vd likewise)
  *   decode_lens[i] += n
- * k_new, v_new bf16 [b][g][n][d] (the step's n new tokens per sample, n from
- * the plan); Kd, Vd, decode_lens as in bifattn_decode, updated in place on
+ * k_new, v_new [b][g][n][d] of the plan's cache element type (the step's n
+ * new tokens per sample, n from the plan; 8-bit codes are copied as they
+ * are, encoded by the caller with the group's scales); Kd, Vd, decode_lens
+ * as in bifattn_decode, updated in place on
  * `stream`. Rows that would pass m_d_max are dropped (the length stops at
  * m_d_max), a length outside [0, m_d_max] is clamped first; both raise the
  * device-side flag that bifattn_plan_status reports as BIFATTN_ELENS.
@@ -173,10 +217,11 @@ bifattn_status_t bifattn_append_kv(bifattn_plan_t plan, const void *k_new, const
                                    void *Kd, void *Vd, int32_t *decode_lens, hipStream_t stream);
 
 /*
- * Synchronise `stream`, then report and clear the plan's device-side flag:
- * BIFATTN_ELENS if any call since the last check saw a decode length outside
- * [0, m_d_max] (the call used the clamped length) or an append ran out of
- * capacity, else BIFATTN_OK.
+ * Synchronise `stream`, then report and clear the plan's device-side flags:
+ * BIFATTN_ESCALE if any call since the last check saw a scale that is not a
+ * positive normal float, else BIFATTN_ELENS if one saw a decode length
+ * outside [0, m_d_max] (the call used the clamped length) or an append ran
+ * out of capacity, else BIFATTN_OK.
  * EHIP if the stream reports an error.
  */
 bifattn_status_t bifattn_plan_status(bifattn_plan_t plan, hipStream_t stream);

@@ -16,12 +16,15 @@ import os
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libbifattn.so")
 
-OK, EINVAL, EUNSUPPORTED, EALIGN, ENOMEM, EHIP, ELENS = 0, -1, -2, -3, -4, -5, -6
+OK, EINVAL, EUNSUPPORTED, EALIGN, ENOMEM, EHIP, ELENS, ESCALE = 0, -1, -2, -3, -4, -5, -6, -7
 KERNEL_PARTIALS, KERNEL_COMBINE, KERNEL_CALL = 0, 1, 2
+#: Cache element types (bifattn_kv_type_t).
+KV_TYPES = {"bf16": 0, "fp8_e4m3": 1, "int8": 2}
 
 EXPORTED = (
     "bifattn_plan_create", "bifattn_plan_destroy", "bifattn_plan_get_info", "bifattn_decode",
-    "bifattn_decode_replicated", "bifattn_append_kv", "bifattn_plan_status", "bifattn_plan_set_timing",
+    "bifattn_decode_scaled", "bifattn_decode_replicated", "bifattn_decode_replicated_scaled",
+    "bifattn_append_kv", "bifattn_plan_status", "bifattn_plan_set_timing",
     "bifattn_plan_read_timing", "bifattn_status_string", "bifattn_version",
 )
 
@@ -35,7 +38,7 @@ class BifattnError(RuntimeError):
 class Dims(ctypes.Structure):
     _fields_ = [("b", ctypes.c_int32), ("h", ctypes.c_int32), ("g", ctypes.c_int32),
                 ("d", ctypes.c_int32), ("m_c", ctypes.c_int32), ("m_d_max", ctypes.c_int32),
-                ("scale", ctypes.c_float), ("n", ctypes.c_int32)]
+                ("scale", ctypes.c_float), ("n", ctypes.c_int32), ("kv_type", ctypes.c_int32)]
 
 
 class PlanInfo(ctypes.Structure):
@@ -65,7 +68,9 @@ def lib() -> ctypes.CDLL:
         L.bifattn_plan_destroy.argtypes = [vp]
         L.bifattn_plan_get_info.argtypes = [vp, ctypes.POINTER(PlanInfo)]
         L.bifattn_decode.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp]
+        L.bifattn_decode_scaled.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp]
         L.bifattn_decode_replicated.argtypes = [vp, vp, vp, vp, vp, vp, vp]
+        L.bifattn_decode_replicated_scaled.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp]
         L.bifattn_append_kv.argtypes = [vp, vp, vp, vp, vp, vp, vp]
         L.bifattn_plan_status.argtypes = [vp, vp]
         L.bifattn_plan_set_timing.argtypes = [vp, st, i32]
@@ -95,10 +100,13 @@ def _check(status: int, what: str):
 
 class Plan:
     """A bifattn_plan_t: problem dimensions plus the workspace it owns
-    (n = new tokens per sample)."""
+    (n = new tokens per sample; kv = cache element type, a KV_TYPES name)."""
 
-    def __init__(self, b, h, g, d, m_c, m_d_max, scale=0.0, n=1):
-        self.dims = Dims(b, h, g, d, m_c, m_d_max, scale, n)
+    def __init__(self, b, h, g, d, m_c, m_d_max, scale=0.0, n=1, kv="bf16"):
+        if kv not in KV_TYPES:
+            raise ValueError(f"kv must be one of {sorted(KV_TYPES)}")
+        self.kv = kv
+        self.dims = Dims(b, h, g, d, m_c, m_d_max, scale, n, KV_TYPES[kv])
         handle = ctypes.c_void_p()
         _check(lib().bifattn_plan_create(ctypes.byref(self.dims), ctypes.byref(handle)),
                "bifattn_plan_create")
@@ -127,8 +135,8 @@ class Plan:
         return info.as_dict()
 
 
-def bifattn_plan_create(b, h, g, d, m_c, m_d_max, scale=0.0, n=1) -> Plan:
-    return Plan(b, h, g, d, m_c, m_d_max, scale, n)
+def bifattn_plan_create(b, h, g, d, m_c, m_d_max, scale=0.0, n=1, kv="bf16") -> Plan:
+    return Plan(b, h, g, d, m_c, m_d_max, scale, n, kv)
 
 
 def bifattn_plan_destroy(plan: Plan):
@@ -147,12 +155,14 @@ def _stream_ptr(stream):
 
 
 def _tensor(t, shape, dtype, device, name):
-    """shape: one shape, or a list of accepted shapes."""
+    """shape: one shape, or a list of accepted shapes; dtype: one dtype or a
+    tuple of accepted dtypes."""
     import torch
     if not isinstance(t, torch.Tensor):
         raise TypeError(f"{name} must be a torch.Tensor")
-    if t.dtype != dtype:
-        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    dtypes = dtype if isinstance(dtype, tuple) else (dtype,)
+    if t.dtype not in dtypes:
+        raise TypeError(f"{name} must be {' or '.join(map(str, dtypes))}, got {t.dtype}")
     shapes = [tuple(x) for x in shape] if isinstance(shape, list) else [tuple(shape)]
     if tuple(t.shape) not in shapes:
         raise ValueError(f"{name} must have shape {' or '.join(map(str, shapes))}, "
@@ -162,6 +172,22 @@ def _tensor(t, shape, dtype, device, name):
     if not t.is_contiguous():
         raise ValueError(f"{name} must be contiguous")
     return ctypes.c_void_p(t.data_ptr())
+
+
+def _cache_dtypes(plan):
+    """torch dtypes accepted for the plan's cache tensors: bf16, or any
+    one-byte type holding the 8-bit codes."""
+    import torch
+    if plan.dims.kv_type == KV_TYPES["bf16"]:
+        return torch.bfloat16
+    return (torch.uint8, torch.int8, torch.float8_e4m3fn)
+
+
+def _scales(plan, k_scale, v_scale, dev):
+    import torch
+    D = plan.dims
+    return [ctypes.c_void_p(None) if s is None else _tensor(s, (D.g,), torch.float32, dev, name)
+            for s, name in ((k_scale, "k_scale"), (v_scale, "v_scale"))]
 
 
 def _query_shapes(D):
@@ -176,65 +202,85 @@ def _query_shapes(D):
 def bifattn_decode(plan: Plan, q, Kc, Vc, Kd, Vd, decode_lens, out, stream=None):
     """Enqueue one bifurcated decode step (see include/bifattn.h).
 
-    q bf16 [b,h,n,d] ([b,h,d] when n = 1); Kc, Vc bf16 [g,m_c,d];
-    Kd, Vd bf16 [b,g,m_d_max,d]; decode_lens int32 [b]; out fp32 shaped like
-    q; all on the same GPU.
+    q bf16 [b,h,n,d] ([b,h,d] when n = 1); Kc, Vc [g,m_c,d] and Kd, Vd
+    [b,g,m_d_max,d] of the plan's cache type (bf16, or one-byte codes);
+    decode_lens int32 [b]; out fp32 shaped like q; all on the same GPU.
     """
+    bifattn_decode_scaled(plan, q, Kc, Vc, Kd, Vd, decode_lens, None, None, out, stream)
+
+
+def bifattn_decode_scaled(plan: Plan, q, Kc, Vc, Kd, Vd, decode_lens, k_scale, v_scale, out,
+                          stream=None):
+    """bifattn_decode with per-group key / value scales (fp32 [g] tensors on
+    the GPU, or None for 1)."""
     import torch
     D = plan.dims
     dev = q.device
+    cd = _cache_dtypes(plan)
     args = [
         _tensor(q, _query_shapes(D), torch.bfloat16, dev, "q"),
-        _tensor(Kc, (D.g, D.m_c, D.d), torch.bfloat16, dev, "Kc"),
-        _tensor(Vc, (D.g, D.m_c, D.d), torch.bfloat16, dev, "Vc"),
-        _tensor(Kd, (D.b, D.g, D.m_d_max, D.d), torch.bfloat16, dev, "Kd"),
-        _tensor(Vd, (D.b, D.g, D.m_d_max, D.d), torch.bfloat16, dev, "Vd"),
+        _tensor(Kc, (D.g, D.m_c, D.d), cd, dev, "Kc"),
+        _tensor(Vc, (D.g, D.m_c, D.d), cd, dev, "Vc"),
+        _tensor(Kd, (D.b, D.g, D.m_d_max, D.d), cd, dev, "Kd"),
+        _tensor(Vd, (D.b, D.g, D.m_d_max, D.d), cd, dev, "Vd"),
         _tensor(decode_lens, (D.b,), torch.int32, dev, "decode_lens"),
+        *_scales(plan, k_scale, v_scale, dev),
         _tensor(out, [tuple(q.shape)], torch.float32, dev, "out"),
     ]
-    _check(lib().bifattn_decode(plan.handle, *args, _stream_ptr(stream)), "bifattn_decode")
+    _check(lib().bifattn_decode_scaled(plan.handle, *args, _stream_ptr(stream)),
+           "bifattn_decode_scaled")
 
 
 def bifattn_decode_replicated(plan: Plan, q, K, V, decode_lens, out, stream=None):
     """Enqueue the ablation over a physically replicated cache
-    K, V bf16 [b, g, m_c + m_d_max, d]."""
+    K, V [b, g, m_c + m_d_max, d] of the plan's cache type."""
+    bifattn_decode_replicated_scaled(plan, q, K, V, decode_lens, None, None, out, stream)
+
+
+def bifattn_decode_replicated_scaled(plan: Plan, q, K, V, decode_lens, k_scale, v_scale, out,
+                                     stream=None):
+    """The replicated ablation with per-group scales."""
     import torch
     D = plan.dims
     dev = q.device
     rows = D.m_c + D.m_d_max
+    cd = _cache_dtypes(plan)
     args = [
         _tensor(q, _query_shapes(D), torch.bfloat16, dev, "q"),
-        _tensor(K, (D.b, D.g, rows, D.d), torch.bfloat16, dev, "K"),
-        _tensor(V, (D.b, D.g, rows, D.d), torch.bfloat16, dev, "V"),
+        _tensor(K, (D.b, D.g, rows, D.d), cd, dev, "K"),
+        _tensor(V, (D.b, D.g, rows, D.d), cd, dev, "V"),
         _tensor(decode_lens, (D.b,), torch.int32, dev, "decode_lens"),
+        *_scales(plan, k_scale, v_scale, dev),
         _tensor(out, [tuple(q.shape)], torch.float32, dev, "out"),
     ]
-    _check(lib().bifattn_decode_replicated(plan.handle, *args, _stream_ptr(stream)),
-           "bifattn_decode_replicated")
+    _check(lib().bifattn_decode_replicated_scaled(plan.handle, *args, _stream_ptr(stream)),
+           "bifattn_decode_replicated_scaled")
 
 
 def bifattn_append_kv(plan: Plan, k_new, v_new, Kd, Vd, decode_lens, stream=None):
     """Enqueue the decode-cache append of one step (see include/bifattn.h):
-    k_new, v_new bf16 [b,g,n,d] go to rows decode_lens[i] .. + n - 1 of
-    Kd, Vd bf16 [b,g,m_d_max,d]; decode_lens int32 [b] advances by n."""
+    k_new, v_new [b,g,n,d] go to rows decode_lens[i] .. + n - 1 of
+    Kd, Vd [b,g,m_d_max,d] (the plan's cache type); decode_lens int32 [b]
+    advances by n."""
     import torch
     D = plan.dims
     dev = Kd.device
     n = max(1, D.n)
+    cd = _cache_dtypes(plan)
     args = [
-        _tensor(k_new, (D.b, D.g, n, D.d), torch.bfloat16, dev, "k_new"),
-        _tensor(v_new, (D.b, D.g, n, D.d), torch.bfloat16, dev, "v_new"),
-        _tensor(Kd, (D.b, D.g, D.m_d_max, D.d), torch.bfloat16, dev, "Kd"),
-        _tensor(Vd, (D.b, D.g, D.m_d_max, D.d), torch.bfloat16, dev, "Vd"),
+        _tensor(k_new, (D.b, D.g, n, D.d), cd, dev, "k_new"),
+        _tensor(v_new, (D.b, D.g, n, D.d), cd, dev, "v_new"),
+        _tensor(Kd, (D.b, D.g, D.m_d_max, D.d), cd, dev, "Kd"),
+        _tensor(Vd, (D.b, D.g, D.m_d_max, D.d), cd, dev, "Vd"),
         _tensor(decode_lens, (D.b,), torch.int32, dev, "decode_lens"),
     ]
     _check(lib().bifattn_append_kv(plan.handle, *args, _stream_ptr(stream)), "bifattn_append_kv")
 
 
 def bifattn_plan_status(plan: Plan, stream=None) -> int:
-    """Synchronise the stream; return OK or ELENS (and clear the flag)."""
+    """Synchronise the stream; return OK, ELENS or ESCALE (and clear the flags)."""
     st = lib().bifattn_plan_status(plan.handle, _stream_ptr(stream))
-    if st not in (OK, ELENS):
+    if st not in (OK, ELENS, ESCALE):
         raise BifattnError(st, "bifattn_plan_status")
     return st
 

@@ -145,6 +145,9 @@ bifattn_status_t check_dims(const bifattn_dims_t* d) {
     return BIFATTN_EINVAL;
   if (d->h % d->g) return BIFATTN_EINVAL;
   if (!(std::isfinite(d->scale))) return BIFATTN_EINVAL;
+  if (d->kv_type != BIFATTN_KV_BF16 && d->kv_type != BIFATTN_KV_FP8_E4M3 &&
+      d->kv_type != BIFATTN_KV_INT8)
+    return BIFATTN_EINVAL;
   if (d->d != 64 && d->d != 128) return BIFATTN_EUNSUPPORTED;
   const double ntok = d->n > 0 ? d->n : 1;
   if ((double)(d->h / d->g) * ntok > kMaxP) return BIFATTN_EUNSUPPORTED;
@@ -158,7 +161,8 @@ bifattn_status_t check_dims(const bifattn_dims_t* d) {
     return BIFATTN_EINVAL;
   // Kernels address one cache (a group's context, a sample's decode rows, or
   // both in the replicated ablation) with 32-bit byte offsets.
-  if (((double)d->m_c + d->m_d_max) * dd * 2 > INT32_MAX) return BIFATTN_EUNSUPPORTED;
+  if (((double)d->m_c + d->m_d_max) * dd * kv_bytes(d->kv_type) > INT32_MAX)
+    return BIFATTN_EUNSUPPORTED;
   return BIFATTN_OK;
 }
 
@@ -187,10 +191,12 @@ struct TimedSection {
   }
 };
 
-PartialsParams base_params(const bifattn_plan_s* P, const void* q, const int32_t* lens) {
+PartialsParams base_params(const bifattn_plan_s* P, const void* q, const int32_t* lens,
+                           const float* k_scale) {
   PartialsParams K{};
   K.q = static_cast<const uint16_t*>(q);
   K.lens = lens;
+  K.k_scale = k_scale;
   K.ctx_acc = P->ctx_acc;
   K.ctx_ml = P->ctx_ml;
   K.dec_acc = P->dec_acc;
@@ -211,8 +217,11 @@ PartialsParams base_params(const bifattn_plan_s* P, const void* q, const int32_t
   return K;
 }
 
-CombineParams combine_params(const bifattn_plan_s* P, const int32_t* lens, float* out) {
+CombineParams combine_params(const bifattn_plan_s* P, const int32_t* lens, const float* k_scale,
+                             const float* v_scale, float* out) {
   CombineParams C{};
+  C.k_scale = k_scale;
+  C.v_scale = v_scale;
   C.ctx_acc = P->ctx_acc;
   C.ctx_ml = P->ctx_ml;
   C.dec_acc = P->dec_acc;
@@ -237,11 +246,14 @@ const char* bifattn_status_string(bifattn_status_t s) {
   switch (s) {
     case BIFATTN_OK: return "ok";
     case BIFATTN_EINVAL: return "invalid argument";
-    case BIFATTN_EUNSUPPORTED: return "unsupported shape (d must be 64 or 128, h/g at most 64)";
+    case BIFATTN_EUNSUPPORTED:
+      return "unsupported shape (d must be 64 or 128, (h/g)*n at most 64, one sample's cache "
+             "rows under 2^31 bytes)";
     case BIFATTN_EALIGN: return "tensor pointer not 16-byte aligned (decode_lens: 4-byte)";
     case BIFATTN_ENOMEM: return "device memory allocation failed";
     case BIFATTN_EHIP: return "HIP runtime error";
     case BIFATTN_ELENS: return "a decode length was outside [0, m_d_max] and was clamped";
+    case BIFATTN_ESCALE: return "a key or value scale was not a positive normal float";
   }
   return "unknown status";
 }
@@ -328,21 +340,24 @@ bifattn_status_t bifattn_plan_get_info(bifattn_plan_t P, bifattn_plan_info_t* in
   return BIFATTN_OK;
 }
 
-bifattn_status_t bifattn_decode(bifattn_plan_t P, const void* q, const void* Kc, const void* Vc,
-                                const void* Kd, const void* Vd, const int32_t* decode_lens,
-                                float* out, hipStream_t stream) {
+bifattn_status_t bifattn_decode_scaled(bifattn_plan_t P, const void* q, const void* Kc,
+                                       const void* Vc, const void* Kd, const void* Vd,
+                                       const int32_t* decode_lens, const float* k_scale,
+                                       const float* v_scale, float* out, hipStream_t stream) {
   if (!P || !q || !Kc || !Vc || !out) return BIFATTN_EINVAL;
+  if (!aligned(k_scale, 4) || !aligned(v_scale, 4)) return BIFATTN_EALIGN;
   const bool has_dec = P->dims.m_d_max > 0;
   if (has_dec && (!Kd || !Vd || !decode_lens)) return BIFATTN_EINVAL;
   if (!aligned(q, 16) || !aligned(Kc, 16) || !aligned(Vc, 16) || !aligned(out, 16))
     return BIFATTN_EALIGN;
   if (has_dec && (!aligned(Kd, 16) || !aligned(Vd, 16) || !aligned(decode_lens, 4)))
     return BIFATTN_EALIGN;
-  PartialsParams K = base_params(P, q, has_dec ? decode_lens : nullptr);
-  K.Kc = static_cast<const uint16_t*>(Kc);
-  K.Vc = static_cast<const uint16_t*>(Vc);
-  K.Kd = static_cast<const uint16_t*>(Kd);
-  K.Vd = static_cast<const uint16_t*>(Vd);
+  const int kv = P->dims.kv_type;
+  PartialsParams K = base_params(P, q, has_dec ? decode_lens : nullptr, k_scale);
+  K.Kc = static_cast<const uint8_t*>(Kc);
+  K.Vc = static_cast<const uint8_t*>(Vc);
+  K.Kd = static_cast<const uint8_t*>(Kd);
+  K.Vd = static_cast<const uint8_t*>(Vd);
   K.dec_rows = P->dims.m_d_max;
   K.len_offset = 0;
   K.ctx_keys = P->ctx_keys;
@@ -359,25 +374,25 @@ bifattn_status_t bifattn_decode(bifattn_plan_t P, const void* q, const void* Kc,
   if (P->ctx_mode == kCtxLarge) {
     // The many-row context kernel, then the decode work-groups.
     K.n_ctx_blocks = P->n_ctx_blocks;
-    e = launch_ctx_large(K, P->dims.d, stream);
+    e = launch_ctx_large(K, P->dims.d, kv, stream);
     K.n_ctx_blocks = 0;
     K.n_dec_blocks = P->n_dec_blocks;
-    if (e == hipSuccess) e = launch_partials(K, P->dims.d, kCtxNone, P->dec_tiles, stream);
+    if (e == hipSuccess) e = launch_partials(K, P->dims.d, kv, kCtxNone, P->dec_tiles, stream);
   } else if (P->fused) {
     K.n_ctx_small_blocks = P->n_ctx_small_blocks;
     K.n_dec_blocks = P->n_dec_blocks;
-    e = launch_partials(K, P->dims.d, P->ctx_mode, P->dec_tiles, stream);
+    e = launch_partials(K, P->dims.d, kv, P->ctx_mode, P->dec_tiles, stream);
   } else {
     K.n_ctx_small_blocks = P->n_ctx_small_blocks;
-    e = launch_partials(K, P->dims.d, P->ctx_mode, P->dec_tiles, stream);
+    e = launch_partials(K, P->dims.d, kv, P->ctx_mode, P->dec_tiles, stream);
     K.n_ctx_small_blocks = 0;
     K.n_dec_blocks = P->n_dec_blocks;
-    if (e == hipSuccess) e = launch_partials(K, P->dims.d, kCtxNone, P->dec_tiles, stream);
+    if (e == hipSuccess) e = launch_partials(K, P->dims.d, kv, kCtxNone, P->dec_tiles, stream);
   }
   part.end();
   if (e != hipSuccess) return BIFATTN_EHIP;
   TimedSection comb(P, BIFATTN_KERNEL_COMBINE, stream);
-  CombineParams C = combine_params(P, has_dec ? decode_lens : nullptr, out);
+  CombineParams C = combine_params(P, has_dec ? decode_lens : nullptr, k_scale, v_scale, out);
   C.S_c = P->S_c;
   C.S_d = P->S_d * kWaves;
   e = launch_combine(C, P->dims.d, stream);
@@ -386,18 +401,26 @@ bifattn_status_t bifattn_decode(bifattn_plan_t P, const void* q, const void* Kc,
   return e == hipSuccess ? BIFATTN_OK : BIFATTN_EHIP;
 }
 
-bifattn_status_t bifattn_decode_replicated(bifattn_plan_t P, const void* q, const void* K_,
-                                           const void* V_, const int32_t* decode_lens, float* out,
-                                           hipStream_t stream) {
+bifattn_status_t bifattn_decode(bifattn_plan_t P, const void* q, const void* Kc, const void* Vc,
+                                const void* Kd, const void* Vd, const int32_t* decode_lens,
+                                float* out, hipStream_t stream) {
+  return bifattn_decode_scaled(P, q, Kc, Vc, Kd, Vd, decode_lens, nullptr, nullptr, out, stream);
+}
+
+bifattn_status_t bifattn_decode_replicated_scaled(bifattn_plan_t P, const void* q, const void* K_,
+                                                  const void* V_, const int32_t* decode_lens,
+                                                  const float* k_scale, const float* v_scale,
+                                                  float* out, hipStream_t stream) {
   if (!P || !q || !K_ || !V_ || !out) return BIFATTN_EINVAL;
+  if (!aligned(k_scale, 4) || !aligned(v_scale, 4)) return BIFATTN_EALIGN;
   const bool has_dec = P->dims.m_d_max > 0;
   if (has_dec && !decode_lens) return BIFATTN_EINVAL;
   if (!aligned(q, 16) || !aligned(K_, 16) || !aligned(V_, 16) || !aligned(out, 16))
     return BIFATTN_EALIGN;
   if (has_dec && !aligned(decode_lens, 4)) return BIFATTN_EALIGN;
-  PartialsParams K = base_params(P, q, has_dec ? decode_lens : nullptr);
-  K.Kd = static_cast<const uint16_t*>(K_);
-  K.Vd = static_cast<const uint16_t*>(V_);
+  PartialsParams K = base_params(P, q, has_dec ? decode_lens : nullptr, k_scale);
+  K.Kd = static_cast<const uint8_t*>(K_);
+  K.Vd = static_cast<const uint8_t*>(V_);
   K.dec_rows = P->dims.m_c + P->dims.m_d_max;
   K.len_offset = P->dims.m_c;
   K.dec_keys = P->rep_keys;
@@ -408,17 +431,24 @@ bifattn_status_t bifattn_decode_replicated(bifattn_plan_t P, const void* q, cons
   K.n_dec_blocks = P->n_rep_blocks;
   TimedSection whole(P, BIFATTN_KERNEL_CALL, stream);
   TimedSection part(P, BIFATTN_KERNEL_PARTIALS, stream);
-  hipError_t e = launch_partials(K, P->dims.d, kCtxNone, P->dec_tiles, stream);
+  hipError_t e = launch_partials(K, P->dims.d, P->dims.kv_type, kCtxNone, P->dec_tiles, stream);
   part.end();
   if (e != hipSuccess) return BIFATTN_EHIP;
   TimedSection comb(P, BIFATTN_KERNEL_COMBINE, stream);
-  CombineParams C = combine_params(P, has_dec ? decode_lens : nullptr, out);
+  CombineParams C = combine_params(P, has_dec ? decode_lens : nullptr, k_scale, v_scale, out);
   C.S_c = 0;
   C.S_d = P->S_r * kWaves;
   e = launch_combine(C, P->dims.d, stream);
   comb.end();
   whole.end();
   return e == hipSuccess ? BIFATTN_OK : BIFATTN_EHIP;
+}
+
+bifattn_status_t bifattn_decode_replicated(bifattn_plan_t P, const void* q, const void* K_,
+                                           const void* V_, const int32_t* decode_lens, float* out,
+                                           hipStream_t stream) {
+  return bifattn_decode_replicated_scaled(P, q, K_, V_, decode_lens, nullptr, nullptr, out,
+                                          stream);
 }
 
 bifattn_status_t bifattn_append_kv(bifattn_plan_t P, const void* k_new, const void* v_new,
@@ -429,17 +459,18 @@ bifattn_status_t bifattn_append_kv(bifattn_plan_t P, const void* k_new, const vo
       !aligned(decode_lens, 4))
     return BIFATTN_EALIGN;
   AppendParams A{};
-  A.k_new = static_cast<const uint16_t*>(k_new);
-  A.v_new = static_cast<const uint16_t*>(v_new);
-  A.Kd = static_cast<uint16_t*>(Kd);
-  A.Vd = static_cast<uint16_t*>(Vd);
+  A.k_new = static_cast<const uint8_t*>(k_new);
+  A.v_new = static_cast<const uint8_t*>(v_new);
+  A.Kd = static_cast<uint8_t*>(Kd);
+  A.Vd = static_cast<uint8_t*>(Vd);
   A.lens = decode_lens;
   A.status = P->status;
   A.b = P->dims.b;
   A.g = P->dims.g;
   A.n = P->ntok;
   A.m_d_max = P->dims.m_d_max;
-  return launch_append(A, P->dims.d, stream) == hipSuccess ? BIFATTN_OK : BIFATTN_EHIP;
+  return launch_append(A, P->dims.d, P->dims.kv_type, stream) == hipSuccess ? BIFATTN_OK
+                                                                              : BIFATTN_EHIP;
 }
 
 bifattn_status_t bifattn_plan_status(bifattn_plan_t P, hipStream_t stream) {
@@ -450,7 +481,7 @@ bifattn_status_t bifattn_plan_status(bifattn_plan_t P, hipStream_t stream) {
     return BIFATTN_EHIP;
   if (flag) {
     if (hipMemset(P->status, 0, sizeof flag) != hipSuccess) return BIFATTN_EHIP;
-    return BIFATTN_ELENS;
+    return (flag & kStatusScale) ? BIFATTN_ESCALE : BIFATTN_ELENS;
   }
   return BIFATTN_OK;
 }

@@ -29,17 +29,24 @@ constexpr float kRescaleSlack = 8.0f;
 
 // Device-side status bits.
 constexpr int kStatusLens = 1;
+constexpr int kStatusScale = 2;
+
+// Cache element types: bf16, or 8-bit codes (OCP fp8 E4M3, int8) with
+// per-group scales.
+enum KvType { kKvBf16 = 0, kKvFp8 = 1, kKvInt8 = 2 };
+constexpr int kv_bytes(int kv) { return kv == kKvBf16 ? 2 : 1; }
 
 // Partial result of one query row over one key range, relative to 2^m:
 // m  = reference maximum of scale*log2(e)*(q.k) over the range (or -inf),
 // l  = sum of 2^(logit - m), acc[d] = sum of 2^(logit - m) * v.
 struct PartialsParams {
   const uint16_t* q;
-  const uint16_t* Kc;
-  const uint16_t* Vc;
-  const uint16_t* Kd;     // decode cache (replicated cache in ablation mode)
-  const uint16_t* Vd;
+  const uint8_t* Kc;      // caches as bytes: bf16 or 8-bit codes
+  const uint8_t* Vc;
+  const uint8_t* Kd;      // decode cache (replicated cache in ablation mode)
+  const uint8_t* Vd;
   const int32_t* lens;
+  const float* k_scale;   // [g] key scales, or null for 1
   float* ctx_acc;         // [g][S_c][M][d]
   float2* ctx_ml;         // [g][S_c][M]
   float* dec_acc;         // [b][g][S_d][4 waves][p][d]
@@ -59,7 +66,7 @@ struct PartialsParams {
   int n_ctx_blocks;       // work-groups of the many-row context path
   int n_ctx_small_blocks; // work-groups of the few-row context path (g * S_c)
   int n_dec_blocks;       // decode work-groups (b * g * S_d); 4 partials each
-  float scale_log2;       // |scale| * log2(e)
+  float scale_log2;       // |scale| * log2(e); a unit of group gam multiplies in k_scale[gam]
   uint32_t q_sign;        // 0x80008000 when scale < 0 (q enters negated, exactly), else 0
 };
 
@@ -69,6 +76,8 @@ struct CombineParams {
   const float* dec_acc;
   const float2* dec_ml;
   const int32_t* lens;
+  const float* k_scale;   // [g] or null: checked here (positive, finite)
+  const float* v_scale;   // [g] or null: multiplies the output rows of group g
   float* out;
   int* status;
   int b, h, g, p, M;      // h, p count query rows (heads x tokens)
@@ -79,10 +88,10 @@ struct CombineParams {
 
 // Decode-cache append: the n new rows of every (sample, group).
 struct AppendParams {
-  const uint16_t* k_new;  // [b][g][n][d]
-  const uint16_t* v_new;
-  uint16_t* Kd;           // [b][g][m_d_max][d]
-  uint16_t* Vd;
+  const uint8_t* k_new;   // [b][g][n][d] elements of the cache type
+  const uint8_t* v_new;
+  uint8_t* Kd;            // [b][g][m_d_max][d]
+  uint8_t* Vd;
   int32_t* lens;          // [b], advanced by n (capped at m_d_max)
   int* status;
   int b, g, n, m_d_max;
@@ -92,12 +101,12 @@ enum CtxMode { kCtxNone = 0, kCtxSmall1 = 1, kCtxSmall2 = 2, kCtxSmall4 = 4, kCt
 
 // Launch the partial kernel over n_ctx_blocks + n_ctx_small_blocks +
 // n_dec_blocks work-groups.
-hipError_t launch_partials(const PartialsParams& P, int d, int ctx_mode, int dec_tiles,
+hipError_t launch_partials(const PartialsParams& P, int d, int kv, int ctx_mode, int dec_tiles,
                            hipStream_t stream);
 hipError_t launch_combine(const CombineParams& C, int d, hipStream_t stream);
 // Launch the decode-cache append (one work-group per sample).
-hipError_t launch_append(const AppendParams& A, int d, hipStream_t stream);
+hipError_t launch_append(const AppendParams& A, int d, int kv, hipStream_t stream);
 // Launch the many-row context kernel over n_ctx_blocks work-groups.
-hipError_t launch_ctx_large(const PartialsParams& P, int d, hipStream_t stream);
+hipError_t launch_ctx_large(const PartialsParams& P, int d, int kv, hipStream_t stream);
 
 }  // namespace bifattn

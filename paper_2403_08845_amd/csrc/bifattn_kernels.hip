@@ -23,6 +23,12 @@
 // per-lane 16-bit transpose; dimension block t of the output holds dims
 // DV*r + t (DV = d/16), so lane (n, G) ends up owning output dims
 // [4*DV*G, 4*DV*G + 4*DV) of query row n.
+//
+// Caches may hold 8-bit codes (OCP fp8 E4M3 or int8, one scale per KV group
+// for keys and one for values): every code value is exactly a bf16 value, so
+// codes are widened to bf16 on the way from memory to the operands and the
+// matrix products stay bf16. The key scale folds into the softmax scale of
+// the group's units and the value scale into the combine.
 #include <hip/hip_runtime.h>
 
 #include "bifattn_internal.h"
@@ -107,28 +113,110 @@ __device__ __forceinline__ int wave_id() {
   return __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
 }
 
-// Value row slice a lane loads: DV consecutive bf16 (16 B for d=128, 8 B for d=64).
-template <int D> struct VSlice;
-template <> struct VSlice<128> {
+// N bytes a lane loads with one buffer instruction, and 32-bit word w of them.
+template <int N> struct Raw;
+template <> struct Raw<16> {
   typedef u32x4 type;
-  static __device__ __forceinline__ type load(const uint16_t* p) {
-    return *reinterpret_cast<const u32x4*>(p);
-  }
-  static __device__ __forceinline__ type zero() { return u32x4{0, 0, 0, 0}; }
-  static __device__ __forceinline__ type load_buf(__amdgpu_buffer_rsrc_t r, int off) {
+  static __device__ __forceinline__ type load(__amdgpu_buffer_rsrc_t r, int off) {
     return __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0);
   }
+  static __device__ __forceinline__ type zero() { return u32x4{0, 0, 0, 0}; }
+  static __device__ __forceinline__ uint32_t word(const type& v, int w) { return v[w]; }
 };
-template <> struct VSlice<64> {
+template <> struct Raw<8> {
   typedef u32x2 type;
-  static __device__ __forceinline__ type load(const uint16_t* p) {
-    return *reinterpret_cast<const u32x2*>(p);
-  }
-  static __device__ __forceinline__ type zero() { return u32x2{0, 0}; }
-  static __device__ __forceinline__ type load_buf(__amdgpu_buffer_rsrc_t r, int off) {
+  static __device__ __forceinline__ type load(__amdgpu_buffer_rsrc_t r, int off) {
     return __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, 0);
   }
+  static __device__ __forceinline__ type zero() { return u32x2{0, 0}; }
+  static __device__ __forceinline__ uint32_t word(const type& v, int w) { return v[w]; }
 };
+template <> struct Raw<4> {
+  typedef uint32_t type;
+  static __device__ __forceinline__ type load(__amdgpu_buffer_rsrc_t r, int off) {
+    return __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, 0);
+  }
+  static __device__ __forceinline__ type zero() { return 0u; }
+  static __device__ __forceinline__ uint32_t word(const type& v, int) { return v; }
+};
+template <> struct Raw<2> {
+  typedef uint32_t type;
+  static __device__ __forceinline__ type load(__amdgpu_buffer_rsrc_t r, int off) {
+    return __builtin_amdgcn_raw_buffer_load_b16(r, off, 0, 0);
+  }
+  static __device__ __forceinline__ type zero() { return 0u; }
+  static __device__ __forceinline__ uint32_t word(const type& v, int) { return v; }
+};
+
+// Pack element t of two bf16 value rows (even key, odd key) into one word.
+__device__ __forceinline__ uint32_t pair_elem(uint32_t even_w, uint32_t odd_w, int t) {
+  return (t & 1) ? ((even_w >> 16) | (odd_w & 0xffff0000u))
+                 : ((even_w & 0xffffu) | (odd_w << 16));
+}
+
+// Cache element codecs. ES: bytes per element. For the 8-bit codes, lo(w) /
+// hi(w) widen codes 0-1 / 2-3 of a word to a bf16 pair (code 0 or 2 in the
+// low half) and pair(e, o, t) widens code t of word e and code t of word o.
+// Both conversions are exact: an fp8 E4M3 value has 4 significant bits and
+// an int8 value 8, and both lie inside bf16's exponent range.
+struct KvBf16 {
+  static constexpr int ES = 2;
+  static __device__ __forceinline__ uint32_t pair(uint32_t e, uint32_t o, int t) {
+    return pair_elem(e, o, t);
+  }
+};
+struct KvFp8 {
+  static constexpr int ES = 1;
+  static __device__ __forceinline__ uint32_t lo(uint32_t w) {
+    return __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(w, 1.f, false));
+  }
+  static __device__ __forceinline__ uint32_t hi(uint32_t w) {
+    return __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(w, 1.f, true));
+  }
+  static __device__ __forceinline__ uint32_t pair(uint32_t e, uint32_t o, int t) {
+    // v_perm_b32: selectors 0-3 take bytes of the second operand (e), 4-7 of
+    // the first (o), 12 gives zero.
+    return lo(__builtin_amdgcn_perm(o, e, 0x0C0C0000u | ((4u + t) << 8) | (uint32_t)t));
+  }
+};
+struct KvInt8 {
+  static constexpr int ES = 1;
+  static __device__ __forceinline__ float code(uint32_t w, int t) {
+    return (float)(signed char)(w >> (8 * t));
+  }
+  // Two integral floats of at most 8 significant bits: their upper halves
+  // are their bf16 values.
+  static __device__ __forceinline__ uint32_t two(float a, float b) {
+    return __builtin_amdgcn_perm(__float_as_uint(b), __float_as_uint(a), 0x07060302u);
+  }
+  static __device__ __forceinline__ uint32_t lo(uint32_t w) { return two(code(w, 0), code(w, 1)); }
+  static __device__ __forceinline__ uint32_t hi(uint32_t w) { return two(code(w, 2), code(w, 3)); }
+  static __device__ __forceinline__ uint32_t pair(uint32_t e, uint32_t o, int t) {
+    return two(code(e, t), code(o, t));
+  }
+};
+
+// 8 cache elements -> 8 bf16 (one MFMA operand): 16 raw bytes (bf16) as
+// they are, or 8 codes widened.
+template <typename KV> struct Widen8;
+template <> struct Widen8<KvBf16> {
+  static __device__ __forceinline__ u32x4 run(const u32x4& r) { return r; }
+};
+template <typename C> struct Widen8Codes {
+  static __device__ __forceinline__ u32x4 run(const u32x2& r) {
+    return u32x4{C::lo(r[0]), C::hi(r[0]), C::lo(r[1]), C::hi(r[1])};
+  }
+};
+template <> struct Widen8<KvFp8> : Widen8Codes<KvFp8> {};
+template <> struct Widen8<KvInt8> : Widen8Codes<KvInt8> {};
+
+// bf16 pair of element t of two value slices (even key, odd key).
+template <typename KV, typename S>
+__device__ __forceinline__ uint32_t value_pair(const S& e, const S& o, int t) {
+  constexpr int PER = 4 / KV::ES;  // elements per 32-bit word
+  typedef Raw<sizeof(S) < 4 ? 4 : (int)sizeof(S)> R;
+  return KV::pair(R::word(e, t / PER), R::word(o, t / PER), t % PER);
+}
 
 __device__ __forceinline__ u32x4 load16(const uint16_t* p) {
   return *reinterpret_cast<const u32x4*>(p);
@@ -139,16 +227,6 @@ __device__ __forceinline__ u32x4 load16(const uint16_t* p) {
 // (j = 0..3), i.e. keys 4e + G for e = 4a + j = 0..7: the same keys, in the
 // same order, as the V^T operand a lane builds from value rows 4e + G.
 __device__ __forceinline__ int qk_key(int a, int r) { return 16 * a + 4 * (r & 3) + (r >> 2); }
-
-// Element t of a value slice: 16-bit lane t of the slice's words.
-template <typename S>
-__device__ __forceinline__ uint32_t vword(const S& s, int t) { return s[t >> 1]; }
-
-// Pack element t of two value rows (even key, odd key) into one 32-bit word.
-__device__ __forceinline__ uint32_t pair_elem(uint32_t even_w, uint32_t odd_w, int t) {
-  return (t & 1) ? ((even_w >> 16) | (odd_w & 0xffff0000u))
-                 : ((even_w & 0xffffu) | (odd_w << 16));
-}
 
 // Per-wave running state of NT query tiles.
 template <int D, int NT> struct RowState {
@@ -314,45 +392,49 @@ __device__ __forceinline__ void load_q(u32x4 (&qop)[NT][D / 32], RowPtr row_ptr,
 }
 
 // Register path: one wave loads a whole 32-key tile, every load instruction
-// reading whole consecutive rows (1 KB contiguous for d = 128):
-//   K: lane l holds row RPI*e + l/CPR, 16-byte chunk l%CPR (CPR = d/8 chunks
-//      per row, RPI = 64/CPR rows per instruction); staged through a
-//      per-wave LDS tile to reach the MFMA operand layout, whose 16 lanes
-//      each want a different row (XOR-swizzled so those reads are
-//      bank-conflict free);
+// reading whole consecutive rows (1 KB contiguous for d = 128 bf16):
+//   K: lane l holds row RPI*e + l/CPR, 16-byte chunk l%CPR (CPR = d*ES/16
+//      chunks per row, RPI = 64/CPR rows per instruction); widened to bf16
+//      and staged through a per-wave LDS tile to reach the MFMA operand
+//      layout, whose 16 lanes each want a different row (XOR-swizzled so
+//      those reads are bank-conflict free);
 //   V: lane (c, G) holds row 4e + G, dims DV*c .. DV*c+DV-1 (e = 0..7), which
 //      is already what its V^T operands need: formed on demand by a 16-bit
-//      transpose inside the lane.
+//      transpose inside the lane (widening 8-bit codes on the way).
 // Loads go through buffer resources whose range ends at the item's last key,
 // so rows past it read as zero without a branch and without a memory access.
-template <int D> struct TileRegs {
+template <int D, typename KV> struct TileRegs {
+  static constexpr int ES = KV::ES;
   static constexpr int KS = D / 32;
   static constexpr int DV = D / 16;
-  static constexpr int CPR = D / 8;
+  static constexpr int RB = D * ES;       // bytes per cache row
+  static constexpr int CPR = RB / 16;     // raw 16-byte chunks per row
   static constexpr int RPI = 64 / CPR;
   static constexpr int KI = kTileKeys / RPI;
-  typedef typename VSlice<D>::type VS;
+  static constexpr int BPR = D / 8;       // bf16 16-byte chunks per row in LDS
+  typedef Raw<DV * ES> VR;
+  typedef typename VR::type VS;
   u32x4 kraw[KI];
   VS vrow[8];
 
-  // Swizzled 16-byte slot of (row, chunk) in a K tile staged in LDS.
+  // Swizzled 16-byte slot of (row, bf16 chunk) in a K tile staged in LDS.
   static __device__ __forceinline__ int kslot(int row, int chunk) {
     const int swz = D == 128 ? (row & 15) : ((row >> 1) & 7);
-    return row * CPR + (chunk ^ swz);
+    return row * BPR + (chunk ^ swz);
   }
 
   __device__ __forceinline__ void load(__amdgpu_buffer_rsrc_t rk, __amdgpu_buffer_rsrc_t rv,
                                        int key0, int lane) {
-    const int koff = ((key0 + lane / CPR) * D + (lane % CPR) * 8) * 2;
+    const int koff = (key0 + lane / CPR) * RB + (lane % CPR) * 16;
 #pragma unroll
     for (int e = 0; e < KI; ++e)
-      kraw[e] = __builtin_amdgcn_raw_buffer_load_b128(rk, koff + e * RPI * D * 2, 0, 0);
+      kraw[e] = __builtin_amdgcn_raw_buffer_load_b128(rk, koff + e * RPI * RB, 0, 0);
     const int c = lane & 15, G = lane >> 4;
-    const int voff = ((key0 + G) * D + DV * c) * 2;
+    const int voff = (key0 + G) * RB + DV * c * ES;
 #pragma unroll
-    for (int e = 0; e < 8; ++e) vrow[e] = VSlice<D>::load_buf(rv, voff + 4 * e * D * 2);
+    for (int e = 0; e < 8; ++e) vrow[e] = VR::load(rv, voff + 4 * e * RB);
   }
-  // Write the raw K rows into this wave's LDS tile (KI*64 16-byte slots).
+  // Write the K rows, as bf16, into this wave's LDS tile (32*d*2 bytes).
   // Lanes read each other's rows afterwards; a wave executes its LDS
   // instructions in order, and the wave barriers stop the compiler from
   // moving reads of the previous tile below these writes or reads of this
@@ -360,8 +442,17 @@ template <int D> struct TileRegs {
   __device__ __forceinline__ void stage_k(u32x4* kl, int lane) const {
     __builtin_amdgcn_wave_barrier();
 #pragma unroll
-    for (int e = 0; e < KI; ++e)
-      *(lds_u32x4*)(kl + kslot(RPI * e + lane / CPR, lane % CPR)) = kraw[e];
+    for (int e = 0; e < KI; ++e) {
+      const int row = RPI * e + lane / CPR, c = lane % CPR;
+      if constexpr (ES == 2) {
+        *(lds_u32x4*)(kl + kslot(row, c)) = kraw[e];
+      } else {
+        // 16 codes: bf16 chunks 2c and 2c + 1 of the row.
+        const u32x4& w = kraw[e];
+        *(lds_u32x4*)(kl + kslot(row, 2 * c)) = Widen8<KV>::run(u32x2{w[0], w[1]});
+        *(lds_u32x4*)(kl + kslot(row, 2 * c + 1)) = Widen8<KV>::run(u32x2{w[2], w[3]});
+      }
+    }
     __builtin_amdgcn_wave_barrier();
   }
   // K operand of sub-tile a, k-step s: row qk_key(a, n), dims 32s + 8G .. +7.
@@ -369,26 +460,28 @@ template <int D> struct TileRegs {
     return *(const lds_u32x4*)(kl + kslot(qk_key(a, lane & 15), 4 * s + (lane >> 4)));
   }
   // Zero the value rows of keys >= nvalid (rows past a sample's length may
-  // hold anything; their weight is 0 but 0 * NaN is not).
+  // hold anything; their weight is 0 but 0 * NaN is not). Zero bytes are the
+  // value 0 in every cache type.
   __device__ __forceinline__ void mask_v(int nvalid, int lane) {
     const int G = lane >> 4;
 #pragma unroll
     for (int e = 0; e < 8; ++e)
-      if (4 * e + G >= nvalid) vrow[e] = VSlice<D>::zero();
+      if (4 * e + G >= nvalid) vrow[e] = VR::zero();
   }
   // V^T operand of dimension block t: keys 4(2w) + G, 4(2w+1) + G in word w.
   __device__ __forceinline__ u32x4 vop(int t) const {
     u32x4 v;
 #pragma unroll
-    for (int w = 0; w < 4; ++w) v[w] = pair_elem(vword(vrow[2 * w], t), vword(vrow[2 * w + 1], t), t);
+    for (int w = 0; w < 4; ++w) v[w] = value_pair<KV>(vrow[2 * w], vrow[2 * w + 1], t);
     return v;
   }
 };
 
-// Buffer resource over `rows` rows of d bf16 starting at `base` (raw, stride 0).
-template <int D>
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t rows_rsrc(const uint16_t* base, int rows) {
-  return __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(base), (short)0, rows * D * 2,
+// Buffer resource over `rows` cache rows of `row_bytes` starting at `base`
+// (raw, stride 0).
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t rows_rsrc(const uint8_t* base, int rows,
+                                                             int row_bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t*>(base), (short)0, rows * row_bytes,
                                            0x00020000);
 }
 
@@ -427,7 +520,7 @@ __device__ __forceinline__ void store_partials(RowState<D, NT>& st, int nrows, f
 
 // One wave streams the 32-key tiles starting at keys k0, k0 + stride,
 // k0 + 2*stride, ... below k1 of one cache segment (buffer resources rk/rv
-// over rows of d bf16) through tile_update, double-buffered: the loads of the
+// over its rows) through tile_update, double-buffered: the loads of the
 // next tile are issued before the current one is consumed, so a tile is
 // always in flight. The caller has already issued the loads of the first tile
 // into A (before anything else, so that they overlap the set-up). The waves
@@ -436,10 +529,10 @@ __device__ __forceinline__ void store_partials(RowState<D, NT>& st, int nrows, f
 // lanes]; kl: this wave's LDS K tile (32*d*2 bytes). kend: the end of the
 // sequence the tokens' causal limits count from (ntok tokens per unit; k1
 // when ntok = 1).
-template <int D, int NT>
+template <int D, int NT, typename KV>
 __device__ __forceinline__ void stream_keys(RowState<D, NT>& st, const u32x4* qw, u32x4* kl,
                                             __amdgpu_buffer_rsrc_t rk, __amdgpu_buffer_rsrc_t rv,
-                                            TileRegs<D>& A, int k0, int k1, int kend, int stride,
+                                            TileRegs<D, KV>& A, int k0, int k1, int kend, int stride,
                                             int ntok, float scale_log2, int lane) {
   constexpr int KS = D / 32;
   if (k0 >= k1) return;
@@ -448,8 +541,8 @@ __device__ __forceinline__ void stream_keys(RowState<D, NT>& st, const u32x4* qw
   auto q_at = [&](int nt, int s) -> u32x4 {
     return *(volatile const lds_u32x4*)(qw + (nt * KS + s) * 64 + lane);
   };
-  auto k_at = [&](int a, int s) { return TileRegs<D>::kop(kl, a, s, lane); };
-  TileRegs<D> B;
+  auto k_at = [&](int a, int s) { return TileRegs<D, KV>::kop(kl, a, s, lane); };
+  TileRegs<D, KV> B;
   // Prefetches are unconditional: past the resource range the buffer load
   // returns zeros without a memory access, and a fixed count of loads in
   // flight lets each wait cover only the tile being consumed.
@@ -488,6 +581,12 @@ __device__ __forceinline__ void stage_q(u32x4* qw, RowPtr row_ptr, uint32_t sign
       *(volatile lds_u32x4*)(qw + (nt * KS + s) * 64 + lane) = qop[nt][s];
 }
 
+// Softmax scale of group gam's units in log2 units, the key scale folded in
+// (logit = scale * k_scale * q . code values).
+__device__ __forceinline__ float unit_scale_log2(const PartialsParams& P, int gam) {
+  return P.k_scale ? P.scale_log2 * P.k_scale[gam] : P.scale_log2;
+}
+
 __device__ __forceinline__ int clamp_len(const int32_t* lens, int i, int m_d_max) {
   const int raw = lens ? lens[i] : 0;
   return raw < 0 ? 0 : (raw > m_d_max ? m_d_max : raw);
@@ -500,19 +599,20 @@ __device__ __forceinline__ int clamp_len(const int32_t* lens, int i, int m_d_max
 // writes its own partial of the p query rows of group gam (partial slot
 // (chunk, wave)); a wave without keys writes the empty partial
 // (m = -inf, l = 0, acc = 0).
-template <int D, int NT>
+template <int D, int NT, typename KV>
 __device__ void decode_block(const PartialsParams& P, int blk, int wave, int lane, u32x4* qw,
                              u32x4* kl) {
+  constexpr int RB = D * KV::ES;
   const int s = blk % P.S_d;
   const int ig = blk / P.S_d;
   const int gam = ig % P.g, i = ig / P.g;
   const int kbeg = s * P.dec_keys;
   const int kcap = min(P.dec_rows, kbeg + P.dec_keys);  // the chunk within the cache capacity
-  const size_t cache = (size_t)(i * P.g + gam) * P.dec_rows * D;
-  const __amdgpu_buffer_rsrc_t rk = rows_rsrc<D>(P.Kd + cache, kcap);
-  const __amdgpu_buffer_rsrc_t rv = rows_rsrc<D>(P.Vd + cache, kcap);
+  const size_t cache = (size_t)(i * P.g + gam) * P.dec_rows * RB;
+  const __amdgpu_buffer_rsrc_t rk = rows_rsrc(P.Kd + cache, kcap, RB);
+  const __amdgpu_buffer_rsrc_t rv = rows_rsrc(P.Vd + cache, kcap, RB);
   const int k0 = kbeg + wave * kTileKeys;
-  TileRegs<D> A;
+  TileRegs<D, KV> A;
   A.load(rk, rv, k0, lane);  // first tile in flight before the length is known
   const int total = P.len_offset + clamp_len(P.lens, i, P.m_d_max);
   const int k1 = min(total, kcap);
@@ -524,8 +624,8 @@ __device__ void decode_block(const PartialsParams& P, int blk, int wave, int lan
   st.init();
   // Keys [k0, k1) of this chunk; the causal limits of the tokens count from
   // the end of the sequence (total), which may lie in a later chunk.
-  stream_keys<D, NT>(st, qw, kl, rk, rv, A, k0, k1, total, kWaves * kTileKeys, P.ntok,
-                     P.scale_log2, lane);
+  stream_keys<D, NT, KV>(st, qw, kl, rk, rv, A, k0, k1, total, kWaves * kTileKeys, P.ntok,
+                         unit_scale_log2(P, gam), lane);
   const size_t prow = ((size_t)blk * kWaves + wave) * P.p;
   store_partials<D, NT>(st, p, P.dec_acc + prow * D, P.dec_ml + prow, lane);
 }
@@ -593,15 +693,16 @@ template <int D, int NT> struct MergeLds {
 // 4s+w+4*S_c, ...), so they sweep K_c/V_c together and each tile is read
 // once, straight into the operands that serve all M query rows. The four
 // waves' states merge in LDS into the split's partial.
-template <int D, int NT>
+template <int D, int NT, typename KV>
 __device__ void ctx_small_block(const PartialsParams& P, int blk, int wave, int lane, u32x4* qw,
                                 u32x4* kl, float* merge_lds) {
+  constexpr int RB = D * KV::ES;
   const int s = blk % P.S_c, gam = blk / P.S_c;
-  const size_t cache = (size_t)gam * P.m_c * D;
-  const __amdgpu_buffer_rsrc_t rk = rows_rsrc<D>(P.Kc + cache, P.m_c);
-  const __amdgpu_buffer_rsrc_t rv = rows_rsrc<D>(P.Vc + cache, P.m_c);
+  const size_t cache = (size_t)gam * P.m_c * RB;
+  const __amdgpu_buffer_rsrc_t rk = rows_rsrc(P.Kc + cache, P.m_c, RB);
+  const __amdgpu_buffer_rsrc_t rv = rows_rsrc(P.Vc + cache, P.m_c, RB);
   const int k0 = (s * kWaves + wave) * kTileKeys;
-  TileRegs<D> A;
+  TileRegs<D, KV> A;
   A.load(rk, rv, k0, lane);  // first tile in flight while Q is staged
   const int M = P.M, p = P.p, h = P.h;
   const uint16_t* q = P.q;
@@ -612,8 +713,8 @@ __device__ void ctx_small_block(const PartialsParams& P, int blk, int wave, int 
   }, P.q_sign, lane);
   RowState<D, NT> st;
   st.init();
-  stream_keys<D, NT>(st, qw, kl, rk, rv, A, k0, P.m_c, P.m_c, P.S_c * kWaves * kTileKeys, 1,
-                     P.scale_log2, lane);
+  stream_keys<D, NT, KV>(st, qw, kl, rk, rv, A, k0, P.m_c, P.m_c, P.S_c * kWaves * kTileKeys, 1,
+                         unit_scale_log2(P, gam), lane);
   const size_t prow = (size_t)blk * P.M;
   __syncthreads();  // the merge buffer overlays the waves' K tiles
   merge_waves_and_store<D, NT>(st, merge_lds, M, P.ctx_acc + prow * D, P.ctx_ml + prow, wave, lane);
@@ -629,24 +730,6 @@ __device__ __forceinline__ int xcd_logical(int bid, int n) {
   return (bid % X) * per + bid / X;
 }
 
-// Value-slice half: the HW = d/32 dimensions DV*r + vh*HW .. + HW of a value
-// row that one wave of the many-row context kernel stages per lane.
-template <int D> struct VHalf;
-template <> struct VHalf<128> {
-  typedef u32x2 type;
-  static __device__ __forceinline__ type load(__amdgpu_buffer_rsrc_t r, int off) {
-    return __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, 0);
-  }
-  static __device__ __forceinline__ uint32_t word(const type& v, int t) { return v[t >> 1]; }
-};
-template <> struct VHalf<64> {
-  typedef uint32_t type;
-  static __device__ __forceinline__ type load(__amdgpu_buffer_rsrc_t r, int off) {
-    return __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, 0);
-  }
-  static __device__ __forceinline__ uint32_t word(const type& v, int) { return v; }
-};
-
 // Context part, many query rows per group: work-group (group gam, key split
 // s, row block rb) of 128 query rows, eight waves with one 16-row query
 // tile each, two work-groups per CU (four waves per SIMD, so one wave's
@@ -655,18 +738,22 @@ template <> struct VHalf<64> {
 // already in MFMA operand order (the V^T transpose is done once, on the way
 // in), and all eight waves read it. Each wave stages one eighth of a tile:
 // one K operand (d = 128; the first four waves for d = 64) and one 32-bit
-// word of half of the V^T operands. Tiles are double-buffered in LDS with
+// word of half of the V^T operands, widening 8-bit codes to bf16 on the way. Tiles are double-buffered in LDS with
 // one barrier per tile, and fetched two tiles ahead into two rotating
 // register sets. Q^T operands stay in registers. Row blocks of one key
 // chunk are scheduled on the same XCD so that they share its L2.
-template <int D>
+template <int D, typename KV>
 __device__ __forceinline__ void ctx_large_body(const PartialsParams& P) {
   constexpr int KS = D / 32;
   constexpr int DV = D / 16;
-  constexpr int KOPS = 2 * KS;  // K operands per tile
+  constexpr int ES = KV::ES;
+  constexpr int RB = D * ES;      // bytes per cache row
+  constexpr int KOPS = 2 * KS;    // K operands per tile
   constexpr int OPS = KOPS + DV;  // operands per tile (16 B per lane each)
   constexpr int HW = DV / 2;      // V^T operands one wave stages a word of
-  typedef typename VHalf<D>::type VH;
+  typedef Raw<8 * ES> KR;         // a lane's 8 elements of its K operand
+  typedef Raw<HW * ES> VR;        // a lane's HW elements of a value row
+  typedef typename VR::type VH;
   __shared__ __attribute__((aligned(16))) u32x4 lds[2 * OPS * 64];
   const int blk = xcd_logical(blockIdx.x, P.n_ctx_blocks);
   const int rb = blk % P.ctx_row_blocks;
@@ -678,9 +765,10 @@ __device__ __forceinline__ void ctx_large_body(const PartialsParams& P) {
   const int r = lane & 15, G = lane >> 4;
   // Buffer resources over the chunk's keys [k0, k0 + nkeys): rows past it
   // load as zero with no memory access and no branch. Offsets count from k0.
-  const size_t chunk = ((size_t)gam * P.m_c + k0) * D;
-  const __amdgpu_buffer_rsrc_t rk = rows_rsrc<D>(P.Kc + chunk, nkeys);
-  const __amdgpu_buffer_rsrc_t rv = rows_rsrc<D>(P.Vc + chunk, nkeys);
+  const size_t chunk = ((size_t)gam * P.m_c + k0) * RB;
+  const __amdgpu_buffer_rsrc_t rk = rows_rsrc(P.Kc + chunk, nkeys, RB);
+  const __amdgpu_buffer_rsrc_t rv = rows_rsrc(P.Vc + chunk, nkeys, RB);
+  const float scale_log2 = unit_scale_log2(P, gam);
   const int M = P.M, p = P.p, h = P.h;
   const int row0 = rb * kLargeRowsPerBlock + wave * kRowsPerTile;
   auto slot = [&](int buf, int op) -> u32x4* { return lds + (buf * OPS + op) * 64; };
@@ -690,24 +778,22 @@ __device__ __forceinline__ void ctx_large_body(const PartialsParams& P) {
 
   // Registers of a tile in flight: this wave's K operand and two value-row halves.
   struct Stage {
-    u32x4 k;
+    typename KR::type k;
     VH v[2];
   };
   auto fetch = [&](Stage& g, int key0) {  // keys past the chunk load as zero
-    if (has_k)
-      g.k = __builtin_amdgcn_raw_buffer_load_b128(
-          rk, ((key0 + qk_key(ka, r)) * D + kss * 32 + G * 8) * 2, 0, 0);
+    if (has_k) g.k = KR::load(rk, (key0 + qk_key(ka, r)) * RB + (kss * 32 + G * 8) * ES);
 #pragma unroll
     for (int c = 0; c < 2; ++c)
-      g.v[c] = VHalf<D>::load(rv, ((key0 + 4 * (2 * vw + c) + G) * D + DV * r + vh * HW) * 2);
+      g.v[c] = VR::load(rv, (key0 + 4 * (2 * vw + c) + G) * RB + (DV * r + vh * HW) * ES);
   };
   auto stage = [&](const Stage& g, int buf) {
-    if (has_k) slot(buf, wave)[lane] = g.k;
+    if (has_k) slot(buf, wave)[lane] = Widen8<KV>::run(g.k);
     // word vw of V^T operand vh*HW + t = keys 4(2vw) + G, 4(2vw+1) + G at dim DV*r + vh*HW + t
 #pragma unroll
     for (int t = 0; t < HW; ++t)
       reinterpret_cast<uint32_t*>(slot(buf, KOPS + vh * HW + t) + lane)[vw] =
-          pair_elem(VHalf<D>::word(g.v[0], t), VHalf<D>::word(g.v[1], t), t);
+          value_pair<KV>(g.v[0], g.v[1], t);
   };
 
   // Q first, then the first two tiles: the wait for the first tile then also
@@ -738,7 +824,7 @@ __device__ __forceinline__ void ctx_large_body(const PartialsParams& P) {
     if (rows)
       tile_update<D, 1>(st, [&](int a, int ss) { return slot(buf, a * KS + ss)[lane]; },
                         [&](int t) { return slot(buf, KOPS + t)[lane]; },
-                        [&](int, int ss) { return qop[0][ss]; }, nkeys - key, 1, P.scale_log2,
+                        [&](int, int ss) { return qop[0][ss]; }, nkeys - key, 1, scale_log2,
                         lane);
     if (stage_next) {
       // The other buffer was last read in the previous step, before the
@@ -772,10 +858,10 @@ __device__ __forceinline__ void ctx_large_body(const PartialsParams& P) {
   }
 }
 
-template <int D>
+template <int D, typename KV>
 __global__ __launch_bounds__(kLargeThreads) __attribute__((amdgpu_waves_per_eu(4))) void
 ctx_large_kernel(PartialsParams P) {
-  ctx_large_body<D>(P);
+  ctx_large_body<D, KV>(P);
 }
 
 constexpr int cmax(int a, int b) { return a > b ? a : b; }
@@ -784,7 +870,7 @@ constexpr int cmax(int a, int b) { return a > b ? a : b; }
 // Grid: n_ctx_small_blocks work-groups of the few-row context path, then
 // n_dec_blocks decode work-groups (the many-row context path has a kernel of
 // its own).
-template <int D, int CTX, int NTD>
+template <int D, typename KV, int CTX, int NTD>
 __device__ __forceinline__ void partials_body(const PartialsParams& P) {
   constexpr bool kSmall = CTX != kCtxNone;
   constexpr int NTC = kSmall ? CTX : 1;
@@ -801,23 +887,24 @@ __device__ __forceinline__ void partials_body(const PartialsParams& P) {
   const int blk = bid;
   if (blk < P.n_ctx_small_blocks) {
     if constexpr (kSmall)
-      ctx_small_block<D, NTC>(P, blk, wave, lane, qw, kl, reinterpret_cast<float*>(lds + QSLOTS));
+      ctx_small_block<D, NTC, KV>(P, blk, wave, lane, qw, kl,
+                                  reinterpret_cast<float*>(lds + QSLOTS));
   } else if (blk - P.n_ctx_small_blocks < P.n_dec_blocks) {
-    decode_block<D, NTD>(P, blk - P.n_ctx_small_blocks, wave, lane, qw, kl);
+    decode_block<D, NTD, KV>(P, blk - P.n_ctx_small_blocks, wave, lane, qw, kl);
   }
 }
 
 // Variants whose waves hold at most two query tiles fit two waves
 // per SIMD (<= 256 registers) and are compiled for that occupancy; the others
 // keep the compiler's choice.
-template <int D, int CTX, int NTD>
+template <int D, typename KV, int CTX, int NTD>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) void
 partials_kernel_2w(PartialsParams P) {
-  partials_body<D, CTX, NTD>(P);
+  partials_body<D, KV, CTX, NTD>(P);
 }
-template <int D, int CTX, int NTD>
+template <int D, typename KV, int CTX, int NTD>
 __global__ __launch_bounds__(kThreads) void partials_kernel(PartialsParams P) {
-  partials_body<D, CTX, NTD>(P);
+  partials_body<D, KV, CTX, NTD>(P);
 }
 template <int D, int CTX, int NTD>
 constexpr bool fits_two_waves() {
@@ -830,7 +917,9 @@ constexpr bool fits_two_waves() {
 // out = sum_k 2^(m_k - M) acc_k / sum_k 2^(m_k - M) l_k, M = max_k m_k.
 // Lane k first fetches the statistics of partial k (all in parallel), so the
 // weights need one wave reduction; the value rows are then summed in a fixed
-// order with their loads issued ahead in batches.
+// order with their loads issued ahead in batches. The group's value scale
+// multiplies the result (every partial of the row shares it); the first row
+// of each group checks that the group's scales are positive normal floats.
 template <int D>
 __global__ __launch_bounds__(256) void combine_kernel(CombineParams C) {
   constexpr int PER = D / 64;
@@ -843,6 +932,13 @@ __global__ __launch_bounds__(256) void combine_kernel(CombineParams C) {
   if (j == 0 && lane == 0 && C.lens) {
     const int raw = C.lens[i];
     if (raw < 0 || raw > C.m_d_max) atomicOr(C.status, kStatusLens);
+  }
+  const float vs = C.v_scale ? C.v_scale[gam] : 1.f;
+  if (i == 0 && jp == 0 && lane == 0) {
+    const float ks = C.k_scale ? C.k_scale[gam] : 1.f;
+    // false for NaN as well
+    const bool ok = ks >= __FLT_MIN__ && ks <= __FLT_MAX__ && vs >= __FLT_MIN__ && vs <= __FLT_MAX__;
+    if (!ok) atomicOr(C.status, kStatusScale);
   }
   const int np = C.S_c + C.S_d;  // every decode wave wrote a partial (maybe empty)
   const size_t cbase = (size_t)gam * C.S_c * C.M + (size_t)i * C.p + jp;  // + k*M
@@ -905,44 +1001,66 @@ __global__ __launch_bounds__(256) void combine_kernel(CombineParams C) {
     }
   }
   float* o = C.out + (size_t)row * D + lane * PER;
-  const float inv = 1.f / L;
+  const float inv = vs / L;
 #pragma unroll
   for (int e = 0; e < PER; ++e) o[e] = acc[e] * inv;
 }
 
-template <int D, int CTX>
+template <int D, typename KV, int CTX>
 hipError_t launch_partials_ctx(const PartialsParams& P, int dec_tiles, hipStream_t stream) {
   const int grid = P.n_ctx_small_blocks + P.n_dec_blocks;
   if (grid == 0) return hipSuccess;
   switch (dec_tiles) {
     case 1:
       if constexpr (fits_two_waves<D, CTX, 1>())
-        partials_kernel_2w<D, CTX, 1><<<grid, kThreads, 0, stream>>>(P);
+        partials_kernel_2w<D, KV, CTX, 1><<<grid, kThreads, 0, stream>>>(P);
       else
-        partials_kernel<D, CTX, 1><<<grid, kThreads, 0, stream>>>(P);
+        partials_kernel<D, KV, CTX, 1><<<grid, kThreads, 0, stream>>>(P);
       break;
     case 2:
       if constexpr (fits_two_waves<D, CTX, 2>())
-        partials_kernel_2w<D, CTX, 2><<<grid, kThreads, 0, stream>>>(P);
+        partials_kernel_2w<D, KV, CTX, 2><<<grid, kThreads, 0, stream>>>(P);
       else
-        partials_kernel<D, CTX, 2><<<grid, kThreads, 0, stream>>>(P);
+        partials_kernel<D, KV, CTX, 2><<<grid, kThreads, 0, stream>>>(P);
       break;
-    case 4: partials_kernel<D, CTX, 4><<<grid, kThreads, 0, stream>>>(P); break;
+    case 4: partials_kernel<D, KV, CTX, 4><<<grid, kThreads, 0, stream>>>(P); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
 }
 
-template <int D>
-hipError_t launch_partials_d(const PartialsParams& P, int ctx_mode, int dec_tiles,
-                             hipStream_t stream) {
+template <int D, typename KV>
+hipError_t launch_partials_dk(const PartialsParams& P, int ctx_mode, int dec_tiles,
+                              hipStream_t stream) {
   switch (ctx_mode) {
-    case kCtxNone: return launch_partials_ctx<D, kCtxNone>(P, dec_tiles, stream);
-    case kCtxSmall1: return launch_partials_ctx<D, kCtxSmall1>(P, dec_tiles, stream);
-    case kCtxSmall2: return launch_partials_ctx<D, kCtxSmall2>(P, dec_tiles, stream);
-    case kCtxSmall4: return launch_partials_ctx<D, kCtxSmall4>(P, dec_tiles, stream);
+    case kCtxNone: return launch_partials_ctx<D, KV, kCtxNone>(P, dec_tiles, stream);
+    case kCtxSmall1: return launch_partials_ctx<D, KV, kCtxSmall1>(P, dec_tiles, stream);
+    case kCtxSmall2: return launch_partials_ctx<D, KV, kCtxSmall2>(P, dec_tiles, stream);
+    case kCtxSmall4: return launch_partials_ctx<D, KV, kCtxSmall4>(P, dec_tiles, stream);
     default: return hipErrorInvalidValue;
   }
+}
+
+template <int D>
+hipError_t launch_partials_d(const PartialsParams& P, int kv, int ctx_mode, int dec_tiles,
+                             hipStream_t stream) {
+  switch (kv) {
+    case kKvBf16: return launch_partials_dk<D, KvBf16>(P, ctx_mode, dec_tiles, stream);
+    case kKvFp8: return launch_partials_dk<D, KvFp8>(P, ctx_mode, dec_tiles, stream);
+    case kKvInt8: return launch_partials_dk<D, KvInt8>(P, ctx_mode, dec_tiles, stream);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+template <int D>
+hipError_t launch_ctx_large_d(const PartialsParams& P, int kv, hipStream_t stream) {
+  switch (kv) {
+    case kKvBf16: ctx_large_kernel<D, KvBf16><<<P.n_ctx_blocks, kLargeThreads, 0, stream>>>(P); break;
+    case kKvFp8: ctx_large_kernel<D, KvFp8><<<P.n_ctx_blocks, kLargeThreads, 0, stream>>>(P); break;
+    case kKvInt8: ctx_large_kernel<D, KvInt8><<<P.n_ctx_blocks, kLargeThreads, 0, stream>>>(P); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
 }
 
 // Decode-cache append (the decode cache holds the keys and values of the
@@ -950,10 +1068,11 @@ hipError_t launch_partials_d(const PartialsParams& P, int ctx_mode, int dec_tile
 // rows of every group to rows len_i .. len_i + n - 1 of its decode cache and
 // then advances len_i by n. One work-group per sample, so every thread reads
 // len_i before thread 0 rewrites it. Rows past the capacity are dropped; a
-// length outside [0, m_d_max] is clamped; both raise the status flag.
-template <int D>
+// length outside [0, m_d_max] is clamped; both raise the status flag. RB:
+// bytes per row (elements of the cache type, copied as they are).
+template <int RB>
 __global__ __launch_bounds__(256) void append_kernel(AppendParams A) {
-  constexpr int CH = D / 8;  // 16-byte chunks per row
+  constexpr int CH = RB / 16;  // 16-byte chunks per row
   const int i = blockIdx.x;
   const int raw = A.lens[i];
   const int len = raw < 0 ? 0 : (raw > A.m_d_max ? A.m_d_max : raw);
@@ -964,8 +1083,8 @@ __global__ __launch_bounds__(256) void append_kernel(AppendParams A) {
     const int r = (idx / CH) % room;
     const int gam = idx / CH / room;
     const size_t unit = (size_t)i * A.g + gam;
-    const size_t src = (unit * A.n + r) * D + c * 8;
-    const size_t dst = (unit * A.m_d_max + len + r) * D + c * 8;
+    const size_t src = (unit * A.n + r) * RB + c * 16;
+    const size_t dst = (unit * A.m_d_max + len + r) * RB + c * 16;
     *reinterpret_cast<u32x4*>(A.Kd + dst) = *reinterpret_cast<const u32x4*>(A.k_new + src);
     *reinterpret_cast<u32x4*>(A.Vd + dst) = *reinterpret_cast<const u32x4*>(A.v_new + src);
   }
@@ -978,29 +1097,25 @@ __global__ __launch_bounds__(256) void append_kernel(AppendParams A) {
 
 }  // namespace
 
-hipError_t launch_append(const AppendParams& A, int d, hipStream_t stream) {
-  if (d == 128)
-    append_kernel<128><<<A.b, 256, 0, stream>>>(A);
-  else if (d == 64)
-    append_kernel<64><<<A.b, 256, 0, stream>>>(A);
-  else
-    return hipErrorInvalidValue;
+hipError_t launch_append(const AppendParams& A, int d, int kv, hipStream_t stream) {
+  switch (d * kv_bytes(kv)) {
+    case 256: append_kernel<256><<<A.b, 256, 0, stream>>>(A); break;
+    case 128: append_kernel<128><<<A.b, 256, 0, stream>>>(A); break;
+    case 64: append_kernel<64><<<A.b, 256, 0, stream>>>(A); break;
+    default: return hipErrorInvalidValue;
+  }
   return hipGetLastError();
 }
-hipError_t launch_ctx_large(const PartialsParams& P, int d, hipStream_t stream) {
+hipError_t launch_ctx_large(const PartialsParams& P, int d, int kv, hipStream_t stream) {
   if (P.n_ctx_blocks == 0) return hipSuccess;
-  if (d == 128)
-    ctx_large_kernel<128><<<P.n_ctx_blocks, kLargeThreads, 0, stream>>>(P);
-  else if (d == 64)
-    ctx_large_kernel<64><<<P.n_ctx_blocks, kLargeThreads, 0, stream>>>(P);
-  else
-    return hipErrorInvalidValue;
-  return hipGetLastError();
+  if (d == 128) return launch_ctx_large_d<128>(P, kv, stream);
+  if (d == 64) return launch_ctx_large_d<64>(P, kv, stream);
+  return hipErrorInvalidValue;
 }
-hipError_t launch_partials(const PartialsParams& P, int d, int ctx_mode, int dec_tiles,
+hipError_t launch_partials(const PartialsParams& P, int d, int kv, int ctx_mode, int dec_tiles,
                            hipStream_t stream) {
-  if (d == 128) return launch_partials_d<128>(P, ctx_mode, dec_tiles, stream);
-  if (d == 64) return launch_partials_d<64>(P, ctx_mode, dec_tiles, stream);
+  if (d == 128) return launch_partials_d<128>(P, kv, ctx_mode, dec_tiles, stream);
+  if (d == 64) return launch_partials_d<64>(P, kv, ctx_mode, dec_tiles, stream);
   return hipErrorInvalidValue;
 }
 

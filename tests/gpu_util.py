@@ -4,13 +4,28 @@ import numpy as np
 import paper_2403_08845_amd as bif
 
 
+def kv_of(x):
+    return x.get("kv", "bf16")
+
+
+def cache_to_device(a, kv):
+    """bf16 bit patterns -> torch bf16, 8-bit codes -> torch uint8, on the GPU."""
+    import torch
+    if kv == "bf16":
+        return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).cuda()
+    return torch.from_numpy(np.ascontiguousarray(a).view(np.uint8)).cuda()
+
+
 def to_device(x):
     import torch
-    out = {}
-    for k in ("q", "Kc", "Vc", "Kd", "Vd"):
-        a = np.ascontiguousarray(x[k]).view(np.int16)
-        out[k] = torch.from_numpy(a).view(torch.bfloat16).cuda()
+    kv = kv_of(x)
+    out = {"q": cache_to_device(x["q"], "bf16")}
+    for k in ("Kc", "Vc", "Kd", "Vd"):
+        out[k] = cache_to_device(x[k], kv)
     out["lens"] = torch.from_numpy(np.ascontiguousarray(x["lens"], dtype=np.int32)).cuda()
+    for k in ("k_scale", "v_scale"):
+        out[k] = (None if x.get(k) is None else
+                  torch.from_numpy(np.ascontiguousarray(x[k], dtype=np.float32)).cuda())
     return out
 
 
@@ -33,12 +48,16 @@ def run_decode(x, scale=0.0, plan=None, dev=None, check_status=True):
     b, h, g, d, m_c, m_d_max = dims_of(x)
     own = plan is None
     if own:
-        plan = bif.Plan(b, h, g, d, m_c, m_d_max, scale, n=tokens_of(x))
+        plan = bif.Plan(b, h, g, d, m_c, m_d_max, scale, n=tokens_of(x), kv=kv_of(x))
     try:
         dev = dev or to_device(x)
         out = torch.full(tuple(x["q"].shape), float("nan"), dtype=torch.float32, device="cuda")
-        bif.bifattn_decode(plan, dev["q"], dev["Kc"], dev["Vc"], dev["Kd"], dev["Vd"],
-                           dev["lens"], out)
+        if dev.get("k_scale") is None and dev.get("v_scale") is None:
+            bif.bifattn_decode(plan, dev["q"], dev["Kc"], dev["Vc"], dev["Kd"], dev["Vd"],
+                               dev["lens"], out)
+        else:
+            bif.bifattn_decode_scaled(plan, dev["q"], dev["Kc"], dev["Vc"], dev["Kd"], dev["Vd"],
+                                      dev["lens"], dev["k_scale"], dev["v_scale"], out)
         st = bif.bifattn_plan_status(plan)
         if check_status:
             assert st == bif.OK, bif.status_string(st)
@@ -60,12 +79,13 @@ def run_replicated(x, scale=0.0):
     import torch
     b, h, g, d, m_c, m_d_max = dims_of(x)
     K, V = replicate(x)
-    with bif.Plan(b, h, g, d, m_c, m_d_max, scale, n=tokens_of(x)) as plan:
+    kv = kv_of(x)
+    with bif.Plan(b, h, g, d, m_c, m_d_max, scale, n=tokens_of(x), kv=kv) as plan:
         dev = to_device(x)
-        Kt = torch.from_numpy(K.view(np.int16)).view(torch.bfloat16).cuda()
-        Vt = torch.from_numpy(V.view(np.int16)).view(torch.bfloat16).cuda()
+        Kt, Vt = cache_to_device(K, kv), cache_to_device(V, kv)
         out = torch.full(tuple(x["q"].shape), float("nan"), dtype=torch.float32, device="cuda")
-        bif.bifattn_decode_replicated(plan, dev["q"], Kt, Vt, dev["lens"], out)
+        bif.bifattn_decode_replicated_scaled(plan, dev["q"], Kt, Vt, dev["lens"], dev["k_scale"],
+                                             dev["v_scale"], out)
         assert bif.bifattn_plan_status(plan) == bif.OK
         return out.cpu().double().numpy()
 

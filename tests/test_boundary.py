@@ -35,8 +35,9 @@ def test_every_declared_symbol_is_exported(L):
 
 
 def test_version_and_status_strings(L):
-    assert bif.bifattn_version() == 2
-    for code in (bif.OK, bif.EINVAL, bif.EUNSUPPORTED, bif.EALIGN, bif.ENOMEM, bif.EHIP, bif.ELENS):
+    assert bif.bifattn_version() == 3
+    for code in (bif.OK, bif.EINVAL, bif.EUNSUPPORTED, bif.EALIGN, bif.ENOMEM, bif.EHIP, bif.ELENS,
+                 bif.ESCALE):
         assert bif.status_string(code)
     assert bif.status_string(12345) == "unknown status"
 
@@ -61,6 +62,10 @@ def _create(L, *dims):
     ((1, 32, 32, 128, 2**23 - 64, 64, 0.0), bif.EUNSUPPORTED),  # context + decode rows
     ((2, 4, 2, 64, 128, 16, 0.0, -1), bif.EINVAL),          # negative token count
     ((2, 32, 1, 64, 128, 16, 0.0, 3), bif.EUNSUPPORTED),    # p * n = 96 query rows per unit
+    ((2, 4, 2, 64, 128, 16, 0.0, 1, 3), bif.EINVAL),        # unknown cache type
+    ((2, 4, 2, 64, 128, 16, 0.0, 1, -1), bif.EINVAL),
+    ((1, 32, 32, 128, 2**24, 0, 0.0, 1, 1), bif.EUNSUPPORTED),  # fp8 cache past 2^31 bytes
+    ((1, 32, 32, 128, 2**24 - 64, 64, 0.0, 1, 2), bif.EUNSUPPORTED),  # int8, both parts
 ])
 def test_plan_create_rejects_bad_dims_without_a_device(L, dims, expect):
     st, handle = _create(L, *dims)
@@ -74,6 +79,8 @@ def test_null_arguments(L):
     assert L.bifattn_plan_get_info(None, None) == bif.EINVAL
     assert L.bifattn_decode(None, *([None] * 8)) == bif.EINVAL
     assert L.bifattn_decode_replicated(None, *([None] * 6)) == bif.EINVAL
+    assert L.bifattn_decode_scaled(None, *([None] * 10)) == bif.EINVAL
+    assert L.bifattn_decode_replicated_scaled(None, *([None] * 8)) == bif.EINVAL
     assert L.bifattn_plan_status(None, None) == bif.EINVAL
     assert L.bifattn_plan_set_timing(None, 0, 1) == bif.EINVAL
 
@@ -92,3 +99,16 @@ def test_binding_refuses_host_tensors_before_any_call():
         bif.bifattn_decode(FakePlan(), q.float(), q, q, q, q, q, q, stream=0)
     with pytest.raises(ValueError):
         bif.bifattn_decode(FakePlan(), q[:1], q, q, q, q, q, q, stream=0)
+
+
+def test_byte_bound_follows_the_cache_type(L):
+    """One sample's cache rows must fit 2^31 bytes: 2^23 rows of 128 bf16 do
+    not, the same rows of 8-bit codes pass the shape checks (and then need a
+    device)."""
+    bf16 = _create(L, 1, 32, 32, 128, 2**23, 0, 0.0, 1, 0)
+    assert bf16 == (bif.EUNSUPPORTED, None)
+    for kv in (1, 2):
+        st, handle = _create(L, 1, 32, 32, 128, 2**23, 0, 0.0, 1, kv)
+        assert st in (bif.EHIP, bif.OK, bif.ENOMEM)
+        if st == bif.OK:
+            assert L.bifattn_plan_destroy(ctypes.c_void_p(handle)) == bif.OK
