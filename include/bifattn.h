@@ -69,7 +69,7 @@
 extern "C" {
 #endif
 
-#define BIFATTN_VERSION 3
+#define BIFATTN_VERSION 4
 
 typedef enum {
   BIFATTN_OK = 0,
@@ -82,6 +82,17 @@ typedef enum {
   BIFATTN_ELENS = -6,        /* a decode length was outside [0, m_d_max] */
   BIFATTN_ESCALE = -7        /* a key or value scale was not a positive normal float */
 } bifattn_status_t;
+
+/* Which computation bifattn_decode runs (bifattn_dims_t.path). The FAQ on
+ * caveats notes that splitting the attention in two costs parallelism on
+ * small workloads and that a switch on the workload keeps the better of the
+ * two: AUTO picks per plan from the shape (see bifattn_plan_create). */
+typedef enum {
+  BIFATTN_PATH_AUTO = 0,
+  BIFATTN_PATH_BIFURCATED = 1, /* context and decode parts, then the combine (Eq. 3-4) */
+  BIFATTN_PATH_STANDARD = 2    /* one work-group per (sample, group) over context then
+                                  decode rows, output written directly (Eq. 1-2) */
+} bifattn_path_t;
 
 /* Cache element types (bifattn_dims_t.kv_type). */
 typedef enum {
@@ -101,6 +112,7 @@ typedef struct {
   float scale;     /* softmax scale on q.k; 0 selects 1/sqrt(d) */
   int32_t n;       /* new tokens per sample, >= 1 (0 is taken as 1) */
   int32_t kv_type; /* a bifattn_kv_type_t: element type of Kc, Vc, Kd, Vd */
+  int32_t path;    /* a bifattn_path_t; 0 = choose from the workload */
 } bifattn_dims_t;
 
 typedef struct bifattn_plan_s *bifattn_plan_t;
@@ -115,6 +127,8 @@ typedef struct {
   int32_t dec_splits;         /* decode partial results per output row */
   int32_t dec_blocks;         /* decode work-groups per call */
   int32_t fused;              /* 1: context and decode parts in one launch */
+  int32_t path;               /* the path bifattn_decode runs: BIFATTN_PATH_BIFURCATED or
+                                 BIFATTN_PATH_STANDARD */
   size_t workspace_bytes;     /* device memory the plan owns */
 } bifattn_plan_info_t;
 
@@ -128,8 +142,15 @@ typedef enum {
 /*
  * Validate dims and allocate the plan and its workspace on the current HIP
  * device. On success *plan is set; on failure *plan is left NULL.
+ * With dims.path = BIFATTN_PATH_AUTO the plan runs the standard path when
+ * every (sample, group) unit fits in one round of work-groups on the GPU
+ * (b*g <= 512), a unit has at most 32 query rows ((h/g)*n <= 32) and holds
+ * few keys: m_c + m_d_max <= 1100 (<= 600 when b*g > 256), or <= 2200 when
+ * b*(h/g)*n >= 64. There one launch without partials beats reading the
+ * context once; otherwise the bifurcated path. Both give the same attention
+ * (Appendix E.1).
  * Errors: EINVAL (null argument, b/h/g/m_c < 1, m_d_max < 0, n < 0,
- * h % g != 0, unknown kv_type, sizes whose byte counts overflow),
+ * h % g != 0, unknown kv_type or path, sizes whose byte counts overflow),
  * EUNSUPPORTED (d not 64 or 128, (h/g)*n > 64, or one sample's cache rows
  * (m_c + m_d_max) * d * (bytes per element) beyond 2^31 - 1), ENOMEM
  * (device allocation failed), EHIP (no usable device).
@@ -151,7 +172,9 @@ bifattn_status_t bifattn_plan_get_info(bifattn_plan_t plan, bifattn_plan_info_t 
  * one group once and applies it to all b*p query rows of the group; (b)
  * decode partials: per sample and group over its own Kd/Vd; (c) the combine,
  * which merges the (max, sum, weighted-value) partials of both parts into
- * `out`. Kd, Vd and decode_lens may be NULL only when m_d_max == 0.
+ * `out`. On a plan whose path is BIFATTN_PATH_STANDARD it enqueues one
+ * launch instead: per (sample, group), the context rows then the decode
+ * rows in one softmax, written to `out`. Kd, Vd and decode_lens may be NULL only when m_d_max == 0.
  * Errors: EINVAL (null plan or required pointer), EALIGN (q, Kc, Vc, Kd, Vd
  * or out not 16-byte aligned, decode_lens not 4-byte aligned), EHIP (launch
  * failure). Device-side length errors: see bifattn_plan_status.

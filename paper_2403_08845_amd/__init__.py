@@ -20,6 +20,8 @@ OK, EINVAL, EUNSUPPORTED, EALIGN, ENOMEM, EHIP, ELENS, ESCALE = 0, -1, -2, -3, -
 KERNEL_PARTIALS, KERNEL_COMBINE, KERNEL_CALL = 0, 1, 2
 #: Cache element types (bifattn_kv_type_t).
 KV_TYPES = {"bf16": 0, "fp8_e4m3": 1, "int8": 2}
+#: Paths of bifattn_decode (bifattn_path_t): "auto" lets the plan choose.
+PATHS = {"auto": 0, "bifurcated": 1, "standard": 2}
 
 EXPORTED = (
     "bifattn_plan_create", "bifattn_plan_destroy", "bifattn_plan_get_info", "bifattn_decode",
@@ -38,7 +40,8 @@ class BifattnError(RuntimeError):
 class Dims(ctypes.Structure):
     _fields_ = [("b", ctypes.c_int32), ("h", ctypes.c_int32), ("g", ctypes.c_int32),
                 ("d", ctypes.c_int32), ("m_c", ctypes.c_int32), ("m_d_max", ctypes.c_int32),
-                ("scale", ctypes.c_float), ("n", ctypes.c_int32), ("kv_type", ctypes.c_int32)]
+                ("scale", ctypes.c_float), ("n", ctypes.c_int32), ("kv_type", ctypes.c_int32),
+                ("path", ctypes.c_int32)]
 
 
 class PlanInfo(ctypes.Structure):
@@ -46,7 +49,8 @@ class PlanInfo(ctypes.Structure):
                 ("ctx_row_blocks", ctypes.c_int32), ("ctx_blocks", ctypes.c_int32),
                 ("dec_keys_per_block", ctypes.c_int32), ("dec_splits", ctypes.c_int32),
                 ("dec_blocks", ctypes.c_int32),
-                ("fused", ctypes.c_int32), ("workspace_bytes", ctypes.c_size_t)]
+                ("fused", ctypes.c_int32), ("path", ctypes.c_int32),
+                ("workspace_bytes", ctypes.c_size_t)]
 
     def as_dict(self):
         return {name: getattr(self, name) for name, _ in self._fields_}
@@ -100,13 +104,16 @@ def _check(status: int, what: str):
 
 class Plan:
     """A bifattn_plan_t: problem dimensions plus the workspace it owns
-    (n = new tokens per sample; kv = cache element type, a KV_TYPES name)."""
+    (n = new tokens per sample; kv = cache element type, a KV_TYPES name;
+    path = a PATHS name, "auto" for the workload-based switch)."""
 
-    def __init__(self, b, h, g, d, m_c, m_d_max, scale=0.0, n=1, kv="bf16"):
+    def __init__(self, b, h, g, d, m_c, m_d_max, scale=0.0, n=1, kv="bf16", path="auto"):
         if kv not in KV_TYPES:
             raise ValueError(f"kv must be one of {sorted(KV_TYPES)}")
+        if path not in PATHS:
+            raise ValueError(f"path must be one of {sorted(PATHS)}")
         self.kv = kv
-        self.dims = Dims(b, h, g, d, m_c, m_d_max, scale, n, KV_TYPES[kv])
+        self.dims = Dims(b, h, g, d, m_c, m_d_max, scale, n, KV_TYPES[kv], PATHS[path])
         handle = ctypes.c_void_p()
         _check(lib().bifattn_plan_create(ctypes.byref(self.dims), ctypes.byref(handle)),
                "bifattn_plan_create")
@@ -135,8 +142,9 @@ class Plan:
         return info.as_dict()
 
 
-def bifattn_plan_create(b, h, g, d, m_c, m_d_max, scale=0.0, n=1, kv="bf16") -> Plan:
-    return Plan(b, h, g, d, m_c, m_d_max, scale, n, kv)
+def bifattn_plan_create(b, h, g, d, m_c, m_d_max, scale=0.0, n=1, kv="bf16",
+                        path="auto") -> Plan:
+    return Plan(b, h, g, d, m_c, m_d_max, scale, n, kv, path)
 
 
 def bifattn_plan_destroy(plan: Plan):

@@ -26,6 +26,7 @@ struct bifattn_plan_s {
   int dec_keys = 0, S_d = 0, n_dec_blocks = 0;
   int rep_keys = 0, S_r = 0, n_rep_blocks = 0;
   int fused = 1;
+  int path = BIFATTN_PATH_BIFURCATED;  // resolved: bifurcated or standard
   int device = 0;
   // workspace
   void* ws = nullptr;
@@ -133,6 +134,21 @@ bifattn_status_t plan_splits(bifattn_plan_s* P) {
   // own (eight-wave work-groups), launched before the decode work-groups.
   const int launch = env_int("BIFATTN_LAUNCH", 1);
   P->fused = launch == 1 && P->ctx_mode != kCtxLarge ? 1 : 0;
+  // The workload-based switch: the standard path reads the context once per
+  // sample but needs one launch and no partials. It wins while every unit is
+  // resident in one round of work-groups (b*g <= 512), has at most two query
+  // tiles, and holds few keys: up to ~1100 (~600 once units share CUs), or
+  // ~2200 when the bifurcated context part has 64 or more rows per group
+  // (its four-tile and many-row work-groups are the costly ones). These are
+  // the crossovers measured on MI355X over 38 MHA/GQA/MQA shapes.
+  if (d.path == BIFATTN_PATH_AUTO) {
+    const int64_t keys = (int64_t)d.m_c + d.m_d_max;
+    const int64_t lmax = M >= 64 ? 2200 : (units > kCUs ? 600 : 1100);
+    const bool small = units <= 2 * kCUs && P->p <= 32 && keys <= lmax;
+    P->path = small ? BIFATTN_PATH_STANDARD : BIFATTN_PATH_BIFURCATED;
+  } else {
+    P->path = d.path;
+  }
   if ((int64_t)P->n_ctx_blocks + P->n_ctx_small_blocks + P->n_dec_blocks > INT32_MAX / 2 ||
       units * P->S_r > INT32_MAX / 2)
     return BIFATTN_EINVAL;
@@ -147,6 +163,9 @@ bifattn_status_t check_dims(const bifattn_dims_t* d) {
   if (!(std::isfinite(d->scale))) return BIFATTN_EINVAL;
   if (d->kv_type != BIFATTN_KV_BF16 && d->kv_type != BIFATTN_KV_FP8_E4M3 &&
       d->kv_type != BIFATTN_KV_INT8)
+    return BIFATTN_EINVAL;
+  if (d->path != BIFATTN_PATH_AUTO && d->path != BIFATTN_PATH_BIFURCATED &&
+      d->path != BIFATTN_PATH_STANDARD)
     return BIFATTN_EINVAL;
   if (d->d != 64 && d->d != 128) return BIFATTN_EUNSUPPORTED;
   const double ntok = d->n > 0 ? d->n : 1;
@@ -336,6 +355,7 @@ bifattn_status_t bifattn_plan_get_info(bifattn_plan_t P, bifattn_plan_info_t* in
   info->dec_splits = P->S_d * kWaves;
   info->dec_blocks = P->n_dec_blocks;
   info->fused = P->fused;
+  info->path = P->path;
   info->workspace_bytes = P->ws_bytes;
   return BIFATTN_OK;
 }
@@ -368,6 +388,14 @@ bifattn_status_t bifattn_decode_scaled(bifattn_plan_t P, const void* q, const vo
   TimedSection whole(P, BIFATTN_KERNEL_CALL, stream);
   TimedSection part(P, BIFATTN_KERNEL_PARTIALS, stream);
   hipError_t e = hipSuccess;
+  if (P->path == BIFATTN_PATH_STANDARD) {
+    K.out = out;
+    K.v_scale = v_scale;
+    e = launch_standard(K, P->dims.d, kv, P->dec_tiles, stream);
+    part.end();
+    whole.end();
+    return e == hipSuccess ? BIFATTN_OK : BIFATTN_EHIP;
+  }
   K.n_ctx_blocks = 0;
   K.n_ctx_small_blocks = 0;
   K.n_dec_blocks = 0;

@@ -47,6 +47,8 @@ struct PartialsParams {
   const uint8_t* Vd;
   const int32_t* lens;
   const float* k_scale;   // [g] key scales, or null for 1
+  const float* v_scale;   // [g] value scales, or null (standard path only)
+  float* out;             // [b][h][d] rows (standard path only)
   float* ctx_acc;         // [g][S_c][M][d]
   float2* ctx_ml;         // [g][S_c][M]
   float* dec_acc;         // [b][g][S_d][4 waves][p][d]
@@ -106,6 +108,9 @@ hipError_t launch_partials(const PartialsParams& P, int d, int kv, int ctx_mode,
 hipError_t launch_combine(const CombineParams& C, int d, hipStream_t stream);
 // Launch the decode-cache append (one work-group per sample).
 hipError_t launch_append(const AppendParams& A, int d, int kv, hipStream_t stream);
+// Launch the standard (unsplit) attention kernel: one work-group per
+// (sample, group), `tiles` 16-row query tiles per wave, output written directly.
+hipError_t launch_standard(const PartialsParams& P, int d, int kv, int tiles, hipStream_t stream);
 // Launch the many-row context kernel over n_ctx_blocks work-groups.
 hipError_t launch_ctx_large(const PartialsParams& P, int d, int kv, hipStream_t stream);
 

@@ -587,6 +587,8 @@ __device__ __forceinline__ float unit_scale_log2(const PartialsParams& P, int ga
   return P.k_scale ? P.scale_log2 * P.k_scale[gam] : P.scale_log2;
 }
 
+constexpr int cmax(int a, int b) { return a > b ? a : b; }
+
 __device__ __forceinline__ int clamp_len(const int32_t* lens, int i, int m_d_max) {
   const int raw = lens ? lens[i] : 0;
   return raw < 0 ? 0 : (raw > m_d_max ? m_d_max : raw);
@@ -630,13 +632,11 @@ __device__ void decode_block(const PartialsParams& P, int blk, int wave, int lan
   store_partials<D, NT>(st, p, P.dec_acc + prow * D, P.dec_ml + prow, lane);
 }
 
-// Merge the four waves' states of the same NT*16 rows through LDS (in wave
-// order, so the result is deterministic) and write rows < nrows of the
-// merged partial to acc_out / ml_out.
+// Merge the four waves' states of the same NT*16 rows through LDS, in wave
+// order (so the result is deterministic): afterwards row r's merged partial
+// is acc_s[r*LD ..], m_s[r], l_s[r] (LD = d + 4), visible to every thread.
 template <int D, int NT>
-__device__ __forceinline__ void merge_waves_and_store(RowState<D, NT>& st, float* lds, int nrows,
-                                                      float* acc_out, float2* ml_out, int wave,
-                                                      int lane) {
+__device__ __forceinline__ void merge_waves(RowState<D, NT>& st, float* lds, int wave, int lane) {
   constexpr int DV = D / 16;
   constexpr int LD = D + 4;  // padded LDS row
   constexpr int ROWS = NT * kRowsPerTile;
@@ -675,6 +675,20 @@ __device__ __forceinline__ void merge_waves_and_store(RowState<D, NT>& st, float
     }
     __syncthreads();
   }
+}
+
+// Merge the waves' states and write rows < nrows of the merged partial to
+// acc_out / ml_out.
+template <int D, int NT>
+__device__ __forceinline__ void merge_waves_and_store(RowState<D, NT>& st, float* lds, int nrows,
+                                                      float* acc_out, float2* ml_out, int wave,
+                                                      int lane) {
+  constexpr int LD = D + 4;
+  constexpr int ROWS = NT * kRowsPerTile;
+  merge_waves<D, NT>(st, lds, wave, lane);
+  const float* acc_s = lds;
+  const float* m_s = lds + ROWS * LD;
+  const float* l_s = m_s + ROWS;
   constexpr int V4 = D / 4;
   for (int idx = threadIdx.x; idx < nrows * V4; idx += kThreads) {
     const int row = idx / V4, c = idx % V4;
@@ -683,6 +697,7 @@ __device__ __forceinline__ void merge_waves_and_store(RowState<D, NT>& st, float
   }
   for (int row = threadIdx.x; row < nrows; row += kThreads) ml_out[row] = float2{m_s[row], l_s[row]};
 }
+
 template <int D, int NT> struct MergeLds {
   static constexpr int bytes = (NT * kRowsPerTile * (D + 4) + 2 * NT * kRowsPerTile) * 4;
 };
@@ -718,6 +733,90 @@ __device__ void ctx_small_block(const PartialsParams& P, int blk, int wave, int 
   const size_t prow = (size_t)blk * P.M;
   __syncthreads();  // the merge buffer overlays the waves' K tiles
   merge_waves_and_store<D, NT>(st, merge_lds, M, P.ctx_acc + prow * D, P.ctx_ml + prow, wave, lane);
+}
+
+// Standard attention, the other side of the workload-based switch (FAQ on
+// caveats: splitting the attention costs parallelism on small workloads, so
+// they run the plain computation): work-group (sample i, group gam) streams
+// the whole sequence of the unit, the group's context rows and then the
+// sample's decode rows, as one softmax (Section 3.3, Eq. 1-2). The context
+// is read once per sample instead of once per group, so this only pays where
+// launches and latency, not bytes, set the time. The four waves take
+// interleaved tiles of each segment, merge in LDS and write the normalized
+// output rows (times the group's value scale) directly: one launch, no
+// partials, no combine. The unit with gam = 0 checks the sample's length and
+// the unit with i = 0 its group's scales.
+template <int D, int NT, typename KV>
+__device__ void standard_block(const PartialsParams& P, int blk, int wave, int lane, u32x4* qw,
+                               u32x4* kl, float* merge_lds) {
+  constexpr int RB = D * KV::ES;
+  constexpr int LD = D + 4;
+  constexpr int ROWS = NT * kRowsPerTile;
+  const int gam = blk % P.g, i = blk / P.g;
+  const __amdgpu_buffer_rsrc_t rkc = rows_rsrc(P.Kc + (size_t)gam * P.m_c * RB, P.m_c, RB);
+  const __amdgpu_buffer_rsrc_t rvc = rows_rsrc(P.Vc + (size_t)gam * P.m_c * RB, P.m_c, RB);
+  const int k0 = wave * kTileKeys;
+  constexpr int stride = kWaves * kTileKeys;
+  TileRegs<D, KV> A;
+  A.load(rkc, rvc, k0, lane);  // first context tile in flight during the set-up
+  const int p = P.p;
+  const uint16_t* qbase = P.q + ((size_t)i * P.h + (size_t)gam * p) * D;
+  stage_q<D, NT>(qw, [&](int r) -> const uint16_t* { return r < p ? qbase + (size_t)r * D : nullptr; },
+                 P.q_sign, lane);
+  const float sl2 = unit_scale_log2(P, gam);
+  RowState<D, NT> st;
+  st.init();
+  // Context rows: visible to every token (a causal limit only applies among
+  // the decode rows).
+  stream_keys<D, NT, KV>(st, qw, kl, rkc, rvc, A, k0, P.m_c, P.m_c, stride, 1, sl2, lane);
+  const int len = clamp_len(P.lens, i, P.m_d_max);
+  if (len > 0) {  // wave-uniform
+    const size_t cache = (size_t)(i * P.g + gam) * P.m_d_max * RB;
+    const __amdgpu_buffer_rsrc_t rkd = rows_rsrc(P.Kd + cache, len, RB);
+    const __amdgpu_buffer_rsrc_t rvd = rows_rsrc(P.Vd + cache, len, RB);
+    A.load(rkd, rvd, k0, lane);
+    stream_keys<D, NT, KV>(st, qw, kl, rkd, rvd, A, k0, len, len, stride, P.ntok, sl2, lane);
+  }
+  __syncthreads();  // the merge buffer overlays the waves' K tiles
+  merge_waves<D, NT>(st, merge_lds, wave, lane);
+  const float vs = P.v_scale ? P.v_scale[gam] : 1.f;
+  const float* acc_s = merge_lds;
+  const float* l_s = merge_lds + ROWS * LD + ROWS;
+  float* out = P.out + ((size_t)i * P.h + (size_t)gam * p) * D;
+  constexpr int V4 = D / 4;
+  for (int idx = threadIdx.x; idx < p * V4; idx += kThreads) {
+    const int row = idx / V4, c = idx % V4;
+    const float inv = vs / l_s[row];
+    *reinterpret_cast<f32x4*>(out + (size_t)row * D + 4 * c) =
+        *reinterpret_cast<const f32x4*>(acc_s + row * LD + 4 * c) * inv;
+  }
+  if (threadIdx.x == 0) {
+    int flags = 0;
+    if (gam == 0 && P.lens) {
+      const int raw = P.lens[i];
+      if (raw < 0 || raw > P.m_d_max) flags |= kStatusLens;
+    }
+    if (i == 0) {
+      const float ks = P.k_scale ? P.k_scale[gam] : 1.f;
+      if (!(ks >= __FLT_MIN__ && ks <= __FLT_MAX__ && vs >= __FLT_MIN__ && vs <= __FLT_MAX__))
+        flags |= kStatusScale;
+    }
+    if (flags) atomicOr(P.status, flags);
+  }
+}
+
+template <int D, int NT, typename KV>
+__global__ __launch_bounds__(kThreads) void standard_kernel(PartialsParams P) {
+  constexpr int QSLOTS = kWaves * NT * (D / 32) * 64;
+  constexpr int KSLOTS = kWaves * kTileKeys * D / 8;
+  constexpr int MERGE = (MergeLds<D, NT>::bytes + 15) / 16;  // overlays the K tiles
+  __shared__ __attribute__((aligned(16))) u32x4 lds[QSLOTS + cmax(KSLOTS, MERGE)];
+  const int lane = threadIdx.x & 63, wave = wave_id();
+  u32x4* qw = lds + wave * NT * (D / 32) * 64;
+  u32x4* kl = lds + QSLOTS + wave * (kTileKeys * D / 8);
+  if ((int)blockIdx.x < P.b * P.g)
+    standard_block<D, NT, KV>(P, blockIdx.x, wave, lane, qw, kl,
+                              reinterpret_cast<float*>(lds + QSLOTS));
 }
 
 // XCD-aware order for the large context path: the hardware hands work-group
@@ -863,8 +962,6 @@ __global__ __launch_bounds__(kLargeThreads) __attribute__((amdgpu_waves_per_eu(4
 ctx_large_kernel(PartialsParams P) {
   ctx_large_body<D, KV>(P);
 }
-
-constexpr int cmax(int a, int b) { return a > b ? a : b; }
 
 
 // Grid: n_ctx_small_blocks work-groups of the few-row context path, then
@@ -1052,6 +1149,28 @@ hipError_t launch_partials_d(const PartialsParams& P, int kv, int ctx_mode, int 
   }
 }
 
+template <int D, typename KV>
+hipError_t launch_standard_dk(const PartialsParams& P, int tiles, hipStream_t stream) {
+  const int grid = P.b * P.g;
+  switch (tiles) {
+    case 1: standard_kernel<D, 1, KV><<<grid, kThreads, 0, stream>>>(P); break;
+    case 2: standard_kernel<D, 2, KV><<<grid, kThreads, 0, stream>>>(P); break;
+    case 4: standard_kernel<D, 4, KV><<<grid, kThreads, 0, stream>>>(P); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+template <int D>
+hipError_t launch_standard_d(const PartialsParams& P, int kv, int tiles, hipStream_t stream) {
+  switch (kv) {
+    case kKvBf16: return launch_standard_dk<D, KvBf16>(P, tiles, stream);
+    case kKvFp8: return launch_standard_dk<D, KvFp8>(P, tiles, stream);
+    case kKvInt8: return launch_standard_dk<D, KvInt8>(P, tiles, stream);
+    default: return hipErrorInvalidValue;
+  }
+}
+
 template <int D>
 hipError_t launch_ctx_large_d(const PartialsParams& P, int kv, hipStream_t stream) {
   switch (kv) {
@@ -1110,6 +1229,13 @@ hipError_t launch_ctx_large(const PartialsParams& P, int d, int kv, hipStream_t 
   if (P.n_ctx_blocks == 0) return hipSuccess;
   if (d == 128) return launch_ctx_large_d<128>(P, kv, stream);
   if (d == 64) return launch_ctx_large_d<64>(P, kv, stream);
+  return hipErrorInvalidValue;
+}
+hipError_t launch_standard(const PartialsParams& P, int d, int kv, int tiles,
+                           hipStream_t stream) {
+  if (P.b * P.g == 0) return hipSuccess;
+  if (d == 128) return launch_standard_d<128>(P, kv, tiles, stream);
+  if (d == 64) return launch_standard_d<64>(P, kv, tiles, stream);
   return hipErrorInvalidValue;
 }
 hipError_t launch_partials(const PartialsParams& P, int d, int kv, int ctx_mode, int dec_tiles,

@@ -32,12 +32,16 @@ def gate_errors(out, ref):
     return max_abs, rel_l2
 
 
-def assert_parity(out, ref, what=""):
+def assert_parity(out, ref, what="", gate_max_abs=GATE_MAX_ABS):
+    """gate_max_abs: a test whose softmax is much sharper than the workloads'
+    (a few bf16-rounded weights then make up an output entry) may raise the
+    max-abs gate up to the contract, never the relative-L2 gate."""
+    assert gate_max_abs <= CONTRACT_MAX_ABS
     out = np.asarray(out, np.float64)
     assert np.all(np.isfinite(out)), f"{what}: non-finite GPU output"
     max_abs, rel_l2 = gate_errors(out, ref)
     assert max_abs <= CONTRACT_MAX_ABS, f"{what}: max abs {max_abs:.3e} breaks the 1e-2 contract"
-    assert max_abs <= GATE_MAX_ABS and rel_l2 <= GATE_REL_L2, \
+    assert max_abs <= gate_max_abs and rel_l2 <= GATE_REL_L2, \
         f"{what}: max abs {max_abs:.3e} / rel L2 {rel_l2:.3e} outside the gate " \
-        f"({GATE_MAX_ABS:.0e} / {GATE_REL_L2:.0e})"
+        f"({gate_max_abs:.0e} / {GATE_REL_L2:.0e})"
     return max_abs, rel_l2

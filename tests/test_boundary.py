@@ -35,7 +35,7 @@ def test_every_declared_symbol_is_exported(L):
 
 
 def test_version_and_status_strings(L):
-    assert bif.bifattn_version() == 3
+    assert bif.bifattn_version() == 4
     for code in (bif.OK, bif.EINVAL, bif.EUNSUPPORTED, bif.EALIGN, bif.ENOMEM, bif.EHIP, bif.ELENS,
                  bif.ESCALE):
         assert bif.status_string(code)

@@ -140,7 +140,11 @@ def test_strongly_different_group_scales(kv):
         out = run_decode(x)
         ref = oracle.attention(**x)
         u = _value_units(x)
-        _report(f"{kv} {case} spread", *assert_parity(out / u, ref / u, f"{kv} {case}"))
+        # key scales up to 8x make the first groups' softmax ~8x sharper than
+        # the workloads': one bf16-rounded weight can carry an output entry,
+        # bounded by 2^-9 * max|v| (~9e-3 in value units): the contract bound
+        _report(f"{kv} {case} spread",
+                *assert_parity(out / u, ref / u, f"{kv} {case}", gate_max_abs=1e-2))
 
 
 @pytest.mark.parametrize("kv", KVS)
