@@ -15,9 +15,10 @@ Prints ONE JSON line: value = algorithmic KV bytes per step (one copy of the
 context K/V plus every sample's valid decode K/V, Section 4.3) divided by the
 measured time per step, in GB/s. ``roofline`` reports the partial kernel
 (the dominant launch) against the 8 TB/s HBM peak, its duration measured with
-HIP events recorded by the library around that launch on its stream, over a
-second pass of the same steps (events are kept out of the value loop because
-each record costs GPU time between kernels). ``cpu_baseline`` times the fp64 CPU oracle on the host on the same
+HIP events that the library's launch records with the kernel itself
+(hipExtLaunchKernel start/stop events, the span a kernel trace shows), over a
+second pass of the same steps (kept out of the value loop, where no events
+are recorded). ``cpu_baseline`` times the fp64 CPU oracle on the host on the same
 workload. ``ablation`` times the replicated-KV kernel (no bifurcation).
 """
 from __future__ import annotations
@@ -259,10 +260,8 @@ def main():
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
     ms_per_step = elapsed * 1e3 / args.steps
-    # Kernel timing (roofline): the same steps again, with the library
-    # recording HIP events on the launch stream around its partial kernel in
-    # every step. Kept out of the loop above because each event record costs
-    # a few microseconds of GPU time between kernels.
+    # Kernel timing (roofline): the same steps again, the library's partial
+    # launch recording start/stop events with the kernel in every step.
     bif.bifattn_plan_set_timing(plan, bif.KERNEL_PARTIALS, args.steps)
     torch.cuda.synchronize()
     t0 = time.perf_counter()

@@ -251,8 +251,12 @@ bifattn_status_t bifattn_plan_status(bifattn_plan_t plan, hipStream_t stream);
 
 /*
  * Time the selected kernel of the next `capacity` calls with HIP events
- * recorded on each call's stream around that kernel's launch (capacity 0
- * switches timing off). Timing stops recording when full.
+ * (capacity 0 switches timing off). For BIFATTN_KERNEL_PARTIALS and
+ * BIFATTN_KERNEL_COMBINE the launches record the events themselves
+ * (hipExtLaunchKernel), so they span the kernels' own execution, from the
+ * start of the first launch of the section to the end of its last; for
+ * BIFATTN_KERNEL_CALL they are recorded on the stream around the whole
+ * call. Timing stops recording when full.
  * Errors: EINVAL (bad kernel id or negative capacity), ENOMEM, EHIP.
  */
 bifattn_status_t bifattn_plan_set_timing(bifattn_plan_t plan, bifattn_kernel_t kernel,

@@ -192,18 +192,29 @@ void free_events(bifattn_plan_s* P) {
   P->timed_kernel = -1;
 }
 
-// Event pair around one kernel of this call, if that kernel is being timed.
+// Event pair of one timed section of this call, if that section is being
+// timed. With `in_kernel`, the section's launches record the pair
+// themselves (the first launch's kernel start, the last launch's kernel
+// end: first() / last() / both()), so the time is the kernels' own, as a
+// kernel trace shows it; otherwise the pair is recorded on the stream around
+// the section.
 struct TimedSection {
   bifattn_plan_s* P;
   hipStream_t stream;
   bool on = false;
-  TimedSection(bifattn_plan_s* P_, int kernel, hipStream_t s) : P(P_), stream(s) {
+  bool in_kernel = false;
+  TimedSection(bifattn_plan_s* P_, int kernel, hipStream_t s, bool in_kernel_ = false)
+      : P(P_), stream(s), in_kernel(in_kernel_) {
     on = P->timed_kernel == kernel && P->timing_n < P->timing_cap;
-    if (on) (void)hipEventRecord(P->events[2 * P->timing_n], stream);
+    if (on && !in_kernel) (void)hipEventRecord(P->events[2 * P->timing_n], stream);
   }
+  hipEvent_t ev(int k) const { return on && in_kernel ? P->events[2 * P->timing_n + k] : nullptr; }
+  LaunchEvents first() const { return LaunchEvents{ev(0), nullptr}; }
+  LaunchEvents last() const { return LaunchEvents{nullptr, ev(1)}; }
+  LaunchEvents both() const { return LaunchEvents{ev(0), ev(1)}; }
   void end() {
     if (on) {
-      (void)hipEventRecord(P->events[2 * P->timing_n + 1], stream);
+      if (!in_kernel) (void)hipEventRecord(P->events[2 * P->timing_n + 1], stream);
       ++P->timing_n;
       on = false;
     }
@@ -386,12 +397,12 @@ bifattn_status_t bifattn_decode_scaled(bifattn_plan_t P, const void* q, const vo
   K.dec_keys = P->dec_keys;
   K.S_d = P->S_d;
   TimedSection whole(P, BIFATTN_KERNEL_CALL, stream);
-  TimedSection part(P, BIFATTN_KERNEL_PARTIALS, stream);
+  TimedSection part(P, BIFATTN_KERNEL_PARTIALS, stream, true);
   hipError_t e = hipSuccess;
   if (P->path == BIFATTN_PATH_STANDARD) {
     K.out = out;
     K.v_scale = v_scale;
-    e = launch_standard(K, P->dims.d, kv, P->dec_tiles, stream);
+    e = launch_standard(K, P->dims.d, kv, P->dec_tiles, stream, part.both());
     part.end();
     whole.end();
     return e == hipSuccess ? BIFATTN_OK : BIFATTN_EHIP;
@@ -399,31 +410,37 @@ bifattn_status_t bifattn_decode_scaled(bifattn_plan_t P, const void* q, const vo
   K.n_ctx_blocks = 0;
   K.n_ctx_small_blocks = 0;
   K.n_dec_blocks = 0;
+  // Two launches: the first carries the start event and the second the end
+  // event, unless there are no decode work-groups (then the first carries both).
+  const bool two = P->n_dec_blocks > 0;
   if (P->ctx_mode == kCtxLarge) {
     // The many-row context kernel, then the decode work-groups.
     K.n_ctx_blocks = P->n_ctx_blocks;
-    e = launch_ctx_large(K, P->dims.d, kv, stream);
+    e = launch_ctx_large(K, P->dims.d, kv, stream, two ? part.first() : part.both());
     K.n_ctx_blocks = 0;
     K.n_dec_blocks = P->n_dec_blocks;
-    if (e == hipSuccess) e = launch_partials(K, P->dims.d, kv, kCtxNone, P->dec_tiles, stream);
+    if (e == hipSuccess && two)
+      e = launch_partials(K, P->dims.d, kv, kCtxNone, P->dec_tiles, stream, part.last());
   } else if (P->fused) {
     K.n_ctx_small_blocks = P->n_ctx_small_blocks;
     K.n_dec_blocks = P->n_dec_blocks;
-    e = launch_partials(K, P->dims.d, kv, P->ctx_mode, P->dec_tiles, stream);
+    e = launch_partials(K, P->dims.d, kv, P->ctx_mode, P->dec_tiles, stream, part.both());
   } else {
     K.n_ctx_small_blocks = P->n_ctx_small_blocks;
-    e = launch_partials(K, P->dims.d, kv, P->ctx_mode, P->dec_tiles, stream);
+    e = launch_partials(K, P->dims.d, kv, P->ctx_mode, P->dec_tiles, stream,
+                        two ? part.first() : part.both());
     K.n_ctx_small_blocks = 0;
     K.n_dec_blocks = P->n_dec_blocks;
-    if (e == hipSuccess) e = launch_partials(K, P->dims.d, kv, kCtxNone, P->dec_tiles, stream);
+    if (e == hipSuccess && two)
+      e = launch_partials(K, P->dims.d, kv, kCtxNone, P->dec_tiles, stream, part.last());
   }
   part.end();
   if (e != hipSuccess) return BIFATTN_EHIP;
-  TimedSection comb(P, BIFATTN_KERNEL_COMBINE, stream);
+  TimedSection comb(P, BIFATTN_KERNEL_COMBINE, stream, true);
   CombineParams C = combine_params(P, has_dec ? decode_lens : nullptr, k_scale, v_scale, out);
   C.S_c = P->S_c;
   C.S_d = P->S_d * kWaves;
-  e = launch_combine(C, P->dims.d, stream);
+  e = launch_combine(C, P->dims.d, stream, comb.both());
   comb.end();
   whole.end();
   return e == hipSuccess ? BIFATTN_OK : BIFATTN_EHIP;
@@ -458,15 +475,16 @@ bifattn_status_t bifattn_decode_replicated_scaled(bifattn_plan_t P, const void* 
   K.n_ctx_small_blocks = 0;
   K.n_dec_blocks = P->n_rep_blocks;
   TimedSection whole(P, BIFATTN_KERNEL_CALL, stream);
-  TimedSection part(P, BIFATTN_KERNEL_PARTIALS, stream);
-  hipError_t e = launch_partials(K, P->dims.d, P->dims.kv_type, kCtxNone, P->dec_tiles, stream);
+  TimedSection part(P, BIFATTN_KERNEL_PARTIALS, stream, true);
+  hipError_t e = launch_partials(K, P->dims.d, P->dims.kv_type, kCtxNone, P->dec_tiles, stream,
+                                 part.both());
   part.end();
   if (e != hipSuccess) return BIFATTN_EHIP;
-  TimedSection comb(P, BIFATTN_KERNEL_COMBINE, stream);
+  TimedSection comb(P, BIFATTN_KERNEL_COMBINE, stream, true);
   CombineParams C = combine_params(P, has_dec ? decode_lens : nullptr, k_scale, v_scale, out);
   C.S_c = 0;
   C.S_d = P->S_r * kWaves;
-  e = launch_combine(C, P->dims.d, stream);
+  e = launch_combine(C, P->dims.d, stream, comb.both());
   comb.end();
   whole.end();
   return e == hipSuccess ? BIFATTN_OK : BIFATTN_EHIP;

@@ -101,17 +101,27 @@ struct AppendParams {
 
 enum CtxMode { kCtxNone = 0, kCtxSmall1 = 1, kCtxSmall2 = 2, kCtxSmall4 = 4, kCtxLarge = 8 };
 
+// Events a launch records with its kernel (start / end of the kernel itself,
+// not of the stream around it); null members are not recorded.
+struct LaunchEvents {
+  hipEvent_t start = nullptr;
+  hipEvent_t stop = nullptr;
+};
+
 // Launch the partial kernel over n_ctx_blocks + n_ctx_small_blocks +
 // n_dec_blocks work-groups.
 hipError_t launch_partials(const PartialsParams& P, int d, int kv, int ctx_mode, int dec_tiles,
-                           hipStream_t stream);
-hipError_t launch_combine(const CombineParams& C, int d, hipStream_t stream);
+                           hipStream_t stream, const LaunchEvents& ev = {});
+hipError_t launch_combine(const CombineParams& C, int d, hipStream_t stream,
+                          const LaunchEvents& ev = {});
 // Launch the decode-cache append (one work-group per sample).
 hipError_t launch_append(const AppendParams& A, int d, int kv, hipStream_t stream);
 // Launch the standard (unsplit) attention kernel: one work-group per
 // (sample, group), `tiles` 16-row query tiles per wave, output written directly.
-hipError_t launch_standard(const PartialsParams& P, int d, int kv, int tiles, hipStream_t stream);
+hipError_t launch_standard(const PartialsParams& P, int d, int kv, int tiles, hipStream_t stream,
+                           const LaunchEvents& ev = {});
 // Launch the many-row context kernel over n_ctx_blocks work-groups.
-hipError_t launch_ctx_large(const PartialsParams& P, int d, int kv, hipStream_t stream);
+hipError_t launch_ctx_large(const PartialsParams& P, int d, int kv, hipStream_t stream,
+                            const LaunchEvents& ev = {});
 
 }  // namespace bifattn

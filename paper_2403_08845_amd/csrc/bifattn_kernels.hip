@@ -29,6 +29,7 @@
 // codes are widened to bf16 on the way from memory to the operands and the
 // matrix products stay bf16. The key scale folds into the softmax scale of
 // the group's units and the value scale into the combine.
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 
 #include "bifattn_internal.h"
@@ -1103,83 +1104,95 @@ __global__ __launch_bounds__(256) void combine_kernel(CombineParams C) {
   for (int e = 0; e < PER; ++e) o[e] = acc[e] * inv;
 }
 
+// One launch; with events, through hipExtLaunchKernel so that they carry the
+// kernel's own start and end.
+template <typename Prm>
+hipError_t launch(void (*kernel)(Prm), int grid, int block, hipStream_t stream,
+                  const LaunchEvents& ev, const Prm& p) {
+  if (ev.start || ev.stop)
+    hipExtLaunchKernelGGL(kernel, dim3(grid), dim3(block), 0, stream, ev.start, ev.stop, 0, p);
+  else
+    kernel<<<grid, block, 0, stream>>>(p);
+  return hipGetLastError();
+}
+
 template <int D, typename KV, int CTX>
-hipError_t launch_partials_ctx(const PartialsParams& P, int dec_tiles, hipStream_t stream) {
+hipError_t launch_partials_ctx(const PartialsParams& P, int dec_tiles, hipStream_t stream,
+                               const LaunchEvents& ev) {
   const int grid = P.n_ctx_small_blocks + P.n_dec_blocks;
   if (grid == 0) return hipSuccess;
   switch (dec_tiles) {
     case 1:
       if constexpr (fits_two_waves<D, CTX, 1>())
-        partials_kernel_2w<D, KV, CTX, 1><<<grid, kThreads, 0, stream>>>(P);
+        return launch(partials_kernel_2w<D, KV, CTX, 1>, grid, kThreads, stream, ev, P);
       else
-        partials_kernel<D, KV, CTX, 1><<<grid, kThreads, 0, stream>>>(P);
-      break;
+        return launch(partials_kernel<D, KV, CTX, 1>, grid, kThreads, stream, ev, P);
     case 2:
       if constexpr (fits_two_waves<D, CTX, 2>())
-        partials_kernel_2w<D, KV, CTX, 2><<<grid, kThreads, 0, stream>>>(P);
+        return launch(partials_kernel_2w<D, KV, CTX, 2>, grid, kThreads, stream, ev, P);
       else
-        partials_kernel<D, KV, CTX, 2><<<grid, kThreads, 0, stream>>>(P);
-      break;
-    case 4: partials_kernel<D, KV, CTX, 4><<<grid, kThreads, 0, stream>>>(P); break;
+        return launch(partials_kernel<D, KV, CTX, 2>, grid, kThreads, stream, ev, P);
+    case 4: return launch(partials_kernel<D, KV, CTX, 4>, grid, kThreads, stream, ev, P);
     default: return hipErrorInvalidValue;
   }
-  return hipGetLastError();
 }
 
 template <int D, typename KV>
 hipError_t launch_partials_dk(const PartialsParams& P, int ctx_mode, int dec_tiles,
-                              hipStream_t stream) {
+                              hipStream_t stream, const LaunchEvents& ev) {
   switch (ctx_mode) {
-    case kCtxNone: return launch_partials_ctx<D, KV, kCtxNone>(P, dec_tiles, stream);
-    case kCtxSmall1: return launch_partials_ctx<D, KV, kCtxSmall1>(P, dec_tiles, stream);
-    case kCtxSmall2: return launch_partials_ctx<D, KV, kCtxSmall2>(P, dec_tiles, stream);
-    case kCtxSmall4: return launch_partials_ctx<D, KV, kCtxSmall4>(P, dec_tiles, stream);
+    case kCtxNone: return launch_partials_ctx<D, KV, kCtxNone>(P, dec_tiles, stream, ev);
+    case kCtxSmall1: return launch_partials_ctx<D, KV, kCtxSmall1>(P, dec_tiles, stream, ev);
+    case kCtxSmall2: return launch_partials_ctx<D, KV, kCtxSmall2>(P, dec_tiles, stream, ev);
+    case kCtxSmall4: return launch_partials_ctx<D, KV, kCtxSmall4>(P, dec_tiles, stream, ev);
     default: return hipErrorInvalidValue;
   }
 }
 
 template <int D>
 hipError_t launch_partials_d(const PartialsParams& P, int kv, int ctx_mode, int dec_tiles,
-                             hipStream_t stream) {
+                             hipStream_t stream, const LaunchEvents& ev) {
   switch (kv) {
-    case kKvBf16: return launch_partials_dk<D, KvBf16>(P, ctx_mode, dec_tiles, stream);
-    case kKvFp8: return launch_partials_dk<D, KvFp8>(P, ctx_mode, dec_tiles, stream);
-    case kKvInt8: return launch_partials_dk<D, KvInt8>(P, ctx_mode, dec_tiles, stream);
+    case kKvBf16: return launch_partials_dk<D, KvBf16>(P, ctx_mode, dec_tiles, stream, ev);
+    case kKvFp8: return launch_partials_dk<D, KvFp8>(P, ctx_mode, dec_tiles, stream, ev);
+    case kKvInt8: return launch_partials_dk<D, KvInt8>(P, ctx_mode, dec_tiles, stream, ev);
     default: return hipErrorInvalidValue;
   }
 }
 
 template <int D, typename KV>
-hipError_t launch_standard_dk(const PartialsParams& P, int tiles, hipStream_t stream) {
+hipError_t launch_standard_dk(const PartialsParams& P, int tiles, hipStream_t stream,
+                              const LaunchEvents& ev) {
   const int grid = P.b * P.g;
   switch (tiles) {
-    case 1: standard_kernel<D, 1, KV><<<grid, kThreads, 0, stream>>>(P); break;
-    case 2: standard_kernel<D, 2, KV><<<grid, kThreads, 0, stream>>>(P); break;
-    case 4: standard_kernel<D, 4, KV><<<grid, kThreads, 0, stream>>>(P); break;
-    default: return hipErrorInvalidValue;
-  }
-  return hipGetLastError();
-}
-
-template <int D>
-hipError_t launch_standard_d(const PartialsParams& P, int kv, int tiles, hipStream_t stream) {
-  switch (kv) {
-    case kKvBf16: return launch_standard_dk<D, KvBf16>(P, tiles, stream);
-    case kKvFp8: return launch_standard_dk<D, KvFp8>(P, tiles, stream);
-    case kKvInt8: return launch_standard_dk<D, KvInt8>(P, tiles, stream);
+    case 1: return launch(standard_kernel<D, 1, KV>, grid, kThreads, stream, ev, P);
+    case 2: return launch(standard_kernel<D, 2, KV>, grid, kThreads, stream, ev, P);
+    case 4: return launch(standard_kernel<D, 4, KV>, grid, kThreads, stream, ev, P);
     default: return hipErrorInvalidValue;
   }
 }
 
 template <int D>
-hipError_t launch_ctx_large_d(const PartialsParams& P, int kv, hipStream_t stream) {
+hipError_t launch_standard_d(const PartialsParams& P, int kv, int tiles, hipStream_t stream,
+                             const LaunchEvents& ev) {
   switch (kv) {
-    case kKvBf16: ctx_large_kernel<D, KvBf16><<<P.n_ctx_blocks, kLargeThreads, 0, stream>>>(P); break;
-    case kKvFp8: ctx_large_kernel<D, KvFp8><<<P.n_ctx_blocks, kLargeThreads, 0, stream>>>(P); break;
-    case kKvInt8: ctx_large_kernel<D, KvInt8><<<P.n_ctx_blocks, kLargeThreads, 0, stream>>>(P); break;
+    case kKvBf16: return launch_standard_dk<D, KvBf16>(P, tiles, stream, ev);
+    case kKvFp8: return launch_standard_dk<D, KvFp8>(P, tiles, stream, ev);
+    case kKvInt8: return launch_standard_dk<D, KvInt8>(P, tiles, stream, ev);
     default: return hipErrorInvalidValue;
   }
-  return hipGetLastError();
+}
+
+template <int D>
+hipError_t launch_ctx_large_d(const PartialsParams& P, int kv, hipStream_t stream,
+                              const LaunchEvents& ev) {
+  const int grid = P.n_ctx_blocks;
+  switch (kv) {
+    case kKvBf16: return launch(ctx_large_kernel<D, KvBf16>, grid, kLargeThreads, stream, ev, P);
+    case kKvFp8: return launch(ctx_large_kernel<D, KvFp8>, grid, kLargeThreads, stream, ev, P);
+    case kKvInt8: return launch(ctx_large_kernel<D, KvInt8>, grid, kLargeThreads, stream, ev, P);
+    default: return hipErrorInvalidValue;
+  }
 }
 
 // Decode-cache append (the decode cache holds the keys and values of the
@@ -1225,36 +1238,34 @@ hipError_t launch_append(const AppendParams& A, int d, int kv, hipStream_t strea
   }
   return hipGetLastError();
 }
-hipError_t launch_ctx_large(const PartialsParams& P, int d, int kv, hipStream_t stream) {
+hipError_t launch_ctx_large(const PartialsParams& P, int d, int kv, hipStream_t stream,
+                            const LaunchEvents& ev) {
   if (P.n_ctx_blocks == 0) return hipSuccess;
-  if (d == 128) return launch_ctx_large_d<128>(P, kv, stream);
-  if (d == 64) return launch_ctx_large_d<64>(P, kv, stream);
+  if (d == 128) return launch_ctx_large_d<128>(P, kv, stream, ev);
+  if (d == 64) return launch_ctx_large_d<64>(P, kv, stream, ev);
   return hipErrorInvalidValue;
 }
 hipError_t launch_standard(const PartialsParams& P, int d, int kv, int tiles,
-                           hipStream_t stream) {
+                           hipStream_t stream, const LaunchEvents& ev) {
   if (P.b * P.g == 0) return hipSuccess;
-  if (d == 128) return launch_standard_d<128>(P, kv, tiles, stream);
-  if (d == 64) return launch_standard_d<64>(P, kv, tiles, stream);
+  if (d == 128) return launch_standard_d<128>(P, kv, tiles, stream, ev);
+  if (d == 64) return launch_standard_d<64>(P, kv, tiles, stream, ev);
   return hipErrorInvalidValue;
 }
 hipError_t launch_partials(const PartialsParams& P, int d, int kv, int ctx_mode, int dec_tiles,
-                           hipStream_t stream) {
-  if (d == 128) return launch_partials_d<128>(P, kv, ctx_mode, dec_tiles, stream);
-  if (d == 64) return launch_partials_d<64>(P, kv, ctx_mode, dec_tiles, stream);
+                           hipStream_t stream, const LaunchEvents& ev) {
+  if (d == 128) return launch_partials_d<128>(P, kv, ctx_mode, dec_tiles, stream, ev);
+  if (d == 64) return launch_partials_d<64>(P, kv, ctx_mode, dec_tiles, stream, ev);
   return hipErrorInvalidValue;
 }
 
-hipError_t launch_combine(const CombineParams& C, int d, hipStream_t stream) {
+hipError_t launch_combine(const CombineParams& C, int d, hipStream_t stream,
+                          const LaunchEvents& ev) {
   const int rows = C.b * C.h;
   const int grid = (rows + 3) / 4;
-  if (d == 128)
-    combine_kernel<128><<<grid, 256, 0, stream>>>(C);
-  else if (d == 64)
-    combine_kernel<64><<<grid, 256, 0, stream>>>(C);
-  else
-    return hipErrorInvalidValue;
-  return hipGetLastError();
+  if (d == 128) return launch(combine_kernel<128>, grid, 256, stream, ev, C);
+  if (d == 64) return launch(combine_kernel<64>, grid, 256, stream, ev, C);
+  return hipErrorInvalidValue;
 }
 
 }  // namespace bifattn
