@@ -229,19 +229,27 @@ __device__ __forceinline__ u32x4 load16(const uint16_t* p) {
 // same order, as the V^T operand a lane builds from value rows 4e + G.
 __device__ __forceinline__ int qk_key(int a, int r) { return 16 * a + 4 * (r & 3) + (r >> 2); }
 
-// Per-wave running state of NT query tiles.
-template <int D, int NT> struct RowState {
+// Per-wave running state of NT query tiles. With MS (matrix-core sums) the
+// row sums come from one more MFMA per tile against an all-ones operand:
+// lacc holds the row's sum of the bf16-rounded weights (the weights the
+// values are multiplied by) in all four of its elements, instead of the
+// lane's share of the fp32 weights in l.
+template <int D, int NT, bool MS = false> struct RowState {
   static constexpr int DV = D / 16;
   float mref[NT];       // reference maximum (log2 units), uniform over the row's 4 lanes
+  float nbase[MS ? NT : 1];  // with MS: -mref, or 0 while mref = -inf (the exponent's offset)
   float thr[NT];        // raw-logit threshold: a logit above it calls for a higher mref
-  float l[NT];          // this lane's share of the row sum
+  float l[NT];          // this lane's share of the row sum (without MS)
+  f32x4 lacc[MS ? NT : 1];  // row sums (with MS)
   f32x4 acc[NT][DV];    // O^T accumulators
   __device__ __forceinline__ void init() {
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) {
       mref[nt] = kNegInf;
+      if constexpr (MS) nbase[nt] = 0.f;
       thr[nt] = kNegInf;
       l[nt] = 0.f;
+      if constexpr (MS) lacc[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int t = 0; t < DV; ++t) acc[nt][t] = f32x4{0.f, 0.f, 0.f, 0.f};
     }
@@ -257,8 +265,8 @@ template <int D, int NT> struct RowState {
 // r = head*ntok + token), row r sees keys < rem - (ntok - 1) + r % ntok:
 // the range ends at the last token's limit and earlier tokens stop earlier
 // (ntok = 1 masks keys >= rem).
-template <int D, int NT, typename KOp, typename VOp, typename QOp>
-__device__ __forceinline__ void tile_update(RowState<D, NT>& st, KOp&& k_at, VOp&& vop_at,
+template <int D, int NT, bool MS, typename KOp, typename VOp, typename QOp>
+__device__ __forceinline__ void tile_update(RowState<D, NT, MS>& st, KOp&& k_at, VOp&& vop_at,
                                             QOp&& q_at, int rem, int ntok, float scale_log2,
                                             int lane) {
   constexpr int KS = D / 32;
@@ -267,6 +275,7 @@ __device__ __forceinline__ void tile_update(RowState<D, NT>& st, KOp&& k_at, VOp
   f32x4 sacc[NT][2];
 #pragma unroll
   for (int nt = 0; nt < NT; ++nt) sacc[nt][0] = sacc[nt][1] = f32x4{0.f, 0.f, 0.f, 0.f};
+  if constexpr (MS) __builtin_amdgcn_s_setprio(1);
 #pragma unroll
   for (int s = 0; s < KS; ++s) {
     const u32x4 k0 = k_at(0, s), k1 = k_at(1, s);
@@ -277,6 +286,7 @@ __device__ __forceinline__ void tile_update(RowState<D, NT>& st, KOp&& k_at, VOp
       sacc[nt][1] = mfma_bf16(k1, qo, sacc[nt][1]);
     }
   }
+  if constexpr (MS) __builtin_amdgcn_s_setprio(0);
   // Raw logits; scale_log2 > 0, so maxima can be taken before scaling and
   // the scale folds into the exponent's multiply-add. The reference maximum
   // only has to bound the row's logits to within 2^kRescaleSlack (the same
@@ -315,25 +325,40 @@ __device__ __forceinline__ void tile_update(RowState<D, NT>& st, KOp&& k_at, VOp
       // Rows that do not raise keep alpha = 1 (and never form -inf - -inf).
       const bool raise = tmax > st.mref[nt] + kRescaleSlack;
       const float alpha = raise ? exp2_fast(st.mref[nt] - tmax) : 1.f;  // 0 when mref = -inf
-      st.l[nt] *= alpha;
+      if constexpr (MS)
+        st.lacc[nt] *= alpha;
+      else
+        st.l[nt] *= alpha;
 #pragma unroll
       for (int t = 0; t < DV; ++t) st.acc[nt][t] *= alpha;
       st.mref[nt] = raise ? tmax : st.mref[nt];
+      if constexpr (MS) st.nbase[nt] = st.mref[nt] == kNegInf ? 0.f : -st.mref[nt];
       st.thr[nt] = (st.mref[nt] + kRescaleSlack) / scale_log2;
     }
   }
-  auto weights = [&](int nt) -> u32x4 {  // bf16 P^T operand of query tile nt; adds to l
-    const float nbase = st.mref[nt] == kNegInf ? 0.f : -st.mref[nt];
+  auto weights = [&](int nt) -> u32x4 {  // bf16 P^T operand of query tile nt; adds to the sums
+    // kept in the state with MS; recomputed per tile otherwise (registers)
+    float nbase;
+    if constexpr (MS)
+      nbase = st.nbase[nt];
+    else
+      nbase = st.mref[nt] == kNegInf ? 0.f : -st.mref[nt];
     float pr[8];
 #pragma unroll
     for (int e = 0; e < 8; ++e) pr[e] = exp2_fast(__builtin_fmaf(x[nt][e], scale_log2, nbase));
-    float psum = pr[0];
+    if constexpr (!MS) {
+      float psum = pr[0];
 #pragma unroll
-    for (int e = 1; e < 8; ++e) psum += pr[e];
-    st.l[nt] += psum;
+      for (int e = 1; e < 8; ++e) psum += pr[e];
+      st.l[nt] += psum;
+    }
     u32x4 pb;
 #pragma unroll
     for (int w = 0; w < 4; ++w) pb[w] = pack_bf16(pr[2 * w], pr[2 * w + 1]);
+    if constexpr (MS) {
+      constexpr uint32_t kOnes = 0x3F803F80u;  // two bf16 1.0
+      st.lacc[nt] = mfma_bf16(u32x4{kOnes, kOnes, kOnes, kOnes}, pb, st.lacc[nt]);
+    }
     return pb;
   };
   if constexpr (NT == 2) {
@@ -359,8 +384,10 @@ __device__ __forceinline__ void tile_update(RowState<D, NT>& st, KOp&& k_at, VOp
     for (int t = 0; t < DV; ++t) st.acc[1][t] = mfma_bf16(vo[t], pb1, st.acc[1][t]);
   } else if constexpr (NT == 1) {
     const u32x4 pb = weights(0);
+    if constexpr (MS) __builtin_amdgcn_s_setprio(1);
 #pragma unroll
     for (int t = 0; t < DV; ++t) st.acc[0][t] = mfma_bf16(vop_at(t), pb, st.acc[0][t]);
+    if constexpr (MS) __builtin_amdgcn_s_setprio(0);
   } else {
     // Many query tiles: registers are short, so each V^T operand is formed
     // once and used for every tile.
@@ -487,10 +514,15 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t rows_rsrc(const uint8_t* base,
 }
 
 // Row totals of the per-lane sums (the four lanes of a row share the row).
-template <int D, int NT>
-__device__ __forceinline__ void finish_sums(RowState<D, NT>& st) {
+template <int D, int NT, bool MS>
+__device__ __forceinline__ void finish_sums(RowState<D, NT, MS>& st) {
 #pragma unroll
-  for (int nt = 0; nt < NT; ++nt) st.l[nt] = xor32_sum(xor16_sum(st.l[nt]));
+  for (int nt = 0; nt < NT; ++nt) {
+    if constexpr (MS)
+      st.l[nt] = st.lacc[nt][0];
+    else
+      st.l[nt] = xor32_sum(xor16_sum(st.l[nt]));
+  }
 }
 
 // Write the wave's partials of rows row0 + nt*16 + n < nrows: lane (n, G)
@@ -908,7 +940,7 @@ __device__ __forceinline__ void ctx_large_body(const PartialsParams& P) {
   Stage A, B;
   fetch(A, 0);
   fetch(B, kTileKeys);
-  RowState<D, 1> st;
+  RowState<D, 1, true> st;
   st.init();
   const bool rows = row0 < M;  // wave-uniform: waves past the last row only stage
   stage(A, 0);
