@@ -172,7 +172,9 @@ bifattn_status_t bifattn_plan_get_info(bifattn_plan_t plan, bifattn_plan_info_t 
  * one group once and applies it to all b*p query rows of the group; (b)
  * decode partials: per sample and group over its own Kd/Vd; (c) the combine,
  * which merges the (max, sum, weighted-value) partials of both parts into
- * `out`. On a plan whose path is BIFATTN_PATH_STANDARD it enqueues one
+ * `out`. With many query rows per group (b*(h/g)*n > 64) and a decode cache
+ * of 16 MiB or more, (b) runs on a stream the plan owns, beside (a), and
+ * `stream` waits for it before (c). On a plan whose path is BIFATTN_PATH_STANDARD it enqueues one
  * launch instead: per (sample, group), the context rows then the decode
  * rows in one softmax, written to `out`. Kd, Vd and decode_lens may be NULL only when m_d_max == 0.
  * Errors: EINVAL (null plan or required pointer), EALIGN (q, Kc, Vc, Kd, Vd
@@ -254,7 +256,10 @@ bifattn_status_t bifattn_plan_status(bifattn_plan_t plan, hipStream_t stream);
  * (capacity 0 switches timing off). For BIFATTN_KERNEL_PARTIALS and
  * BIFATTN_KERNEL_COMBINE the launches record the events themselves
  * (hipExtLaunchKernel), so they span the kernels' own execution, from the
- * start of the first launch of the section to the end of its last; for
+ * start of the first launch of the section to the end of its last (where a
+ * plan runs its decode launch on a side stream beside the many-row context
+ * kernel, the partial section is recorded on the call's stream from before
+ * the fork to after the join); for
  * BIFATTN_KERNEL_CALL they are recorded on the stream around the whole
  * call. Timing stops recording when full.
  * Errors: EINVAL (bad kernel id or negative capacity), ENOMEM, EHIP.

@@ -26,6 +26,9 @@ struct bifattn_plan_s {
   int dec_keys = 0, S_d = 0, n_dec_blocks = 0;
   int rep_keys = 0, S_r = 0, n_rep_blocks = 0;
   int fused = 1;
+  int fork = 0;        // many-row path: decode launch on a side stream beside the context kernel
+  hipStream_t side = nullptr;
+  hipEvent_t fork_ev = nullptr, join_ev = nullptr;
   int path = BIFATTN_PATH_BIFURCATED;  // resolved: bifurcated or standard
   int device = 0;
   // workspace
@@ -58,6 +61,15 @@ int env_int(const char* name, int fallback) {
   char* end = nullptr;
   long x = std::strtol(v, &end, 10);
   return (end && *end == 0 && x > 0 && x < (1 << 30)) ? (int)x : fallback;
+}
+
+// A switch from the environment: -1 when unset or not an integer, else its value.
+int env_switch(const char* name) {
+  const char* v = std::getenv(name);
+  if (!v || !*v) return -1;
+  char* end = nullptr;
+  long x = std::strtol(v, &end, 10);
+  return (end && *end == 0 && x >= 0 && x < 16) ? (int)x : -1;
 }
 
 bool aligned(const void* ptr, uintptr_t a) { return ((uintptr_t)ptr & (a - 1)) == 0; }
@@ -104,9 +116,18 @@ bifattn_status_t plan_splits(bifattn_plan_s* P) {
   } else {
     // Many rows: eight-wave work-groups of 128 rows share each staged
     // K_c/V_c tile; about two work-groups per CU (four waves per SIMD).
+    // With a large decode part (16 MiB of decode KV or more) the decode
+    // launch runs on a side stream beside the context kernel, which then
+    // takes about one work-group per CU and leaves the other slot to the
+    // decode work-groups (the context part is bound by the matrix cores, the
+    // decode part by HBM). BIFATTN_FORK=0/1 forces it off/on.
     P->ctx_mode = kCtxLarge;
     P->ctx_row_blocks = (int)ceil_div(M, kLargeRowsPerBlock);
-    int64_t splits = ceil_div(2 * kCUs, (int64_t)d.g * P->ctx_row_blocks);
+    const double dec_bytes = 2.0 * d.b * d.g * (double)d.m_d_max * d.d * kv_bytes(d.kv_type);
+    const int fork_env = env_switch("BIFATTN_FORK");
+    P->fork = d.m_d_max > 0 && (fork_env == -1 ? dec_bytes >= 16.0 * (1 << 20) : fork_env == 1);
+    int64_t splits = ceil_div(env_int("BIFATTN_CTX_WGS", P->fork ? kCUs : 2 * kCUs),
+                              (int64_t)d.g * P->ctx_row_blocks);
     if (splits < 1) splits = 1;
     const int64_t ck = round_up(ceil_div(d.m_c, splits), kTileKeys);
     P->ctx_keys = (int)round_up(env_int("BIFATTN_CTX_KEYS", (int)ck), kTileKeys);
@@ -212,6 +233,13 @@ struct TimedSection {
   LaunchEvents first() const { return LaunchEvents{ev(0), nullptr}; }
   LaunchEvents last() const { return LaunchEvents{nullptr, ev(1)}; }
   LaunchEvents both() const { return LaunchEvents{ev(0), ev(1)}; }
+  // For sections that span streams: the pair recorded on the call's stream.
+  void record_start() {
+    if (on && in_kernel) (void)hipEventRecord(P->events[2 * P->timing_n], stream);
+  }
+  void record_stop() {
+    if (on && in_kernel) (void)hipEventRecord(P->events[2 * P->timing_n + 1], stream);
+  }
   void end() {
     if (on) {
       if (!in_kernel) (void)hipEventRecord(P->events[2 * P->timing_n + 1], stream);
@@ -342,6 +370,14 @@ bifattn_status_t bifattn_plan_create(const bifattn_dims_t* dims, bifattn_plan_t*
     delete P;
     return BIFATTN_EHIP;
   }
+  if (P->fork) {
+    if (hipStreamCreateWithFlags(&P->side, hipStreamNonBlocking) != hipSuccess ||
+        hipEventCreateWithFlags(&P->fork_ev, hipEventDisableTiming) != hipSuccess ||
+        hipEventCreateWithFlags(&P->join_ev, hipEventDisableTiming) != hipSuccess) {
+      (void)hipGetLastError();
+      P->fork = 0;
+    }
+  }
   *plan = P;
   return BIFATTN_OK;
 }
@@ -351,6 +387,9 @@ bifattn_status_t bifattn_plan_destroy(bifattn_plan_t P) {
   bifattn_status_t st = BIFATTN_OK;
   if (hipDeviceSynchronize() != hipSuccess) st = BIFATTN_EHIP;
   free_events(P);
+  if (P->fork_ev) (void)hipEventDestroy(P->fork_ev);
+  if (P->join_ev) (void)hipEventDestroy(P->join_ev);
+  if (P->side) (void)hipStreamDestroy(P->side);
   if (P->ws && hipFree(P->ws) != hipSuccess) st = BIFATTN_EHIP;
   delete P;
   return st;
@@ -413,7 +452,25 @@ bifattn_status_t bifattn_decode_scaled(bifattn_plan_t P, const void* q, const vo
   // Two launches: the first carries the start event and the second the end
   // event, unless there are no decode work-groups (then the first carries both).
   const bool two = P->n_dec_blocks > 0;
-  if (P->ctx_mode == kCtxLarge) {
+  if (P->ctx_mode == kCtxLarge && P->fork && two) {
+    // The decode work-groups on the side stream, beside the many-row context
+    // kernel; the call's stream waits for them before the combine. The timed
+    // section is the call's stream from before the fork to after the join.
+    PartialsParams Kd = K;
+    Kd.n_dec_blocks = P->n_dec_blocks;
+    part.record_start();
+    if (hipEventRecord(P->fork_ev, stream) != hipSuccess ||
+        hipStreamWaitEvent(P->side, P->fork_ev, 0) != hipSuccess)
+      return BIFATTN_EHIP;
+    e = launch_partials(Kd, P->dims.d, kv, kCtxNone, P->dec_tiles, P->side);
+    K.n_ctx_blocks = P->n_ctx_blocks;
+    if (e == hipSuccess) e = launch_ctx_large(K, P->dims.d, kv, stream);
+    if (e == hipSuccess && (hipEventRecord(P->join_ev, P->side) != hipSuccess ||
+                            hipStreamWaitEvent(stream, P->join_ev, 0) != hipSuccess))
+      e = hipErrorUnknown;
+    part.record_stop();
+    K.n_ctx_blocks = 0;
+  } else if (P->ctx_mode == kCtxLarge) {
     // The many-row context kernel, then the decode work-groups.
     K.n_ctx_blocks = P->n_ctx_blocks;
     e = launch_ctx_large(K, P->dims.d, kv, stream, two ? part.first() : part.both());

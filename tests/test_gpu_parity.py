@@ -237,3 +237,20 @@ def test_draft_tokens_masked_tail_and_replicated():
     a = run_decode(x)
     assert np.array_equal(a, run_decode(y))
     assert_parity(run_replicated(x), oracle.attention(**x), "replicated, n = 4")
+
+
+@pytest.mark.parametrize("case", [(40, 32, 1, 128, 2000, 64, 1), (6, 32, 2, 128, 700, 40, 1),
+                                  (8, 32, 32, 128, 900, 120, 4)],
+                         ids=lambda c: "b%d_h%d_g%d_d%d_mc%d_md%d_n%d" % c)
+def test_side_stream_decode(case, monkeypatch):
+    """Many-row plans may run the decode launch on a side stream beside the
+    context kernel (the call's stream waits for it before the combine):
+    forced on and off, the outputs are bitwise equal and match the oracle."""
+    b, h, g, d, m_c, m_d, n = case
+    x = workloads.make_inputs(b, h, g, d, m_c, m_d, seed=1200 + m_c, ragged=True, n=n)
+    outs = []
+    for fork in ("0", "1"):
+        monkeypatch.setenv("BIFATTN_FORK", fork)
+        outs.append(run_decode(x))
+    assert np.array_equal(outs[0], outs[1])
+    _report(f"side stream {case}", *assert_parity(outs[1], oracle.attention(**x), str(case)))
