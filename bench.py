@@ -195,6 +195,35 @@ def summarize_profile(stats_dir: str, fetch_dir: str, write_dir: str, workload: 
     return lines
 
 
+def summarize_stats(stats_dir: str, workload: str, out_dir: str):
+    """Kernel-trace statistics of one rocprofv3 run of this script as a
+    markdown table (profiles/stats_<workload>.md)."""
+    import csv
+    import glob
+    files = glob.glob(os.path.join(stats_dir, "**", "*kernel_stats.csv"), recursive=True)
+    if not files:
+        raise SystemExit(f"no kernel_stats.csv under {stats_dir}")
+    lines = [f"| kernel | calls | avg us | min us | max us | % time |", "|---|---|---|---|---|---|"]
+    for r in csv.DictReader(open(files[0])):
+        lines.append(f"| {r['Name'][:110]} | {r['Calls']} | {float(r['AverageNs']) / 1e3:.2f} | "
+                     f"{float(r['MinNs']) / 1e3:.2f} | {float(r['MaxNs']) / 1e3:.2f} | "
+                     f"{float(r['Percentage']):.2f} |")
+    w = workloads.WORKLOADS[workload]
+    head = [f"# rocprofv3 kernel statistics, {workload}", "",
+            f"b={w.b}, h={w.h}, g={w.g}, d={w.d}, m_c={w.m_c}, m_d={w.m_d_max}, "
+            f"new tokens {w.n}, KV {w.kv}, lengths {'ragged' if w.ragged else 'uniform'}.", "",
+            "Commands (repository root, one MI355X, after `cd /tmp && export TMPDIR=/tmp`; "
+            "`gpurun_out/` is scratch):", "", "```",
+            f"rocprofv3 --kernel-trace --stats -d gpurun_out/st_{workload} -o run --output-format csv "
+            f"-- python -u bench.py --workload {workload} --steps 100 --no-cpu-baseline --no-ablation",
+            f"python bench.py --workload {workload} --summarize-stats gpurun_out/st_{workload} profiles",
+            "```", "", "Every launch of the run (warmup, timed loop, event-timed loop, warm loop).", ""]
+    os.makedirs(out_dir, exist_ok=True)
+    text = "\n".join(head + lines) + "\n"
+    open(os.path.join(out_dir, f"stats_{workload}.md"), "w").write(text)
+    print(text)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -208,7 +237,12 @@ def main():
                     help="first run the 1 GiB copy-equivalent kernel that scales HBM counters")
     ap.add_argument("--summarize-profile", nargs=4, metavar=("STATS", "FETCH", "WRITE", "OUT"),
                     help="summarize rocprofv3 outputs of the workload into OUT")
+    ap.add_argument("--summarize-stats", nargs=2, metavar=("STATS", "OUT"),
+                    help="write the kernel statistics of a rocprofv3 run of the workload into OUT")
     args = ap.parse_args()
+    if args.summarize_stats:
+        summarize_stats(args.summarize_stats[0], args.workload, args.summarize_stats[1])
+        return
     if args.summarize_profile:
         summarize_profile(*args.summarize_profile[:3], args.workload, args.summarize_profile[3],
                           args.warmup, args.steps)
@@ -231,7 +265,7 @@ def main():
     torch.cuda.set_device(0)
     dev0 = to_device(x)
     # Rotate over device copies so each step's KV is cold in the Infinity Cache.
-    copies = max(3, -(-4 * MALL_BYTES // B_kv))
+    copies = min(512, max(3, -(-4 * MALL_BYTES // B_kv)))
     devs = [dev0] + [{k: v.clone() for k, v in dev0.items()} for _ in range(copies - 1)]
     out = torch.empty(tuple(x["q"].shape), dtype=torch.float32, device="cuda")
     plan = bif.Plan(w.b, w.h, w.g, w.d, w.m_c, w.m_d_max, n=w.n, kv=w.kv)
