@@ -871,7 +871,7 @@ __device__ __forceinline__ int xcd_logical(int bid, int n) {
 // in), and all eight waves read it. Each wave stages one eighth of a tile:
 // one K operand (d = 128; the first four waves for d = 64) and one 32-bit
 // word of half of the V^T operands, widening 8-bit codes to bf16 on the way. Tiles are double-buffered in LDS with
-// one barrier per tile, and fetched two tiles ahead into two rotating
+// one barrier per tile, and fetched three tiles ahead into three rotating
 // register sets. Q^T operands stay in registers. Row blocks of one key
 // chunk are scheduled on the same XCD so that they share its L2.
 template <int D, typename KV>
@@ -937,22 +937,25 @@ __device__ __forceinline__ void ctx_large_body(const PartialsParams& P) {
     const int i = row / p, jp = row - i * p;
     return P.q + ((size_t)i * h + (size_t)gam * p + jp) * D;
   }, P.q_sign, lane);
-  Stage A, B;
-  fetch(A, 0);
-  fetch(B, kTileKeys);
+  constexpr int T = kTileKeys;
+  Stage S0, S1, S2;
+  fetch(S0, 0);
+  fetch(S1, T);
+  fetch(S2, 2 * T);
   RowState<D, 1, true> st;
   st.init();
   const bool rows = row0 < M;  // wave-uniform: waves past the last row only stage
-  stage(A, 0);
+  stage(S0, 0);
   __syncthreads();
-  // Tile `key` (in LDS buffer buf) is consumed while the next tile is in
-  // flight in one register set and the one after that is issued into the
-  // other; fetches past the chunk are unconditional (they read zeros), so
-  // every wait covers exactly one set. The loop runs while two more tiles
-  // follow (a single exit at the bottom keeps the waits exact); the last one
-  // or two tiles are the tail.
-  auto step = [&](int key, int buf, Stage& next, Stage& spare, bool stage_next) {
-    fetch(spare, key + 2 * kTileKeys);
+  // Tile `key` (in LDS buffer buf) is consumed while the next two tiles are
+  // in flight in two register sets and the one after them is issued into
+  // the third (the set tile `key` came from); fetches past the chunk are
+  // unconditional (they read zeros), so every wait covers exactly one set.
+  // The loop runs six tiles per turn while a seventh follows (a single exit
+  // at the bottom keeps the waits exact); the last one to six tiles are the
+  // tail.
+  auto step = [&](int key, int buf, Stage& spare, Stage& next, bool stage_next) {
+    fetch(spare, key + 3 * T);
     if (rows)
       tile_update<D, 1>(st, [&](int a, int ss) { return slot(buf, a * KS + ss)[lane]; },
                         [&](int t) { return slot(buf, KOPS + t)[lane]; },
@@ -966,13 +969,20 @@ __device__ __forceinline__ void ctx_large_body(const PartialsParams& P) {
     }
   };
   int key = 0;
-  for (; key + 2 * kTileKeys < nkeys; key += 2 * kTileKeys) {
-    step(key, 0, B, A, true);
-    step(key + kTileKeys, 1, A, B, true);
+  for (; key + 6 * T < nkeys; key += 6 * T) {
+    step(key, 0, S0, S1, true);
+    step(key + T, 1, S1, S2, true);
+    step(key + 2 * T, 0, S2, S0, true);
+    step(key + 3 * T, 1, S0, S1, true);
+    step(key + 4 * T, 0, S1, S2, true);
+    step(key + 5 * T, 1, S2, S0, true);
   }
-  const bool two = key + kTileKeys < nkeys;
-  step(key, 0, B, A, two);
-  if (two) step(key + kTileKeys, 1, A, B, false);
+  step(key, 0, S0, S1, key + T < nkeys);
+  if (key + T < nkeys) step(key + T, 1, S1, S2, key + 2 * T < nkeys);
+  if (key + 2 * T < nkeys) step(key + 2 * T, 0, S2, S0, key + 3 * T < nkeys);
+  if (key + 3 * T < nkeys) step(key + 3 * T, 1, S0, S1, key + 4 * T < nkeys);
+  if (key + 4 * T < nkeys) step(key + 4 * T, 0, S1, S2, key + 5 * T < nkeys);
+  if (key + 5 * T < nkeys) step(key + 5 * T, 1, S2, S0, false);
 
   finish_sums(st);
   const int row = row0 + r;
