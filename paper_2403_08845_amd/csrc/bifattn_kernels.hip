@@ -114,6 +114,13 @@ __device__ __forceinline__ int wave_id() {
   return __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
 }
 
+// Byte offsets into a buffer resource are formed in 32-bit unsigned
+// arithmetic: prefetches past the end of a cache near the 2^31-byte limit may
+// wrap, which is well defined here and lands outside the resource's range
+// (or inside it, on bytes that are never consumed), where a raw buffer load
+// returns zeros or valid memory and never faults.
+__device__ __forceinline__ int boff(uint32_t x) { return __builtin_bit_cast(int, x); }
+
 // N bytes a lane loads with one buffer instruction, and 32-bit word w of them.
 template <int N> struct Raw;
 template <> struct Raw<16> {
@@ -453,14 +460,15 @@ template <int D, typename KV> struct TileRegs {
 
   __device__ __forceinline__ void load(__amdgpu_buffer_rsrc_t rk, __amdgpu_buffer_rsrc_t rv,
                                        int key0, int lane) {
-    const int koff = (key0 + lane / CPR) * RB + (lane % CPR) * 16;
+    const uint32_t koff = (uint32_t)(key0 + lane / CPR) * RB + (uint32_t)(lane % CPR) * 16;
 #pragma unroll
     for (int e = 0; e < KI; ++e)
-      kraw[e] = __builtin_amdgcn_raw_buffer_load_b128(rk, koff + e * RPI * RB, 0, 0);
+      kraw[e] = __builtin_amdgcn_raw_buffer_load_b128(rk, boff(koff + (uint32_t)(e * RPI * RB)), 0,
+                                                      0);
     const int c = lane & 15, G = lane >> 4;
-    const int voff = (key0 + G) * RB + DV * c * ES;
+    const uint32_t voff = (uint32_t)(key0 + G) * RB + (uint32_t)(DV * c * ES);
 #pragma unroll
-    for (int e = 0; e < 8; ++e) vrow[e] = VR::load(rv, voff + 4 * e * RB);
+    for (int e = 0; e < 8; ++e) vrow[e] = VR::load(rv, boff(voff + (uint32_t)(4 * e * RB)));
   }
   // Write the K rows, as bf16, into this wave's LDS tile (32*d*2 bytes).
   // Lanes read each other's rows afterwards; a wave executes its LDS
@@ -914,10 +922,12 @@ __device__ __forceinline__ void ctx_large_body(const PartialsParams& P) {
     VH v[2];
   };
   auto fetch = [&](Stage& g, int key0) {  // keys past the chunk load as zero
-    if (has_k) g.k = KR::load(rk, (key0 + qk_key(ka, r)) * RB + (kss * 32 + G * 8) * ES);
+    if (has_k)
+      g.k = KR::load(rk, boff((uint32_t)(key0 + qk_key(ka, r)) * RB + (uint32_t)((kss * 32 + G * 8) * ES)));
 #pragma unroll
     for (int c = 0; c < 2; ++c)
-      g.v[c] = VR::load(rv, (key0 + 4 * (2 * vw + c) + G) * RB + (DV * r + vh * HW) * ES);
+      g.v[c] = VR::load(rv, boff((uint32_t)(key0 + 4 * (2 * vw + c) + G) * RB +
+                                 (uint32_t)((DV * r + vh * HW) * ES)));
   };
   auto stage = [&](const Stage& g, int buf) {
     if (has_k) slot(buf, wave)[lane] = Widen8<KV>::run(g.k);

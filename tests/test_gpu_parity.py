@@ -254,3 +254,41 @@ def test_side_stream_decode(case, monkeypatch):
         outs.append(run_decode(x))
     assert np.array_equal(outs[0], outs[1])
     _report(f"side stream {case}", *assert_parity(outs[1], oracle.attention(**x), str(case)))
+
+
+def test_largest_context_rows_are_addressed():
+    """A context near the per-cache limit ((m_c + m_d_max) * d * 2 bytes just
+    under 2^31; prefetches past its end wrap their 32-bit offsets): every
+    logit is 0 except one key at the far end of the context, whose logit is
+    ~30, so each output row is that key's value row up to its softmax weight
+    1 / (1 + (N - 1) e^-logit) (a property that holds at any size; the
+    oracle would need gigabytes per row)."""
+    import torch
+    b, h, g, d, m_d = 2, 4, 1, 128, 64
+    m_c = (2 ** 31 - 1) // (d * 2) - m_d - 1
+    with bif.Plan(b, h, g, d, m_c, m_d) as plan:
+        assert plan.info()["path"] == bif.PATHS["bifurcated"]
+        print(f"[case] m_c={m_c} plan={plan.info()}", flush=True)
+        bf = torch.bfloat16
+        q = torch.zeros(b, h, d, dtype=bf, device="cuda")
+        q[..., 0] = 1.0
+        Kc = torch.zeros(g, m_c, d, dtype=bf, device="cuda")
+        Vc = torch.zeros(g, m_c, d, dtype=bf, device="cuda")
+        Kd = torch.zeros(b, g, m_d, d, dtype=bf, device="cuda")
+        Vd = torch.zeros(b, g, m_d, d, dtype=bf, device="cuda")
+        lens = torch.tensor([m_d, 17], dtype=torch.int32, device="cuda")
+        far = m_c - 1
+        Kc[0, far, 0] = 340.0                      # exact in bf16
+        v = (torch.arange(d, dtype=torch.float32) - 64.0) / 64.0  # exact in bf16
+        Vc[0, far] = v.to(bf).cuda()
+        out = torch.empty(b, h, d, dtype=torch.float32, device="cuda")
+        bif.bifattn_decode(plan, q, Kc, Vc, Kd, Vd, lens, out)
+        assert bif.bifattn_plan_status(plan) == bif.OK
+        got = out.cpu().double().numpy()
+    z = 340.0 / np.sqrt(d)
+    for i, L in enumerate((m_d, 17)):
+        w = 1.0 / (1.0 + (m_c + L - 1) * np.exp(-z))
+        exp = w * v.double().numpy()
+        err = float(np.max(np.abs(got[i] - exp[None, :])))
+        print(f"[parity] far key, sample {i}: max_abs={err:.3e}", flush=True)
+        assert err <= 1e-5, err
