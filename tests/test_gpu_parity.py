@@ -292,3 +292,19 @@ def test_largest_context_rows_are_addressed():
         err = float(np.max(np.abs(got[i] - exp[None, :])))
         print(f"[parity] far key, sample {i}: max_abs={err:.3e}", flush=True)
         assert err <= 1e-5, err
+
+
+@pytest.mark.parametrize("case", [(3, 8, 8, 128, 1000, 77), (7, 32, 8, 128, 700, 129),
+                                  (2, 4, 2, 128, 96, 0)],
+                         ids=lambda c: "b%d_h%d_g%d_d%d_mc%d_md%d" % c)
+def test_split_launch_equals_fused(case, monkeypatch):
+    """The few-row context work-groups and the decode work-groups in two
+    launches (BIFATTN_LAUNCH=2) instead of one: the same work-groups, so the
+    outputs are bitwise equal, and they match the oracle."""
+    b, h, g, d, m_c, m_d = case
+    x = workloads.make_inputs(b, h, g, d, m_c, m_d, seed=1300 + m_c, ragged=True)
+    fused = run_decode(x)
+    monkeypatch.setenv("BIFATTN_LAUNCH", "2")
+    split = run_decode(x)
+    assert np.array_equal(fused, split)
+    _report(f"split launch {case}", *assert_parity(split, oracle.attention(**x), str(case)))
