@@ -213,10 +213,10 @@ def summarize_stats(stats_dir: str, workload: str, out_dir: str):
             f"b={w.b}, h={w.h}, g={w.g}, d={w.d}, m_c={w.m_c}, m_d={w.m_d_max}, "
             f"new tokens {w.n}, KV {w.kv}, lengths {'ragged' if w.ragged else 'uniform'}.", "",
             "Commands (repository root, one MI355X, after `cd /tmp && export TMPDIR=/tmp`; "
-            "`gpurun_out/` is scratch):", "", "```",
-            f"rocprofv3 --kernel-trace --stats -d gpurun_out/st_{workload} -o run --output-format csv "
+            f"`{stats_dir}` holds the raw output):", "", "```",
+            f"rocprofv3 --kernel-trace --stats -d {stats_dir} -o run --output-format csv "
             f"-- python -u bench.py --workload {workload} --steps 100 --no-cpu-baseline --no-ablation",
-            f"python bench.py --workload {workload} --summarize-stats gpurun_out/st_{workload} profiles",
+            f"python bench.py --workload {workload} --summarize-stats {stats_dir} {out_dir}",
             "```", "", "Every launch of the run (warmup, timed loop, event-timed loop, warm loop).", ""]
     os.makedirs(out_dir, exist_ok=True)
     text = "\n".join(head + lines) + "\n"
@@ -249,7 +249,8 @@ def main():
         return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU: the bifurcated decode step runs on a single MI355X "
-              "(see DESIGN.md for how it would shard); --gpus must be 1.", file=sys.stderr)
+              "(the sample axis and the KV groups are the axes a multi-GPU layout would split); "
+              "--gpus must be 1.", file=sys.stderr)
         sys.exit(2)
 
     import torch

@@ -66,6 +66,11 @@ def lib() -> ctypes.CDLL:
         if not os.path.exists(LIB_PATH):
             raise RuntimeError(f"{LIB_PATH} is missing: build it with "
                                "`python -m paper_2403_08845_amd.build`")
+        # One HIP runtime per process: torch's is loaded first, so that the
+        # library's libamdhip64 dependency resolves to it (the tensors and
+        # streams handed over are torch's); a second runtime loaded beside it
+        # keeps the first from opening the device.
+        import torch  # noqa: F401
         L = ctypes.CDLL(LIB_PATH)
         vp, i32, st = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int
         L.bifattn_plan_create.argtypes = [ctypes.POINTER(Dims), ctypes.POINTER(vp)]
