@@ -177,9 +177,13 @@ bifattn_status_t bifattn_plan_get_info(bifattn_plan_t plan, bifattn_plan_info_t 
  * `stream` waits for it before (c). On a plan whose path is BIFATTN_PATH_STANDARD it enqueues one
  * launch instead: per (sample, group), the context rows then the decode
  * rows in one softmax, written to `out`. Kd, Vd and decode_lens may be NULL only when m_d_max == 0.
- * Errors: EINVAL (null plan or required pointer), EALIGN (q, Kc, Vc, Kd, Vd
- * or out not 16-byte aligned, decode_lens not 4-byte aligned), EHIP (launch
- * failure). Device-side length errors: see bifattn_plan_status.
+ * All tensors live on the plan's device (the one current at plan creation)
+ * and `stream` belongs to it (NULL: the null stream of the current device,
+ * which must then be the plan's).
+ * Errors: EINVAL (null plan or required pointer, a stream of another
+ * device), EALIGN (q, Kc, Vc, Kd, Vd or out not 16-byte aligned, decode_lens
+ * not 4-byte aligned), EHIP (launch failure). Device-side length errors: see
+ * bifattn_plan_status.
  */
 bifattn_status_t bifattn_decode(bifattn_plan_t plan, const void *q, const void *Kc,
                                 const void *Vc, const void *Kd, const void *Vd,
@@ -235,8 +239,9 @@ bifattn_status_t bifattn_decode_replicated_scaled(bifattn_plan_t plan, const voi
  * `stream`. Rows that would pass m_d_max are dropped (the length stops at
  * m_d_max), a length outside [0, m_d_max] is clamped first; both raise the
  * device-side flag that bifattn_plan_status reports as BIFATTN_ELENS.
- * Errors: EINVAL (null argument, m_d_max = 0), EALIGN (a tensor not 16-byte
- * aligned, decode_lens not 4-byte aligned), EHIP (launch failure).
+ * Errors: EINVAL (null argument, m_d_max = 0, a stream of another device
+ * than the plan's), EALIGN (a tensor not 16-byte aligned, decode_lens not
+ * 4-byte aligned), EHIP (launch failure).
  */
 bifattn_status_t bifattn_append_kv(bifattn_plan_t plan, const void *k_new, const void *v_new,
                                    void *Kd, void *Vd, int32_t *decode_lens, hipStream_t stream);

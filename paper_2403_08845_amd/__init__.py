@@ -123,6 +123,10 @@ class Plan:
         _check(lib().bifattn_plan_create(ctypes.byref(self.dims), ctypes.byref(handle)),
                "bifattn_plan_create")
         self.handle = handle
+        import torch
+        #: The device the plan's workspace lives on (current at creation):
+        #: every tensor and the stream of a call must belong to it.
+        self.device = torch.device("cuda", torch.cuda.current_device())
 
     def close(self):
         if getattr(self, "handle", None) is not None and self.handle.value:
@@ -160,10 +164,12 @@ def bifattn_plan_get_info(plan: Plan) -> dict:
     return plan.info()
 
 
-def _stream_ptr(stream):
+def _stream_ptr(stream, device=None):
+    """A torch stream, a raw hipStream_t (int), or None for torch's current
+    stream of `device`."""
     if stream is None:
         import torch
-        stream = torch.cuda.current_stream()
+        stream = torch.cuda.current_stream(device)
     return ctypes.c_void_p(stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream))
 
 
@@ -228,7 +234,7 @@ def bifattn_decode_scaled(plan: Plan, q, Kc, Vc, Kd, Vd, decode_lens, k_scale, v
     the GPU, or None for 1)."""
     import torch
     D = plan.dims
-    dev = q.device
+    dev = plan.device
     cd = _cache_dtypes(plan)
     args = [
         _tensor(q, _query_shapes(D), torch.bfloat16, dev, "q"),
@@ -240,7 +246,7 @@ def bifattn_decode_scaled(plan: Plan, q, Kc, Vc, Kd, Vd, decode_lens, k_scale, v
         *_scales(plan, k_scale, v_scale, dev),
         _tensor(out, [tuple(q.shape)], torch.float32, dev, "out"),
     ]
-    _check(lib().bifattn_decode_scaled(plan.handle, *args, _stream_ptr(stream)),
+    _check(lib().bifattn_decode_scaled(plan.handle, *args, _stream_ptr(stream, dev)),
            "bifattn_decode_scaled")
 
 
@@ -255,7 +261,7 @@ def bifattn_decode_replicated_scaled(plan: Plan, q, K, V, decode_lens, k_scale, 
     """The replicated ablation with per-group scales."""
     import torch
     D = plan.dims
-    dev = q.device
+    dev = plan.device
     rows = D.m_c + D.m_d_max
     cd = _cache_dtypes(plan)
     args = [
@@ -266,7 +272,7 @@ def bifattn_decode_replicated_scaled(plan: Plan, q, K, V, decode_lens, k_scale, 
         *_scales(plan, k_scale, v_scale, dev),
         _tensor(out, [tuple(q.shape)], torch.float32, dev, "out"),
     ]
-    _check(lib().bifattn_decode_replicated_scaled(plan.handle, *args, _stream_ptr(stream)),
+    _check(lib().bifattn_decode_replicated_scaled(plan.handle, *args, _stream_ptr(stream, dev)),
            "bifattn_decode_replicated_scaled")
 
 
@@ -277,7 +283,7 @@ def bifattn_append_kv(plan: Plan, k_new, v_new, Kd, Vd, decode_lens, stream=None
     advances by n."""
     import torch
     D = plan.dims
-    dev = Kd.device
+    dev = plan.device
     n = max(1, D.n)
     cd = _cache_dtypes(plan)
     args = [
@@ -287,12 +293,13 @@ def bifattn_append_kv(plan: Plan, k_new, v_new, Kd, Vd, decode_lens, stream=None
         _tensor(Vd, (D.b, D.g, D.m_d_max, D.d), cd, dev, "Vd"),
         _tensor(decode_lens, (D.b,), torch.int32, dev, "decode_lens"),
     ]
-    _check(lib().bifattn_append_kv(plan.handle, *args, _stream_ptr(stream)), "bifattn_append_kv")
+    _check(lib().bifattn_append_kv(plan.handle, *args, _stream_ptr(stream, dev)),
+           "bifattn_append_kv")
 
 
 def bifattn_plan_status(plan: Plan, stream=None) -> int:
     """Synchronise the stream; return OK, ELENS or ESCALE (and clear the flags)."""
-    st = lib().bifattn_plan_status(plan.handle, _stream_ptr(stream))
+    st = lib().bifattn_plan_status(plan.handle, _stream_ptr(stream, plan.device))
     if st not in (OK, ELENS, ESCALE):
         raise BifattnError(st, "bifattn_plan_status")
     return st

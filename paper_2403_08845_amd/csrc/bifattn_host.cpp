@@ -74,6 +74,26 @@ int env_switch(const char* name) {
 
 bool aligned(const void* ptr, uintptr_t a) { return ((uintptr_t)ptr & (a - 1)) == 0; }
 
+// The plan's workspace lives on the device that was current at its creation:
+// a call is accepted only on a stream of that device (the null stream: the
+// current device), so that no kernel runs on one GPU against another GPU's
+// workspace.
+bool on_plan_device(const bifattn_plan_s* P, hipStream_t stream) {
+  int dev = -1;
+  if (stream) {
+    hipDevice_t d = -1;
+    if (hipStreamGetDevice(stream, &d) != hipSuccess) {
+      (void)hipGetLastError();
+      return false;
+    }
+    dev = d;
+  } else if (hipGetDevice(&dev) != hipSuccess) {
+    (void)hipGetLastError();
+    return false;
+  }
+  return dev == P->device;
+}
+
 // Keys one decode work-group reads: the whole decode cache up to 1024 keys
 // (each work-group writes partials for p rows per wave, so short chunks
 // multiply that traffic, and ragged lengths leave short chunks nearly empty),
@@ -414,7 +434,7 @@ bifattn_status_t bifattn_decode_scaled(bifattn_plan_t P, const void* q, const vo
                                        const void* Vc, const void* Kd, const void* Vd,
                                        const int32_t* decode_lens, const float* k_scale,
                                        const float* v_scale, float* out, hipStream_t stream) {
-  if (!P || !q || !Kc || !Vc || !out) return BIFATTN_EINVAL;
+  if (!P || !q || !Kc || !Vc || !out || !on_plan_device(P, stream)) return BIFATTN_EINVAL;
   if (!aligned(k_scale, 4) || !aligned(v_scale, 4)) return BIFATTN_EALIGN;
   const bool has_dec = P->dims.m_d_max > 0;
   if (has_dec && (!Kd || !Vd || !decode_lens)) return BIFATTN_EINVAL;
@@ -513,7 +533,7 @@ bifattn_status_t bifattn_decode_replicated_scaled(bifattn_plan_t P, const void* 
                                                   const void* V_, const int32_t* decode_lens,
                                                   const float* k_scale, const float* v_scale,
                                                   float* out, hipStream_t stream) {
-  if (!P || !q || !K_ || !V_ || !out) return BIFATTN_EINVAL;
+  if (!P || !q || !K_ || !V_ || !out || !on_plan_device(P, stream)) return BIFATTN_EINVAL;
   if (!aligned(k_scale, 4) || !aligned(v_scale, 4)) return BIFATTN_EALIGN;
   const bool has_dec = P->dims.m_d_max > 0;
   if (has_dec && !decode_lens) return BIFATTN_EINVAL;
@@ -556,7 +576,8 @@ bifattn_status_t bifattn_decode_replicated(bifattn_plan_t P, const void* q, cons
 
 bifattn_status_t bifattn_append_kv(bifattn_plan_t P, const void* k_new, const void* v_new,
                                    void* Kd, void* Vd, int32_t* decode_lens, hipStream_t stream) {
-  if (!P || !k_new || !v_new || !Kd || !Vd || !decode_lens || P->dims.m_d_max < 1)
+  if (!P || !k_new || !v_new || !Kd || !Vd || !decode_lens || P->dims.m_d_max < 1 ||
+      !on_plan_device(P, stream))
     return BIFATTN_EINVAL;
   if (!aligned(k_new, 16) || !aligned(v_new, 16) || !aligned(Kd, 16) || !aligned(Vd, 16) ||
       !aligned(decode_lens, 4))

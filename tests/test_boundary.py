@@ -91,6 +91,7 @@ def test_binding_refuses_host_tensors_before_any_call():
     class FakePlan:
         dims = bif.Dims(2, 4, 2, 64, 32, 8, 0.0)
         handle = ctypes.c_void_p(0)
+        device = torch.device("cuda", 0)
 
     q = torch.zeros(2, 4, 64, dtype=torch.bfloat16)
     with pytest.raises(ValueError):
