@@ -44,7 +44,8 @@
  *
  * Ownership and concurrency: the caller owns every tensor and the stream;
  * the library never frees caller memory. A plan owns its workspace (allocated
- * at create, freed at destroy). Calls are asynchronous on the given stream
+ * at create, freed at destroy) on the device current at create; its calls
+ * take that device's memory and streams. Calls are asynchronous on the given stream
  * (no host synchronisation) except bifattn_plan_status and
  * bifattn_plan_read_timing. One plan must not be used by two calls that may
  * run concurrently (they share the workspace). Results are bitwise
