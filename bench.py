@@ -18,8 +18,11 @@ measured time per step, in GB/s. ``roofline`` reports the partial kernel
 HIP events that the library's launch records with the kernel itself
 (hipExtLaunchKernel start/stop events, the span a kernel trace shows), over a
 second pass of the same steps (kept out of the value loop, where no events
-are recorded). ``cpu_baseline`` times the fp64 CPU oracle on the host on the same
-workload. ``ablation`` times the replicated-KV kernel (no bifurcation).
+are recorded). ``extra.call_us`` gives the 10th, 50th and 90th percentiles of
+single calls timed with events on the call's stream around each call.
+``cpu_baseline`` times the fp64 CPU oracle on the host on the same workload
+(all threads; ``single_thread``: one thread over the first samples; the CPU
+model). ``ablation`` times the replicated-KV kernel (no bifurcation).
 """
 from __future__ import annotations
 
@@ -27,6 +30,7 @@ import argparse
 import hashlib
 import json
 import os
+import platform
 import sys
 import time
 
@@ -84,23 +88,48 @@ def to_device(x):
     return out
 
 
-def cpu_baseline(x, w, min_seconds):
+def cpu_model() -> str:
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return platform.processor() or "unknown"
+
+
+def cpu_baseline(x, w, min_seconds, single_thread=True):
     """The fp64 oracle on the host's cores, repeated over the whole workload
-    until min_seconds have elapsed (at least once)."""
+    until min_seconds have elapsed (at least once); then one pass on a single
+    thread, over the sample rows the same number of seconds allow."""
     import oracle
     threads = oracle.max_threads()
     reps, t0 = 0, time.perf_counter()
     while True:
-        oracle.attention(**x)
+        oracle.attention(**x, nthreads=threads)
         reps += 1
         el = time.perf_counter() - t0
         if el >= min_seconds:
             break
     per = el / reps
     B = workloads.kv_bytes(w.g, w.d, w.m_c, x["lens"], w.kv)
-    return {"value": round(B / per / 1e9, 4), "unit": "GB/s", "cores": threads, "kind": "oracle",
-            "sample": f"whole {w.name} step (b={w.b}), fp64, repeated {reps}x over {el:.1f} s; "
-                      f"{per * 1e3:.1f} ms per step"}
+    rec = {"value": round(B / per / 1e9, 4), "unit": "GB/s", "cores": threads, "kind": "oracle",
+           "sample": f"whole {w.name} step (b={w.b}), fp64, repeated {reps}x over {el:.1f} s; "
+                     f"{per * 1e3:.1f} ms per step",
+           "cpu_model": cpu_model()}
+    if single_thread:
+        # Single thread over the first samples: their rows cost about
+        # per * threads seconds per step, so take a share that fits.
+        nb = max(1, min(w.b, int(w.b * min_seconds / max(per * threads, 1e-9))))
+        xs = workloads.first_samples(x, nb)
+        t0 = time.perf_counter()
+        oracle.attention(**xs, nthreads=1)
+        el1 = time.perf_counter() - t0
+        B1 = workloads.kv_bytes(w.g, w.d, w.m_c, xs["lens"], w.kv)
+        rec["single_thread"] = {"value": round(B1 / el1 / 1e9, 4), "unit": "GB/s",
+                                "sample": f"first {nb} of {w.b} samples, one pass, {el1:.1f} s"}
+        oracle.attention(**workloads.first_samples(x, 1), nthreads=threads)  # thread count back
+    return rec
 
 
 COPY_BYTES = 1 << 30
@@ -311,6 +340,20 @@ def main():
     log(f"[bench] timed {args.steps} steps: {ms_per_step * 1e3:.2f} us/step, "
         f"partial kernel {part_us:.2f} us (event loop {evt_loop_us:.2f} us/step)")
 
+    # Per-call latency distribution: events on the call's stream around each
+    # call (the whole call: partial and combine launches).
+    starts = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+    ends = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    for k in range(args.steps):
+        starts[k].record()
+        step(k)
+        ends[k].record()
+    torch.cuda.synchronize()
+    call_us = np.sort([a.elapsed_time(b) * 1e3 for a, b in zip(starts, ends)])
+    call_stats = {q: round(float(np.percentile(call_us, pct)), 3)
+                  for q, pct in (("p10", 10), ("median", 50), ("p90", 90))}
+
     # Warm variant (same inputs every step: KV partly served by the Infinity Cache).
     torch.cuda.synchronize()
     t0 = time.perf_counter()
@@ -320,6 +363,7 @@ def main():
     warm_us = (time.perf_counter() - t0) * 1e6 / args.steps
 
     extra = {"warm_us_per_step": round(warm_us, 3), "event_loop_us_per_step": round(evt_loop_us, 3),
+             "call_us": call_stats,
              "plan": info, "input_copies": copies,
              "kv_bytes_per_step": B_kv, "flops_per_step": flops}
 

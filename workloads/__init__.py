@@ -186,6 +186,14 @@ def make_workload_inputs(w: Workload, *, seed=None, poison_tail=False):
                        poison_tail=poison_tail, n=w.n, kv=w.kv)
 
 
+def first_samples(x, nb):
+    """The inputs of the first nb samples (the shared context unchanged)."""
+    y = dict(x)
+    for k in ("q", "Kd", "Vd", "lens"):
+        y[k] = np.ascontiguousarray(x[k][:nb])
+    return y
+
+
 def kv_bytes(g, d, m_c, lens, kv="bf16") -> int:
     """Algorithmic KV bytes of one bifurcated step: one copy of context K and
     V plus every sample's valid decode K and V (Section 4.3), at the cache's
