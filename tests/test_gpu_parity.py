@@ -245,15 +245,21 @@ def test_draft_tokens_masked_tail_and_replicated():
 def test_side_stream_decode(case, monkeypatch):
     """Many-row plans may run the decode launch on a side stream beside the
     context kernel (the call's stream waits for it before the combine):
-    forced on and off, the outputs are bitwise equal and match the oracle."""
+    forced on and off, both outputs match the oracle, and they are bitwise
+    equal when the two plans split the context alike."""
     b, h, g, d, m_c, m_d, n = case
     x = workloads.make_inputs(b, h, g, d, m_c, m_d, seed=1200 + m_c, ragged=True, n=n)
-    outs = []
+    ref = oracle.attention(**x)
+    runs = []
     for fork in ("0", "1"):
         monkeypatch.setenv("BIFATTN_FORK", fork)
-        outs.append(run_decode(x))
-    assert np.array_equal(outs[0], outs[1])
-    _report(f"side stream {case}", *assert_parity(outs[1], oracle.attention(**x), str(case)))
+        with bif.Plan(b, h, g, d, m_c, m_d, n=n) as plan:
+            splits = plan.info()["ctx_splits"]
+            out = run_decode(x, plan=plan)
+        _report(f"side stream {case} fork={fork}", *assert_parity(out, ref, f"{case} fork={fork}"))
+        runs.append((splits, out))
+    if runs[0][0] == runs[1][0]:
+        assert np.array_equal(runs[0][1], runs[1][1])
 
 
 def test_largest_context_rows_are_addressed():
