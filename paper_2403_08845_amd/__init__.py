@@ -164,33 +164,46 @@ def bifattn_plan_get_info(plan: Plan) -> dict:
     return plan.info()
 
 
+def _torch():
+    import torch
+    return torch
+
+
 def _stream_ptr(stream, device=None):
     """A torch stream, a raw hipStream_t (int), or None for torch's current
     stream of `device`."""
     if stream is None:
-        import torch
+        torch = _torch()
+        raw = getattr(torch._C, "_cuda_getCurrentRawStream", None)
+        if raw is not None:
+            return ctypes.c_void_p(raw(device.index if device is not None
+                                       else torch.cuda.current_device()))
         stream = torch.cuda.current_stream(device)
     return ctypes.c_void_p(stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream))
 
 
 def _tensor(t, shape, dtype, device, name):
-    """shape: one shape, or a list of accepted shapes; dtype: one dtype or a
-    tuple of accepted dtypes."""
-    import torch
+    """The device pointer of torch tensor t after checking it. shape: one
+    shape, or a list of accepted shapes; dtype: one dtype or a tuple of
+    accepted dtypes; device: the plan's device. The common case passes one
+    combined test; a failing tensor gets the specific error."""
+    dtypes = dtype if isinstance(dtype, tuple) else (dtype,)
+    shapes = shape if isinstance(shape, list) else [shape]
+    torch = _torch()
+    if (isinstance(t, torch.Tensor) and t.dtype in dtypes and t.device == device
+            and t.shape in shapes and t.is_contiguous()):
+        return ctypes.c_void_p(t.data_ptr())
     if not isinstance(t, torch.Tensor):
         raise TypeError(f"{name} must be a torch.Tensor")
-    dtypes = dtype if isinstance(dtype, tuple) else (dtype,)
     if t.dtype not in dtypes:
         raise TypeError(f"{name} must be {' or '.join(map(str, dtypes))}, got {t.dtype}")
-    shapes = [tuple(x) for x in shape] if isinstance(shape, list) else [tuple(shape)]
+    shapes = [tuple(x) for x in shapes]
     if tuple(t.shape) not in shapes:
         raise ValueError(f"{name} must have shape {' or '.join(map(str, shapes))}, "
                          f"got {tuple(t.shape)}")
-    if not t.is_cuda or (device is not None and t.device != device):
-        raise ValueError(f"{name} must live on {device or 'the GPU'}")
-    if not t.is_contiguous():
-        raise ValueError(f"{name} must be contiguous")
-    return ctypes.c_void_p(t.data_ptr())
+    if not t.is_cuda or t.device != device:
+        raise ValueError(f"{name} must live on {device}")
+    raise ValueError(f"{name} must be contiguous")
 
 
 def _cache_dtypes(plan):
