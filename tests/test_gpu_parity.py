@@ -81,6 +81,23 @@ def test_workload_sampled_rows(name):
     _report(name, *assert_parity(got, ref, name))
 
 
+@pytest.mark.parametrize("case", [(2048, 8, 1, 64, 300, 20), (512, 64, 64, 128, 100, 40)],
+                         ids=lambda c: "b%d_h%d_g%d_d%d_mc%d_md%d" % c)
+def test_large_batches_sampled_rows(case):
+    """Very many samples: 16384 query rows in 128 row blocks on one group, and
+    32768 (sample, group) units of a 64-head MHA layer; every output finite,
+    sampled rows (first, last, longest and shortest samples, random ones)
+    against the oracle row by row."""
+    b, h, g, d, m_c, m_d = case
+    x = workloads.make_inputs(b, h, g, d, m_c, m_d, seed=1700 + b, ragged=True)
+    print(f"[case] large batch {case}", flush=True)
+    out = run_decode(x)
+    assert np.all(np.isfinite(out))
+    ri, rj = sample_rows(b, h, x["lens"], 64, seed=1701)
+    ref = oracle.attention_rows(**x, rows_i=ri, rows_j=rj)
+    _report(f"large batch {case}", *assert_parity(out[ri, rj], ref, str(case)))
+
+
 def test_masked_tail_is_never_read():
     """NaN in decode rows past each sample's length changes no output bit."""
     b, h, g, d, m_c, m_d = 6, 16, 4, 128, 300, 150
