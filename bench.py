@@ -54,7 +54,14 @@ def log(msg):
 
 
 def kernel_source_hash() -> str:
-    return hashlib.sha256(open(KERNEL_SRC, "rb").read()).hexdigest()[:16]
+    """Hash of the kernel source's code: line comments, trailing blanks and
+    empty lines removed, so that editing a comment keeps a counter record."""
+    code = []
+    for line in open(KERNEL_SRC, encoding="utf-8"):
+        line = line.split("//", 1)[0].rstrip()
+        if line:
+            code.append(line)
+    return hashlib.sha256("\n".join(code).encode()).hexdigest()[:16]
 
 
 def measured_traffic(workload: str):
@@ -246,7 +253,7 @@ def summarize_stats(stats_dir: str, workload: str, out_dir: str):
             f"rocprofv3 --kernel-trace --stats -d {stats_dir} -o run --output-format csv "
             f"-- python -u bench.py --workload {workload} --steps 100 --no-cpu-baseline --no-ablation",
             f"python bench.py --workload {workload} --summarize-stats {stats_dir} {out_dir}",
-            "```", "", "Every launch of the run (warmup, timed loop, event-timed loop, warm loop).", ""]
+            "```", "", "Every launch of the run (warmup, timed loop, event-timed loop, per-call loop, warm loop).", ""]
     os.makedirs(out_dir, exist_ok=True)
     text = "\n".join(head + lines) + "\n"
     open(os.path.join(out_dir, f"stats_{workload}.md"), "w").write(text)

@@ -15,14 +15,17 @@
 //   A (16 x 32): lane holds A[n][8G .. 8G+7]
 //   B (32 x 16): lane holds B[8G .. 8G+7][n]
 //   C (16 x 16): lane holds C[4G .. 4G+3][n]
-// Logits are computed transposed, S^T = K Q^T, so that a lane's 8 logits are
-// one query row n and keys 8G..8G+7 -- exactly the B operand of the value
-// product O^T = V^T P^T. Within a 32-key tile, QK sub-tile a (0/1) puts key
-// 8*(r>>2) + 4a + (r&3) on MFMA row r; the accumulator of sub-tile a then
-// holds keys 8G+4a .. 8G+4a+3. V^T operands are built from value rows by a
-// per-lane 16-bit transpose; dimension block t of the output holds dims
-// DV*r + t (DV = d/16), so lane (n, G) ends up owning output dims
-// [4*DV*G, 4*DV*G + 4*DV) of query row n.
+// Logits are computed transposed, S^T = K Q^T: query rows are the MFMA
+// columns, so all logits a lane holds belong to one query row n. Within a
+// 32-key tile, row r of QK sub-tile a (0/1) is tile key 16a + 4(r&3) + (r>>2)
+// (qk_key); the accumulators of the two sub-tiles then give lane (n, G) the
+// logits of keys 4e + G, e = 0..7. After the softmax those 8 weights, packed
+// to bf16, are the lane's B operand of the value product O^T = V^T P^T, whose
+// k-slot (G, e) is key 4e + G; the lane builds its V^T operand from the same
+// value rows 4e + G (a 16-bit transpose inside the lane), so both operands
+// agree on the key of every k-slot. Dimension block t of the output holds
+// dims DV*m + t on MFMA row m (DV = d/16), so lane (n, G) ends up owning
+// output dims [4*DV*G, 4*DV*G + 4*DV) of query row n.
 //
 // Caches may hold 8-bit codes (OCP fp8 E4M3 or int8, one scale per KV group
 // for keys and one for values): every code value is exactly a bf16 value, so

@@ -34,6 +34,17 @@ def test_traffic_record_follows_the_kernel_source(tmp_path, monkeypatch):
     assert bench.measured_traffic("missing") is None
 
 
+def test_kernel_hash_ignores_comments(tmp_path, monkeypatch):
+    src = tmp_path / "k.hip"
+    src.write_text("// header\nint a = 1;  // trailing\n\n__global__ void k() {}\n")
+    monkeypatch.setattr(bench, "KERNEL_SRC", str(src))
+    h = bench.kernel_source_hash()
+    src.write_text("// another header\nint a = 1;\n__global__ void k() {}  // note\n")
+    assert bench.kernel_source_hash() == h
+    src.write_text("int a = 2;\n__global__ void k() {}\n")
+    assert bench.kernel_source_hash() != h
+
+
 def _write_csv(path, header, rows):
     os.makedirs(os.path.dirname(path), exist_ok=True)
     with open(path, "w", newline="") as f:
