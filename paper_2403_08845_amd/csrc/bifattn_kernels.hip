@@ -124,36 +124,48 @@ __device__ __forceinline__ int wave_id() {
 // returns zeros or valid memory and never faults.
 __device__ __forceinline__ int boff(uint32_t x) { return __builtin_bit_cast(int, x); }
 
-// N bytes a lane loads with one buffer instruction, and 32-bit word w of them.
+// Cache policy of the loads that stream a cache: every byte of the decode
+// cache, and of the context on the few-row path, is read exactly once per
+// step, so those loads are non-temporal (the nt bit: streamed past the caches
+// instead of displacing lines). Measured on MI355X over 402 MB of loads-only
+// regions: 6.0 TB/s with the default policy, 6.7 TB/s with nt.
+constexpr int kAuxStream = 2;
+
+// N bytes a lane loads with one buffer instruction (cache policy AUX), and
+// 32-bit word w of them.
 template <int N> struct Raw;
 template <> struct Raw<16> {
   typedef u32x4 type;
+  template <int AUX = 0>
   static __device__ __forceinline__ type load(__amdgpu_buffer_rsrc_t r, int off) {
-    return __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0);
+    return __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, AUX);
   }
   static __device__ __forceinline__ type zero() { return u32x4{0, 0, 0, 0}; }
   static __device__ __forceinline__ uint32_t word(const type& v, int w) { return v[w]; }
 };
 template <> struct Raw<8> {
   typedef u32x2 type;
+  template <int AUX = 0>
   static __device__ __forceinline__ type load(__amdgpu_buffer_rsrc_t r, int off) {
-    return __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, 0);
+    return __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, AUX);
   }
   static __device__ __forceinline__ type zero() { return u32x2{0, 0}; }
   static __device__ __forceinline__ uint32_t word(const type& v, int w) { return v[w]; }
 };
 template <> struct Raw<4> {
   typedef uint32_t type;
+  template <int AUX = 0>
   static __device__ __forceinline__ type load(__amdgpu_buffer_rsrc_t r, int off) {
-    return __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, 0);
+    return __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, AUX);
   }
   static __device__ __forceinline__ type zero() { return 0u; }
   static __device__ __forceinline__ uint32_t word(const type& v, int) { return v; }
 };
 template <> struct Raw<2> {
   typedef uint32_t type;
+  template <int AUX = 0>
   static __device__ __forceinline__ type load(__amdgpu_buffer_rsrc_t r, int off) {
-    return __builtin_amdgcn_raw_buffer_load_b16(r, off, 0, 0);
+    return __builtin_amdgcn_raw_buffer_load_b16(r, off, 0, AUX);
   }
   static __device__ __forceinline__ type zero() { return 0u; }
   static __device__ __forceinline__ uint32_t word(const type& v, int) { return v; }
@@ -461,17 +473,19 @@ template <int D, typename KV> struct TileRegs {
     return row * BPR + (chunk ^ swz);
   }
 
+  // AUX: cache policy (streamed, read-once rows by default).
+  template <int AUX = kAuxStream>
   __device__ __forceinline__ void load(__amdgpu_buffer_rsrc_t rk, __amdgpu_buffer_rsrc_t rv,
                                        int key0, int lane) {
     const uint32_t koff = (uint32_t)(key0 + lane / CPR) * RB + (uint32_t)(lane % CPR) * 16;
 #pragma unroll
     for (int e = 0; e < KI; ++e)
-      kraw[e] = __builtin_amdgcn_raw_buffer_load_b128(rk, boff(koff + (uint32_t)(e * RPI * RB)), 0,
-                                                      0);
+      kraw[e] = Raw<16>::load<AUX>(rk, boff(koff + (uint32_t)(e * RPI * RB)));
     const int c = lane & 15, G = lane >> 4;
     const uint32_t voff = (uint32_t)(key0 + G) * RB + (uint32_t)(DV * c * ES);
 #pragma unroll
-    for (int e = 0; e < 8; ++e) vrow[e] = VR::load(rv, boff(voff + (uint32_t)(4 * e * RB)));
+    for (int e = 0; e < 8; ++e)
+      vrow[e] = VR::template load<AUX>(rv, boff(voff + (uint32_t)(4 * e * RB)));
   }
   // Write the K rows, as bf16, into this wave's LDS tile (32*d*2 bytes).
   // Lanes read each other's rows afterwards; a wave executes its LDS
@@ -573,7 +587,7 @@ __device__ __forceinline__ void store_partials(RowState<D, NT>& st, int nrows, f
 // lanes]; kl: this wave's LDS K tile (32*d*2 bytes). kend: the end of the
 // sequence the tokens' causal limits count from (ntok tokens per unit; k1
 // when ntok = 1).
-template <int D, int NT, typename KV>
+template <int D, int NT, typename KV, int AUX = kAuxStream>
 __device__ __forceinline__ void stream_keys(RowState<D, NT>& st, const u32x4* qw, u32x4* kl,
                                             __amdgpu_buffer_rsrc_t rk, __amdgpu_buffer_rsrc_t rv,
                                             TileRegs<D, KV>& A, int k0, int k1, int kend, int stride,
@@ -592,7 +606,7 @@ __device__ __forceinline__ void stream_keys(RowState<D, NT>& st, const u32x4* qw
   // flight lets each wait cover only the tile being consumed.
   for (int key = k0;; key += 2 * stride) {
     const int key1 = key + stride;
-    B.load(rk, rv, key1, lane);
+    B.template load<AUX>(rk, rv, key1, lane);
     const int nv0 = min(kTileKeys, k1 - key);
     if (nv0 < kTileKeys) A.mask_v(nv0, lane);
     A.stage_k(kl, lane);
@@ -600,7 +614,7 @@ __device__ __forceinline__ void stream_keys(RowState<D, NT>& st, const u32x4* qw
                        scale_log2, lane);
     if (key1 >= k1) break;
     const int key2 = key1 + stride;
-    A.load(rk, rv, key2, lane);
+    A.template load<AUX>(rk, rv, key2, lane);
     const int nv1 = min(kTileKeys, k1 - key1);
     if (nv1 < kTileKeys) B.mask_v(nv1, lane);
     B.stage_k(kl, lane);
@@ -802,7 +816,9 @@ __device__ void standard_block(const PartialsParams& P, int blk, int wave, int l
   const int k0 = wave * kTileKeys;
   constexpr int stride = kWaves * kTileKeys;
   TileRegs<D, KV> A;
-  A.load(rkc, rvc, k0, lane);  // first context tile in flight during the set-up
+  // The context rows are read once per sample here: loaded with the default
+  // cache policy, so that the group's other samples may find them cached.
+  A.template load<0>(rkc, rvc, k0, lane);  // first context tile in flight during the set-up
   const int p = P.p;
   const uint16_t* qbase = P.q + ((size_t)i * P.h + (size_t)gam * p) * D;
   stage_q<D, NT>(qw, [&](int r) -> const uint16_t* { return r < p ? qbase + (size_t)r * D : nullptr; },
@@ -812,7 +828,7 @@ __device__ void standard_block(const PartialsParams& P, int blk, int wave, int l
   st.init();
   // Context rows: visible to every token (a causal limit only applies among
   // the decode rows).
-  stream_keys<D, NT, KV>(st, qw, kl, rkc, rvc, A, k0, P.m_c, P.m_c, stride, 1, sl2, lane);
+  stream_keys<D, NT, KV, 0>(st, qw, kl, rkc, rvc, A, k0, P.m_c, P.m_c, stride, 1, sl2, lane);
   const int len = clamp_len(P.lens, i, P.m_d_max);
   if (len > 0) {  // wave-uniform
     const size_t cache = (size_t)(i * P.g + gam) * P.m_d_max * RB;
