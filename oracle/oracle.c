@@ -104,26 +104,48 @@ double oracle_code_value(int kv_type, int code) {
 }
 
 /* One output row (sample i, head j): the textbook two-pass softmax over the
- * materialised per-sample cache of the head's group. */
+ * materialised per-sample cache of the head's group. Every sum runs
+ * sequentially in index order: each logit over u, Z over t, and each output
+ * element over t. The loops are arranged so that several independent sums
+ * advance together (four keys' logits at a time; all d output elements per
+ * key), which leaves each sum's order, and so its value, unchanged. */
 static void attend_row(int d, int m_i, double scale, const double *qrow,
                        const double *K, const double *V, double *s, double *o) {
   double mu = -INFINITY;
-  for (int t = 0; t < m_i; ++t) {
+  int t = 0;
+  for (; t + 4 <= m_i; t += 4) {
+    const double *k0 = K + (size_t)t * d;
+    double a0 = 0.0, a1 = 0.0, a2 = 0.0, a3 = 0.0;
+    for (int u = 0; u < d; ++u) {
+      a0 += qrow[u] * k0[u];
+      a1 += qrow[u] * k0[d + u];
+      a2 += qrow[u] * k0[2 * d + u];
+      a3 += qrow[u] * k0[3 * d + u];
+    }
+    s[t] = scale * a0;
+    s[t + 1] = scale * a1;
+    s[t + 2] = scale * a2;
+    s[t + 3] = scale * a3;
+  }
+  for (; t < m_i; ++t) {
     double acc = 0.0;
     for (int u = 0; u < d; ++u) acc += qrow[u] * K[(size_t)t * d + u];
     s[t] = scale * acc;
-    if (s[t] > mu) mu = s[t];
   }
+  for (t = 0; t < m_i; ++t)
+    if (s[t] > mu) mu = s[t];
   double Z = 0.0;
-  for (int t = 0; t < m_i; ++t) {
+  for (t = 0; t < m_i; ++t) {
     s[t] = exp(s[t] - mu);
     Z += s[t];
   }
-  for (int u = 0; u < d; ++u) {
-    double acc = 0.0;
-    for (int t = 0; t < m_i; ++t) acc += s[t] * V[(size_t)t * d + u];
-    o[u] = acc / Z;
+  for (int u = 0; u < d; ++u) o[u] = 0.0;
+  for (t = 0; t < m_i; ++t) {
+    const double w = s[t];
+    const double *vr = V + (size_t)t * d;
+    for (int u = 0; u < d; ++u) o[u] += w * vr[u];
   }
+  for (int u = 0; u < d; ++u) o[u] /= Z;
 }
 
 /* Decode rows that query token r (of n) of a sample with len valid rows sees. */
