@@ -286,11 +286,13 @@ template <int D, int NT, bool MS = false> struct RowState {
 // to the end of the range. With ntok tokens per (sample, group) unit (rows
 // r = head*ntok + token), row r sees keys < rem - (ntok - 1) + r % ntok:
 // the range ends at the last token's limit and earlier tokens stop earlier
-// (ntok = 1 masks keys >= rem).
+// (ntok = 1 masks keys >= rem). Keys below `vfloor` (counted from the tile's
+// first key, like rem) are seen by every row whatever its causal limit: the
+// context rows that precede the decode rows in a replicated cache.
 template <int D, int NT, bool MS, typename KOp, typename VOp, typename QOp>
 __device__ __forceinline__ void tile_update(RowState<D, NT, MS>& st, KOp&& k_at, VOp&& vop_at,
-                                            QOp&& q_at, int rem, int ntok, float scale_log2,
-                                            int lane) {
+                                            QOp&& q_at, int rem, int ntok, int vfloor,
+                                            float scale_log2, int lane) {
   constexpr int KS = D / 32;
   constexpr int DV = D / 16;
   const int G = lane >> 4;
@@ -329,7 +331,9 @@ __device__ __forceinline__ void tile_update(RowState<D, NT, MS>& st, KOp&& k_at,
       // The bound passes through readfirstlane (convergent), so the compiler
       // cannot hoist these compares out of the branch into every full tile.
       const int nv = __builtin_amdgcn_readfirstlane(rem) - (ntok - 1);
-      const int lim = ntok == 1 ? nv : nv + (nt * kRowsPerTile + (lane & 15)) % ntok;
+      const int lim = ntok == 1 ? nv
+                                : max(nv + (nt * kRowsPerTile + (lane & 15)) % ntok,
+                                      __builtin_amdgcn_readfirstlane(vfloor));
 #pragma unroll
       for (int e = 0; e < 8; ++e)
         if (4 * e + G >= lim) x[nt][e] = kNegInf;
@@ -586,12 +590,12 @@ __device__ __forceinline__ void store_partials(RowState<D, NT>& st, int nrows, f
 // one window of it. qw: this wave's Q^T operands in LDS, [NT][d/32][64
 // lanes]; kl: this wave's LDS K tile (32*d*2 bytes). kend: the end of the
 // sequence the tokens' causal limits count from (ntok tokens per unit; k1
-// when ntok = 1).
+// when ntok = 1); keys below vis0 are seen by every token.
 template <int D, int NT, typename KV, int AUX = kAuxStream>
 __device__ __forceinline__ void stream_keys(RowState<D, NT>& st, const u32x4* qw, u32x4* kl,
                                             __amdgpu_buffer_rsrc_t rk, __amdgpu_buffer_rsrc_t rv,
                                             TileRegs<D, KV>& A, int k0, int k1, int kend, int stride,
-                                            int ntok, float scale_log2, int lane) {
+                                            int ntok, int vis0, float scale_log2, int lane) {
   constexpr int KS = D / 32;
   if (k0 >= k1) return;
   // Volatile: a real LDS read at each use, not a register copy kept alive
@@ -611,7 +615,7 @@ __device__ __forceinline__ void stream_keys(RowState<D, NT>& st, const u32x4* qw
     if (nv0 < kTileKeys) A.mask_v(nv0, lane);
     A.stage_k(kl, lane);
     tile_update<D, NT>(st, k_at, [&](int t) { return A.vop(t); }, q_at, kend - key, ntok,
-                       scale_log2, lane);
+                       vis0 - key, scale_log2, lane);
     if (key1 >= k1) break;
     const int key2 = key1 + stride;
     A.template load<AUX>(rk, rv, key2, lane);
@@ -619,7 +623,7 @@ __device__ __forceinline__ void stream_keys(RowState<D, NT>& st, const u32x4* qw
     if (nv1 < kTileKeys) B.mask_v(nv1, lane);
     B.stage_k(kl, lane);
     tile_update<D, NT>(st, k_at, [&](int t) { return B.vop(t); }, q_at, kend - key1, ntok,
-                       scale_log2, lane);
+                       vis0 - key1, scale_log2, lane);
     if (key2 >= k1) break;
   }
 }
@@ -685,7 +689,7 @@ __device__ void decode_block(const PartialsParams& P, int blk, int wave, int lan
   // Keys [k0, k1) of this chunk; the causal limits of the tokens count from
   // the end of the sequence (total), which may lie in a later chunk.
   stream_keys<D, NT, KV>(st, qw, kl, rk, rv, A, k0, k1, total, kWaves * kTileKeys, P.ntok,
-                         unit_scale_log2(P, gam), lane);
+                         P.len_offset, unit_scale_log2(P, gam), lane);
   const size_t prow = ((size_t)blk * kWaves + wave) * P.p;
   store_partials<D, NT>(st, p, P.dec_acc + prow * D, P.dec_ml + prow, lane);
 }
@@ -787,7 +791,7 @@ __device__ void ctx_small_block(const PartialsParams& P, int blk, int wave, int 
   RowState<D, NT> st;
   st.init();
   stream_keys<D, NT, KV>(st, qw, kl, rk, rv, A, k0, P.m_c, P.m_c, P.S_c * kWaves * kTileKeys, 1,
-                         unit_scale_log2(P, gam), lane);
+                         0, unit_scale_log2(P, gam), lane);
   const size_t prow = (size_t)blk * P.M;
   __syncthreads();  // the merge buffer overlays the waves' K tiles
   merge_waves_and_store<D, NT>(st, merge_lds, M, P.ctx_acc + prow * D, P.ctx_ml + prow, wave, lane);
@@ -828,14 +832,14 @@ __device__ void standard_block(const PartialsParams& P, int blk, int wave, int l
   st.init();
   // Context rows: visible to every token (a causal limit only applies among
   // the decode rows).
-  stream_keys<D, NT, KV, 0>(st, qw, kl, rkc, rvc, A, k0, P.m_c, P.m_c, stride, 1, sl2, lane);
+  stream_keys<D, NT, KV, 0>(st, qw, kl, rkc, rvc, A, k0, P.m_c, P.m_c, stride, 1, 0, sl2, lane);
   const int len = clamp_len(P.lens, i, P.m_d_max);
   if (len > 0) {  // wave-uniform
     const size_t cache = (size_t)(i * P.g + gam) * P.m_d_max * RB;
     const __amdgpu_buffer_rsrc_t rkd = rows_rsrc(P.Kd + cache, len, RB);
     const __amdgpu_buffer_rsrc_t rvd = rows_rsrc(P.Vd + cache, len, RB);
     A.load(rkd, rvd, k0, lane);
-    stream_keys<D, NT, KV>(st, qw, kl, rkd, rvd, A, k0, len, len, stride, P.ntok, sl2, lane);
+    stream_keys<D, NT, KV>(st, qw, kl, rkd, rvd, A, k0, len, len, stride, P.ntok, 0, sl2, lane);
   }
   __syncthreads();  // the merge buffer overlays the waves' K tiles
   merge_waves<D, NT>(st, merge_lds, wave, lane);
@@ -988,8 +992,8 @@ __device__ __forceinline__ void ctx_large_body(const PartialsParams& P) {
     if (rows)
       tile_update<D, 1>(st, [&](int a, int ss) { return slot(buf, a * KS + ss)[lane]; },
                         [&](int t) { return slot(buf, KOPS + t)[lane]; },
-                        [&](int, int ss) { return qop[0][ss]; }, nkeys - key, 1, scale_log2,
-                        lane);
+                        [&](int, int ss) { return qop[0][ss]; }, nkeys - key, 1, 0,
+                        scale_log2, lane);
     if (stage_next) {
       // The other buffer was last read in the previous step, before the
       // barrier that ended it.

@@ -12,15 +12,40 @@ error <= 2^-9 each, independent across keys). The output is a weighted mean
 of value rows with random signs, so those roundings perturb it by about
 2^-9/sqrt(3) ~ 1.1e-3 of its own norm (measured: 1.1e-3 to 1.7e-3 relative
 L2 on every workload); fp32 summation adds orders of magnitude less. The
-gate allows 5e-3 relative L2. Per entry the same rounding is bounded by
-2^-9 * max_t |v_t| (~1e-2 for N(0,1) values), but few-key rows with O(1)
-outputs reach ~2e-3 in practice, so the max-abs gate is 5e-3.
+gate allows 5e-3 relative L2.
+
+Max-abs gate, split by how many keys a row sees. Per entry the same rounding
+is bounded by 2^-9 * max_t |v_t| (~1e-2 for N(0,1) values), reached only when
+one weight carries the entry. Rows over long sequences average thousands of
+independently rounded weights (measured max-abs on the five workloads:
+0.8e-4 to 7.6e-4), so the gate there is 2e-3. Two kinds of rows come closer
+to the per-entry bound and get 5e-3 (measured up to 3.6e-3):
+  * few keys: some row sees fewer than FEW_KEYS keys (a single context key,
+    short contexts with several tokens), so single weights are O(0.1-1);
+  * sharpened softmax: 8-bit caches, whose per-group key scales make some
+    groups' logits up to 2x larger than the bf16 workloads'.
+Tests that sharpen the softmax further on purpose (key scales up to 8x) may
+pass the contract bound itself; the relative-L2 gate is never raised.
 """
 import numpy as np
 
 CONTRACT_MAX_ABS = 1e-2
-GATE_MAX_ABS = 5e-3
+GATE_MAX_ABS = 2e-3
+GATE_MAX_ABS_FEW_KEYS = 5e-3
 GATE_REL_L2 = 5e-3
+FEW_KEYS = 256
+
+
+def gate_max_abs_for(x):
+    """The max-abs gate for the rows of problem x (a make_inputs dict)."""
+    q = np.asarray(x["q"])
+    n = 1 if q.ndim == 3 else q.shape[2]
+    m_c = np.asarray(x["Kc"]).shape[1]
+    lens = np.asarray(x["lens"])
+    min_keys = m_c + max(0, int(lens.min()) - n + 1) if lens.size else m_c
+    if min_keys < FEW_KEYS or x.get("kv", "bf16") != "bf16":
+        return GATE_MAX_ABS_FEW_KEYS
+    return GATE_MAX_ABS
 
 
 def gate_errors(out, ref):
@@ -32,14 +57,18 @@ def gate_errors(out, ref):
     return max_abs, rel_l2
 
 
-def assert_parity(out, ref, what="", gate_max_abs=GATE_MAX_ABS):
-    """gate_max_abs: a test whose softmax is much sharper than the workloads'
-    (a few bf16-rounded weights then make up an output entry) may raise the
-    max-abs gate up to the contract, never the relative-L2 gate."""
+def assert_parity(out, ref, what="", gate_max_abs=None, x=None):
+    """The gate is gate_max_abs_for(x) when the problem x is given, else
+    GATE_MAX_ABS; gate_max_abs overrides it (a test whose softmax is much
+    sharper than the workloads' may raise it up to the contract, never the
+    relative-L2 gate)."""
+    if gate_max_abs is None:
+        gate_max_abs = GATE_MAX_ABS if x is None else gate_max_abs_for(x)
     assert gate_max_abs <= CONTRACT_MAX_ABS
     out = np.asarray(out, np.float64)
     assert np.all(np.isfinite(out)), f"{what}: non-finite GPU output"
     max_abs, rel_l2 = gate_errors(out, ref)
+    print(f"[gate] {what}: max_abs={max_abs:.3e} rel_l2={rel_l2:.3e}", flush=True)
     assert max_abs <= CONTRACT_MAX_ABS, f"{what}: max abs {max_abs:.3e} breaks the 1e-2 contract"
     assert max_abs <= gate_max_abs and rel_l2 <= GATE_REL_L2, \
         f"{what}: max abs {max_abs:.3e} / rel L2 {rel_l2:.3e} outside the gate " \

@@ -78,8 +78,8 @@ def test_generation_loop(case):
             Vd_host[:, :, lens_host[0]:lens_host[0] + n] = v_new
             lens_host += n
             if step % 5 == 0 or step == m_d // n - 1:
-                ref = oracle.attention(q=q, Kc=x["Kc"], Vc=x["Vc"], Kd=Kd_host, Vd=Vd_host,
-                                       lens=lens_host)
-                assert_parity(out.cpu().double().numpy(), ref, f"{case} step {step}")
+                y = dict(q=q, Kc=x["Kc"], Vc=x["Vc"], Kd=Kd_host, Vd=Vd_host, lens=lens_host)
+                ref = oracle.attention(**y)
+                assert_parity(out.cpu().double().numpy(), ref, f"{case} step {step}", x=y)
         assert bif.bifattn_plan_status(plan) == bif.OK
     assert np.array_equal(dev["lens"].cpu().numpy(), lens_host)

@@ -82,7 +82,7 @@ def test_every_key_code(kv):
     print(f"[case] {kv} key table", flush=True)
     out = run_decode(x, scale=0.5)
     ref = oracle.attention(**x, scale=0.5)
-    _report(f"{kv} key table", *assert_parity(out, ref, f"{kv} key table"))
+    _report(f"{kv} key table", *assert_parity(out, ref, f"{kv} key table", x=x))
 
 
 # (b, h, g, d, m_c, m_d_max, n, ragged): few-row and many-row context paths,
@@ -107,7 +107,7 @@ def test_small_shapes_full_output(kv, case):
     print(f"[case] {kv} {case} lens={x['lens'].tolist()[:8]}", flush=True)
     out = run_decode(x)
     ref = oracle.attention(**x)
-    _report(f"{kv} {case}", *assert_parity(out, ref, f"{kv} {case}"))
+    _report(f"{kv} {case}", *assert_parity(out, ref, f"{kv} {case}", x=x))
 
 
 @pytest.mark.parametrize("kv", KVS)
@@ -152,7 +152,7 @@ def test_replicated_ablation(kv):
     x = workloads.make_inputs(3, 16, 4, 128, 700, 90, seed=950, ragged=True, kv=kv)
     out = run_replicated(x)
     ref = oracle.attention(**x)
-    _report(f"{kv} replicated", *assert_parity(out, ref, f"{kv} replicated"))
+    _report(f"{kv} replicated", *assert_parity(out, ref, f"{kv} replicated", x=x))
 
 
 @pytest.mark.parametrize("bad", [0.0, -1.0, float("nan"), float("inf"), 1e-40])
@@ -213,5 +213,5 @@ def test_generation_loop_with_codes(kv):
             got = out.cpu().double().numpy()
             u = _value_units(y)
             _report(f"{kv} loop step {step}",
-                    *assert_parity(got / u, ref / u, f"{kv} loop step {step}"))
+                    *assert_parity(got / u, ref / u, f"{kv} loop step {step}", x=y))
         assert bif.bifattn_plan_status(plan) == bif.OK

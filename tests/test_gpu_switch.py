@@ -59,7 +59,7 @@ def test_standard_path_full_output(case):
     print(f"[case] standard {case} lens={x['lens'].tolist()[:8]}", flush=True)
     out = run_path(x, "standard")
     ref = oracle.attention(**x)
-    _report(f"standard {case}", *assert_parity(out, ref, f"standard {case}"))
+    _report(f"standard {case}", *assert_parity(out, ref, f"standard {case}", x=x))
 
 
 def test_standard_path_poisoned_tail_and_flags():
@@ -73,7 +73,7 @@ def test_standard_path_poisoned_tail_and_flags():
     z["lens"][2] = 10 ** 6
     out = run_path(z, "standard", expect=bif.ELENS)
     z["lens"][2] = 150
-    assert_parity(out, oracle.attention(**z), "clamped length")
+    assert_parity(out, oracle.attention(**z), "clamped length", x=z)
     w8 = workloads.make_inputs(*args, seed=1111, ragged=True, kv="fp8_e4m3")
     w8["v_scale"] = w8["v_scale"].copy()
     w8["v_scale"][3] = -1.0
@@ -101,4 +101,4 @@ def test_paths_agree_on_the_workloads():
         x = workloads.make_inputs(*shape, seed=1120, ragged=True)
         ref = oracle.attention(**x)
         for path in ("bifurcated", "standard", "auto"):
-            _report(f"{name} {path}", *assert_parity(run_path(x, path), ref, f"{name} {path}"))
+            _report(f"{name} {path}", *assert_parity(run_path(x, path), ref, f"{name} {path}", x=x))
