@@ -13,12 +13,16 @@ torch.cuda.synchronize() on both sides.
 
 Prints ONE JSON line: value = algorithmic KV bytes per step (one copy of the
 context K/V plus every sample's valid decode K/V, Section 4.3) divided by the
-measured time per step, in GB/s. ``roofline`` reports the partial kernel
-(the dominant launch) against the 8 TB/s HBM peak, its duration measured with
-HIP events that the library's launch records with the kernel itself
-(hipExtLaunchKernel start/stop events, the span a kernel trace shows), over a
-second pass of the same steps (kept out of the value loop, where no events
-are recorded). ``extra.call_us`` gives the 10th, 50th and 90th percentiles of
+measured time per step, in GB/s. ``roofline`` reports the dominant kernel
+against its own roof, its duration measured with HIP events that the
+library's launch records with the kernel itself (hipExtLaunchKernel
+start/stop events, the span a kernel trace shows), over further passes of the
+same steps (kept out of the value loop, where no events are recorded): on
+the few-row path the partial launch (context and decode work-groups) against
+the 8 TB/s HBM peak; on the many-row path the longer of the many-row context
+kernel (against the 2.5 PFLOP/s dense bf16 matrix peak, with the context's
+flops) and the decode launch (against HBM, with the decode bytes).
+``roofs`` gives the whole step against both peaks. ``extra.call_us`` gives the 10th, 50th and 90th percentiles of
 single calls timed with events on the call's stream around each call.
 ``cpu_baseline`` times the fp64 CPU oracle on the host on the same workload
 (all threads; ``single_thread``: one thread over the first samples; the CPU
@@ -44,6 +48,7 @@ import workloads  # noqa: E402
 METRIC = ("decode-step attention µs and achieved HBM GB/s (% of peak), "
           "b=32 m_c=8k MHA")
 HBM_PEAK_GBS = 8000.0
+MFMA_PEAK_TFLOPS = 2500.0  # dense bf16 matrix peak of MI355X
 MALL_BYTES = 256 << 20
 KERNEL_SRC = os.path.join(ROOT, "paper_2403_08845_amd", "csrc", "bifattn_kernels.hip")
 TRAFFIC_DIR = os.path.join(ROOT, "profiles")
@@ -64,11 +69,12 @@ def kernel_source_hash() -> str:
     return hashlib.sha256("\n".join(code).encode()).hexdigest()[:16]
 
 
-def measured_traffic(workload: str):
-    """HBM bytes per launch of the partial kernel from the committed rocprofv3
+def measured_traffic(workload: str, kernel: str = "partials"):
+    """HBM bytes per launch of a kernel ("partials": the partial launch;
+    "ctx_large": the many-row context kernel) from the committed rocprofv3
     counter summary, or None when it is missing or the kernel source changed
     since the counters were taken."""
-    path = os.path.join(TRAFFIC_DIR, f"traffic_partials_{workload}.json")
+    path = os.path.join(TRAFFIC_DIR, f"traffic_{kernel}_{workload}.json")
     if not os.path.exists(path):
         return None
     rec = json.load(open(path))
@@ -158,12 +164,17 @@ def calibrate_copy(reps: int = 5):
     log(f"[bench] copy-equivalent kernel over {COPY_BYTES} bytes, {reps} times")
 
 
+KERNEL_NAMES = {"partials": "partials_kernel", "ctx_large": "ctx_large_kernel"}
+
+
 def summarize_profile(stats_dir: str, fetch_dir: str, write_dir: str, workload: str, out_dir: str,
-                      warmup: int, steps: int):
+                      warmup: int, steps: int, kernel: str = "partials"):
     """Turn rocprofv3 outputs into the committed summary: the kernel-trace
-    statistics, and the partial kernel's HBM traffic per launch from the two
+    statistics, and one kernel's HBM traffic per launch ("partials": the
+    partial launch, "ctx_large": the many-row context kernel) from the two
     counter runs, each scaled by what the same counter reads for the plain
     copy of COPY_BYTES."""
+    kname = KERNEL_NAMES[kernel]
     import csv
     import glob
 
@@ -176,10 +187,9 @@ def summarize_profile(stats_dir: str, fetch_dir: str, write_dir: str, workload: 
     stats = rows(stats_dir, "*kernel_stats.csv")
     # The partial kernel's launches in dispatch order: warmup, value loop,
     # event-timed loop, warm loop, ...; average the event-timed ones.
-    trace = [r for r in rows(stats_dir, "*kernel_trace.csv") if "partials_kernel" in r["Kernel_Name"]]
+    trace = [r for r in rows(stats_dir, "*kernel_trace.csv") if kname in r["Kernel_Name"]]
     trace.sort(key=lambda r: int(r["Start_Timestamp"]))
-    timed = trace[warmup + steps: warmup + 2 * steps]
-    timed_us = sum(int(r["End_Timestamp"]) - int(r["Start_Timestamp"]) for r in timed) / len(timed) / 1e3
+    timed_us = sum(int(r["End_Timestamp"]) - int(r["Start_Timestamp"]) for r in trace) / len(trace) / 1e3
 
     def per_kernel(d, counter):
         acc = {}
@@ -198,7 +208,7 @@ def summarize_profile(stats_dir: str, fetch_dir: str, write_dir: str, workload: 
         raise SystemExit(f"kernel not found in counters: {list(acc)}")
 
     is_copy = lambda n: "neg" in n.lower()
-    is_part = lambda n: "partials_kernel" in n
+    is_part = lambda n: kname in n
     _, copy_fetch_kib, _ = pick(fetch, is_copy)
     _, copy_write_kib, _ = pick(write, is_copy)
     pname, part_fetch_kib, nf = pick(fetch, is_part)
@@ -213,17 +223,16 @@ def summarize_profile(stats_dir: str, fetch_dir: str, write_dir: str, workload: 
            "copy_bytes": COPY_BYTES, "fetch_scale": f_scale, "write_scale": w_scale,
            "hbm_fetch_bytes_per_launch": fetch_b, "hbm_write_bytes_per_launch": write_b,
            "hbm_bytes_per_launch": fetch_b + write_b,
-           "trace_avg_us_event_timed_launches": timed_us}
+           "trace_avg_us_all_launches": timed_us}
     os.makedirs(out_dir, exist_ok=True)
-    json.dump(rec, open(os.path.join(out_dir, f"traffic_partials_{workload}.json"), "w"), indent=1)
+    json.dump(rec, open(os.path.join(out_dir, f"traffic_{kernel}_{workload}.json"), "w"), indent=1)
     lines = [f"# rocprofv3 kernel statistics, {workload}", "",
              "| kernel | calls | avg us | min us | max us | % time |", "|---|---|---|---|---|---|"]
     for r in stats:
         lines.append(f"| {r['Name'][:90]} | {r['Calls']} | {float(r['AverageNs']) / 1e3:.2f} | "
                      f"{float(r['MinNs']) / 1e3:.2f} | {float(r['MaxNs']) / 1e3:.2f} | "
                      f"{float(r['Percentage']):.2f} |")
-    lines += ["", f"`{pname}` over the {len(timed)} launches that bench.py times with HIP events "
-              f"(dispatches {warmup + steps}..{warmup + 2 * steps - 1}): average {timed_us:.2f} us."]
+    lines += ["", f"`{pname}` over all {len(trace)} launches of the run: average {timed_us:.2f} us."]
     lines += ["", f"HBM traffic of `{pname}` per launch (FETCH_SIZE / WRITE_SIZE, scaled by a "
               f"{COPY_BYTES}-byte copy: fetch x{f_scale:.4f}, write x{w_scale:.4f}): "
               f"{fetch_b / 1e6:.2f} MB read, {write_b / 1e6:.2f} MB written."]
@@ -273,6 +282,8 @@ def main():
                     help="first run the 1 GiB copy-equivalent kernel that scales HBM counters")
     ap.add_argument("--summarize-profile", nargs=4, metavar=("STATS", "FETCH", "WRITE", "OUT"),
                     help="summarize rocprofv3 outputs of the workload into OUT")
+    ap.add_argument("--kernel", default="partials", choices=sorted(KERNEL_NAMES),
+                    help="kernel whose counters --summarize-profile records")
     ap.add_argument("--summarize-stats", nargs=2, metavar=("STATS", "OUT"),
                     help="write the kernel statistics of a rocprofv3 run of the workload into OUT")
     args = ap.parse_args()
@@ -281,7 +292,7 @@ def main():
         return
     if args.summarize_profile:
         summarize_profile(*args.summarize_profile[:3], args.workload, args.summarize_profile[3],
-                          args.warmup, args.steps)
+                          args.warmup, args.steps, args.kernel)
         return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU: the bifurcated decode step runs on a single MI355X "
@@ -331,21 +342,31 @@ def main():
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
     ms_per_step = elapsed * 1e3 / args.steps
-    # Kernel timing (roofline): the same steps again, the library's partial
-    # launch recording start/stop events with the kernel in every step.
-    bif.bifattn_plan_set_timing(plan, bif.KERNEL_PARTIALS, args.steps)
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for k in range(args.steps):
-        step(k)
-    torch.cuda.synchronize()
-    evt_loop_us = (time.perf_counter() - t0) * 1e6 / args.steps
-    n_timed, part_ms = bif.bifattn_plan_read_timing(plan)
-    bif.bifattn_plan_set_timing(plan, bif.KERNEL_PARTIALS, 0)
-    assert n_timed == args.steps
-    part_us = part_ms * 1e3 / n_timed
+    # Kernel timing (roofline): the same steps again, the library's launch
+    # recording start/stop events with the selected kernel in every step.
+    def timed_pass(kernel):
+        bif.bifattn_plan_set_timing(plan, kernel, args.steps)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for k in range(args.steps):
+            step(k)
+        torch.cuda.synchronize()
+        loop_us = (time.perf_counter() - t0) * 1e6 / args.steps
+        n_timed, ms = bif.bifattn_plan_read_timing(plan)
+        bif.bifattn_plan_set_timing(plan, kernel, 0)
+        assert n_timed == args.steps
+        return ms * 1e3 / n_timed, loop_us
+
+    part_us, evt_loop_us = timed_pass(bif.KERNEL_PARTIALS)
+    many_rows = w.b * (w.h // w.g) * w.n > 64 and info["path"] == bif.PATHS["bifurcated"]
+    ctx_us = dec_us = None
+    if many_rows:
+        ctx_us, _ = timed_pass(bif.KERNEL_CONTEXT)
+        if w.m_d_max > 0:
+            dec_us, _ = timed_pass(bif.KERNEL_DECODE)
     log(f"[bench] timed {args.steps} steps: {ms_per_step * 1e3:.2f} us/step, "
-        f"partial kernel {part_us:.2f} us (event loop {evt_loop_us:.2f} us/step)")
+        f"partial section {part_us:.2f} us, context kernel {ctx_us} us, decode launch {dec_us} us "
+        f"(event loop {evt_loop_us:.2f} us/step)")
 
     # Per-call latency distribution: events on the call's stream around each
     # call (the whole call: partial and combine launches).
@@ -409,8 +430,41 @@ def main():
         cpu = cpu_baseline(x, w, args.cpu_seconds)
 
     value = B_kv / (ms_per_step * 1e-3) / 1e9
-    achieved = B_kv / (part_us * 1e-6) / 1e9
-    traffic = measured_traffic(w.name)
+    es = workloads.KV_BYTES[w.kv]
+    ctx_bytes = 2 * es * w.g * w.d * w.m_c
+    dec_bytes = B_kv - ctx_bytes
+    ctx_flops = 4 * w.h * w.n * w.d * w.b * w.m_c
+    if many_rows and (dec_us is None or ctx_us >= dec_us):
+        # The many-row context kernel: a contraction over b*p*n rows per group.
+        tflops = ctx_flops / (ctx_us * 1e-6) / 1e12
+        roofline = {"kernel": "ctx_large_kernel (many-row context partials)", "bound": "mfma",
+                    "achieved": round(tflops, 1), "peak": MFMA_PEAK_TFLOPS, "unit": "TFLOP/s",
+                    "frac": round(tflops / MFMA_PEAK_TFLOPS, 4),
+                    "traffic": measured_traffic(w.name, "ctx_large"),
+                    "avg_launch_us": round(ctx_us, 3), "flops_per_launch": ctx_flops,
+                    "bytes_per_launch": ctx_bytes}
+    elif many_rows:
+        gbs = dec_bytes / (dec_us * 1e-6) / 1e9
+        roofline = {"kernel": "partials_kernel (decode partials)", "bound": "hbm",
+                    "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                    "frac": round(gbs / HBM_PEAK_GBS, 4),
+                    "traffic": measured_traffic(w.name, "partials"),
+                    "avg_launch_us": round(dec_us, 3), "bytes_per_launch": dec_bytes}
+    else:
+        gbs = B_kv / (part_us * 1e-6) / 1e9
+        roofline = {"kernel": "partials_kernel (context + decode partials)", "bound": "hbm",
+                    "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                    "frac": round(gbs / HBM_PEAK_GBS, 4),
+                    "traffic": measured_traffic(w.name, "partials"),
+                    "avg_launch_us": round(part_us, 3), "bytes_per_launch": B_kv}
+    step_s = ms_per_step * 1e-3
+    roofs = {"hbm_frac_step": round(B_kv / step_s / 1e9 / HBM_PEAK_GBS, 4),
+             "mfma_frac_step": round(flops / step_s / 1e12 / MFMA_PEAK_TFLOPS, 4),
+             "hbm_time_us": round(B_kv / (HBM_PEAK_GBS * 1e9) * 1e6, 3),
+             "mfma_time_us": round(flops / (MFMA_PEAK_TFLOPS * 1e12) * 1e6, 3)}
+    extra["kernel_us"] = {"partial_section": round(part_us, 3),
+                          "context": None if ctx_us is None else round(ctx_us, 3),
+                          "decode": None if dec_us is None else round(dec_us, 3)}
     rec = {
         "metric": METRIC,
         "value": round(value, 1),
@@ -424,16 +478,16 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "bf16",
+        # bf16 caches: bf16 products, fp32 accumulation; 8-bit caches: the
+        # codes, widened exactly to bf16 for the same products.
+        "dtype": w.kv,
         "data": "synthetic",
         "config": {"workload": w.name, "b": w.b, "h": w.h, "g": w.g, "d": w.d, "m_c": w.m_c,
                    "m_d": w.m_d_max, "new_tokens": w.n, "kv_cache": w.kv,
                    "decode_lens": "ragged" if w.ragged else "uniform",
                    "parallelism": "single GPU"},
-        "roofline": {"kernel": "partials_kernel (context + decode partials)", "bound": "hbm",
-                     "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
-                     "avg_launch_us": round(part_us, 3)},
+        "roofline": roofline,
+        "roofs": roofs,
         "cpu_baseline": cpu,
         "ablation": ablation,
         "extra": extra,

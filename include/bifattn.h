@@ -137,7 +137,9 @@ typedef struct {
 typedef enum {
   BIFATTN_KERNEL_PARTIALS = 0, /* context + decode partial kernel(s) of a call */
   BIFATTN_KERNEL_COMBINE = 1,  /* online-softmax combine of a call */
-  BIFATTN_KERNEL_CALL = 2      /* the whole call, first launch to last */
+  BIFATTN_KERNEL_CALL = 2,     /* the whole call, first launch to last */
+  BIFATTN_KERNEL_CONTEXT = 3,  /* the launch holding the context work-groups */
+  BIFATTN_KERNEL_DECODE = 4    /* the launch holding the decode work-groups */
 } bifattn_kernel_t;
 
 /*
@@ -158,8 +160,13 @@ typedef enum {
  */
 bifattn_status_t bifattn_plan_create(const bifattn_dims_t *dims, bifattn_plan_t *plan);
 
-/* Free the plan and its workspace after waiting for its device work.
- * NULL is accepted and ignored. */
+/* Free the plan and its workspace after waiting for the plan's own device
+ * work: the end of its last call (an event every call records on its stream
+ * after its last launch) and the plan's own stream. The workspace comes from
+ * the stream-ordered allocator and is freed in the plan's stream order, so
+ * other streams on the device are not waited for (where that allocator is
+ * unavailable the plan falls back to hipMalloc, whose free synchronises the
+ * device). NULL is accepted and ignored. */
 bifattn_status_t bifattn_plan_destroy(bifattn_plan_t plan);
 
 /* Fill *info with the plan's split decisions. EINVAL on null arguments. */
@@ -265,9 +272,13 @@ bifattn_status_t bifattn_plan_status(bifattn_plan_t plan, hipStream_t stream);
  * start of the first launch of the section to the end of its last (where a
  * plan runs its decode launch on a side stream beside the many-row context
  * kernel, the partial section is recorded on the call's stream from before
- * the fork to after the join); for
+ * the fork to after the join); BIFATTN_KERNEL_CONTEXT and
+ * BIFATTN_KERNEL_DECODE time the launch that holds the context (decode)
+ * work-groups alone, which is the partial launch itself where one launch
+ * holds both (and nothing on the standard path or the replicated ablation); for
  * BIFATTN_KERNEL_CALL they are recorded on the stream around the whole
- * call. Timing stops recording when full.
+ * call. Timing stops recording when full. Before replacing the recorder it
+ * waits for the plan's own last call (not for the whole device).
  * Errors: EINVAL (bad kernel id or negative capacity), ENOMEM, EHIP.
  */
 bifattn_status_t bifattn_plan_set_timing(bifattn_plan_t plan, bifattn_kernel_t kernel,

@@ -17,7 +17,7 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libbifattn.so")
 
 OK, EINVAL, EUNSUPPORTED, EALIGN, ENOMEM, EHIP, ELENS, ESCALE = 0, -1, -2, -3, -4, -5, -6, -7
-KERNEL_PARTIALS, KERNEL_COMBINE, KERNEL_CALL = 0, 1, 2
+KERNEL_PARTIALS, KERNEL_COMBINE, KERNEL_CALL, KERNEL_CONTEXT, KERNEL_DECODE = 0, 1, 2, 3, 4
 #: Cache element types (bifattn_kv_type_t).
 KV_TYPES = {"bf16": 0, "fp8_e4m3": 1, "int8": 2}
 #: Paths of bifattn_decode (bifattn_path_t): "auto" lets the plan choose.

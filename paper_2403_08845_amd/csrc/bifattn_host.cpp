@@ -27,8 +27,18 @@ struct bifattn_plan_s {
   int rep_keys = 0, S_r = 0, n_rep_blocks = 0;
   int fused = 1;
   int fork = 0;        // many-row path: decode launch on a side stream beside the context kernel
+  // The plan's own stream (non-blocking, default priority): the workspace is
+  // allocated and freed in its order (stream-ordered allocator, so that
+  // freeing it does not synchronise the device) and, on many-row plans with
+  // a large decode part, the decode launch runs on it beside the context
+  // kernel.
   hipStream_t side = nullptr;
+  bool ws_async = false;  // workspace from hipMallocAsync (else hipMalloc)
   hipEvent_t fork_ev = nullptr, join_ev = nullptr;
+  // Recorded on the call's stream after the last launch of every call: what
+  // destroy and set_timing wait for (the plan's own work, not the device's).
+  hipEvent_t done_ev = nullptr;
+  bool done_recorded = false;
   int path = BIFATTN_PATH_BIFURCATED;  // resolved: bifurcated or standard
   int device = 0;
   // workspace
@@ -47,6 +57,13 @@ struct bifattn_plan_s {
 };
 
 namespace {
+
+// Events that only order the plan's work on its device (the completion
+// mark, the side-stream fork and join): no timing, and no system-scope fence
+// when recorded (the host reads nothing through them; a recorded system
+// fence writes back the L2 and costs ~3 us per call). Each kernel's own
+// end-of-dispatch release still publishes its results to the device.
+constexpr unsigned kOrderEventFlags = hipEventDisableTiming | hipEventDisableSystemFence;
 
 constexpr int kCUs = 256;  // MI355X compute units; split heuristics aim at whole waves of them
 
@@ -226,6 +243,59 @@ bifattn_status_t check_dims(const bifattn_dims_t* d) {
   return BIFATTN_OK;
 }
 
+// Mark the end of a call's work on its stream.
+void mark_done(bifattn_plan_s* P, hipStream_t stream) {
+  if (hipEventRecord(P->done_ev, stream) == hipSuccess)
+    P->done_recorded = true;
+  else
+    (void)hipGetLastError();
+}
+
+// The events of a call's last launch with the completion mark added: the
+// launch records the plan's done event itself at the kernel's end (no
+// separate marker on the stream), unless it already records a timing stop.
+LaunchEvents last_launch(bifattn_plan_s* P, LaunchEvents ev) {
+  if (!ev.stop) {
+    ev.stop = P->done_ev;
+    P->done_recorded = true;
+  }
+  return ev;
+}
+
+// Wait for the plan's own enqueued work: the last call's end (every earlier
+// call of the plan ran on a stream its successor was ordered after, or is
+// covered by the caller's one-stream-at-a-time contract) and the side stream.
+bool wait_done(bifattn_plan_s* P) {
+  bool ok = true;
+  if (P->done_recorded && hipEventSynchronize(P->done_ev) != hipSuccess) ok = false;
+  if (P->side && hipStreamSynchronize(P->side) != hipSuccess) ok = false;
+  return ok;
+}
+
+void free_events(bifattn_plan_s* P);
+
+// Free everything the plan owns and the plan itself. The workspace is freed
+// in the order of the plan's own stream (a stream-ordered free waits for
+// that stream only; hipFree would synchronise the whole device), so the
+// caller must have waited for the plan's work first.
+bool release_plan(bifattn_plan_s* P) {
+  bool ok = true;
+  free_events(P);
+  if (P->done_ev) (void)hipEventDestroy(P->done_ev);
+  if (P->fork_ev) (void)hipEventDestroy(P->fork_ev);
+  if (P->join_ev) (void)hipEventDestroy(P->join_ev);
+  if (P->ws) {
+    if (P->ws_async)
+      ok = hipFreeAsync(P->ws, P->side) == hipSuccess && hipStreamSynchronize(P->side) == hipSuccess;
+    else
+      ok = hipFree(P->ws) == hipSuccess;
+  }
+  if (P->side) (void)hipStreamDestroy(P->side);
+  if (!ok) (void)hipGetLastError();
+  delete P;
+  return ok;
+}
+
 void free_events(bifattn_plan_s* P) {
   for (hipEvent_t e : P->events) (void)hipEventDestroy(e);
   P->events.clear();
@@ -253,6 +323,11 @@ struct TimedSection {
   LaunchEvents first() const { return LaunchEvents{ev(0), nullptr}; }
   LaunchEvents last() const { return LaunchEvents{nullptr, ev(1)}; }
   LaunchEvents both() const { return LaunchEvents{ev(0), ev(1)}; }
+  // This section's events where they are set, else the other's (sections of
+  // one call may share a launch; at most one of them is being timed).
+  static LaunchEvents either(const LaunchEvents& a, const LaunchEvents& b) {
+    return LaunchEvents{a.start ? a.start : b.start, a.stop ? a.stop : b.stop};
+  }
   // For sections that span streams: the pair recorded on the call's stream.
   void record_start() {
     if (on && in_kernel) (void)hipEventRecord(P->events[2 * P->timing_n], stream);
@@ -373,10 +448,22 @@ bifattn_status_t bifattn_plan_create(const bifattn_dims_t* dims, bifattn_plan_t*
   off = align256(off + dec_rows * 8);
   const size_t o_status = off;
   off = align256(off + 4);
-  if (hipMalloc(&P->ws, off) != hipSuccess) {
+  if (hipStreamCreateWithFlags(&P->side, hipStreamNonBlocking) != hipSuccess) {
     (void)hipGetLastError();
     delete P;
-    return BIFATTN_ENOMEM;
+    return BIFATTN_EHIP;
+  }
+  if (hipMallocAsync(&P->ws, off, P->side) == hipSuccess) {
+    P->ws_async = true;
+  } else {
+    (void)hipGetLastError();
+    P->ws = nullptr;
+    if (hipMalloc(&P->ws, off) != hipSuccess) {
+      (void)hipGetLastError();
+      P->ws = nullptr;
+      release_plan(P);
+      return BIFATTN_ENOMEM;
+    }
   }
   P->ws_bytes = off;
   char* base = static_cast<char*>(P->ws);
@@ -385,15 +472,16 @@ bifattn_status_t bifattn_plan_create(const bifattn_dims_t* dims, bifattn_plan_t*
   P->dec_acc = reinterpret_cast<float*>(base + o_dec_acc);
   P->dec_ml = reinterpret_cast<float2*>(base + o_dec_ml);
   P->status = reinterpret_cast<int*>(base + o_status);
-  if (hipMemset(P->status, 0, 4) != hipSuccess) {
-    (void)hipFree(P->ws);
-    delete P;
+  if (hipMemsetAsync(P->status, 0, 4, P->side) != hipSuccess ||
+      hipStreamSynchronize(P->side) != hipSuccess ||
+      hipEventCreateWithFlags(&P->done_ev, kOrderEventFlags) != hipSuccess) {
+    (void)hipGetLastError();
+    release_plan(P);
     return BIFATTN_EHIP;
   }
   if (P->fork) {
-    if (hipStreamCreateWithFlags(&P->side, hipStreamNonBlocking) != hipSuccess ||
-        hipEventCreateWithFlags(&P->fork_ev, hipEventDisableTiming) != hipSuccess ||
-        hipEventCreateWithFlags(&P->join_ev, hipEventDisableTiming) != hipSuccess) {
+    if (hipEventCreateWithFlags(&P->fork_ev, kOrderEventFlags) != hipSuccess ||
+        hipEventCreateWithFlags(&P->join_ev, kOrderEventFlags) != hipSuccess) {
       (void)hipGetLastError();
       P->fork = 0;
     }
@@ -405,13 +493,8 @@ bifattn_status_t bifattn_plan_create(const bifattn_dims_t* dims, bifattn_plan_t*
 bifattn_status_t bifattn_plan_destroy(bifattn_plan_t P) {
   if (!P) return BIFATTN_OK;
   bifattn_status_t st = BIFATTN_OK;
-  if (hipDeviceSynchronize() != hipSuccess) st = BIFATTN_EHIP;
-  free_events(P);
-  if (P->fork_ev) (void)hipEventDestroy(P->fork_ev);
-  if (P->join_ev) (void)hipEventDestroy(P->join_ev);
-  if (P->side) (void)hipStreamDestroy(P->side);
-  if (P->ws && hipFree(P->ws) != hipSuccess) st = BIFATTN_EHIP;
-  delete P;
+  if (!wait_done(P)) st = BIFATTN_EHIP;
+  if (!release_plan(P)) st = BIFATTN_EHIP;
   return st;
 }
 
@@ -457,13 +540,18 @@ bifattn_status_t bifattn_decode_scaled(bifattn_plan_t P, const void* q, const vo
   K.S_d = P->S_d;
   TimedSection whole(P, BIFATTN_KERNEL_CALL, stream);
   TimedSection part(P, BIFATTN_KERNEL_PARTIALS, stream, true);
+  TimedSection ctxs(P, BIFATTN_KERNEL_CONTEXT, stream, true);
+  TimedSection decs(P, BIFATTN_KERNEL_DECODE, stream, true);
+  auto ev = [](const LaunchEvents& a, const LaunchEvents& b) { return TimedSection::either(a, b); };
   hipError_t e = hipSuccess;
   if (P->path == BIFATTN_PATH_STANDARD) {
     K.out = out;
     K.v_scale = v_scale;
-    e = launch_standard(K, P->dims.d, kv, P->dec_tiles, stream, part.both());
+    const LaunchEvents lev = part.both();
+    e = launch_standard(K, P->dims.d, kv, P->dec_tiles, stream, last_launch(P, lev));
     part.end();
     whole.end();
+    if (lev.stop) mark_done(P, stream);
     return e == hipSuccess ? BIFATTN_OK : BIFATTN_EHIP;
   }
   K.n_ctx_blocks = 0;
@@ -482,9 +570,9 @@ bifattn_status_t bifattn_decode_scaled(bifattn_plan_t P, const void* q, const vo
     if (hipEventRecord(P->fork_ev, stream) != hipSuccess ||
         hipStreamWaitEvent(P->side, P->fork_ev, 0) != hipSuccess)
       return BIFATTN_EHIP;
-    e = launch_partials(Kd, P->dims.d, kv, kCtxNone, P->dec_tiles, P->side);
+    e = launch_partials(Kd, P->dims.d, kv, kCtxNone, P->dec_tiles, P->side, decs.both());
     K.n_ctx_blocks = P->n_ctx_blocks;
-    if (e == hipSuccess) e = launch_ctx_large(K, P->dims.d, kv, stream);
+    if (e == hipSuccess) e = launch_ctx_large(K, P->dims.d, kv, stream, ctxs.both());
     if (e == hipSuccess && (hipEventRecord(P->join_ev, P->side) != hipSuccess ||
                             hipStreamWaitEvent(stream, P->join_ev, 0) != hipSuccess))
       e = hipErrorUnknown;
@@ -493,33 +581,46 @@ bifattn_status_t bifattn_decode_scaled(bifattn_plan_t P, const void* q, const vo
   } else if (P->ctx_mode == kCtxLarge) {
     // The many-row context kernel, then the decode work-groups.
     K.n_ctx_blocks = P->n_ctx_blocks;
-    e = launch_ctx_large(K, P->dims.d, kv, stream, two ? part.first() : part.both());
+    e = launch_ctx_large(K, P->dims.d, kv, stream,
+                         ev(two ? part.first() : part.both(), ctxs.both()));
     K.n_ctx_blocks = 0;
     K.n_dec_blocks = P->n_dec_blocks;
     if (e == hipSuccess && two)
-      e = launch_partials(K, P->dims.d, kv, kCtxNone, P->dec_tiles, stream, part.last());
+      e = launch_partials(K, P->dims.d, kv, kCtxNone, P->dec_tiles, stream,
+                          ev(part.last(), decs.both()));
   } else if (P->fused) {
+    // One launch holds the context and the decode work-groups: each section
+    // times it.
     K.n_ctx_small_blocks = P->n_ctx_small_blocks;
     K.n_dec_blocks = P->n_dec_blocks;
-    e = launch_partials(K, P->dims.d, kv, P->ctx_mode, P->dec_tiles, stream, part.both());
+    e = launch_partials(K, P->dims.d, kv, P->ctx_mode, P->dec_tiles, stream,
+                        ev(ev(part.both(), ctxs.both()), decs.both()));
   } else {
     K.n_ctx_small_blocks = P->n_ctx_small_blocks;
     e = launch_partials(K, P->dims.d, kv, P->ctx_mode, P->dec_tiles, stream,
-                        two ? part.first() : part.both());
+                        ev(two ? part.first() : part.both(), ctxs.both()));
     K.n_ctx_small_blocks = 0;
     K.n_dec_blocks = P->n_dec_blocks;
     if (e == hipSuccess && two)
-      e = launch_partials(K, P->dims.d, kv, kCtxNone, P->dec_tiles, stream, part.last());
+      e = launch_partials(K, P->dims.d, kv, kCtxNone, P->dec_tiles, stream,
+                          ev(part.last(), decs.both()));
   }
   part.end();
-  if (e != hipSuccess) return BIFATTN_EHIP;
+  ctxs.end();
+  decs.end();
+  if (e != hipSuccess) {
+    mark_done(P, stream);
+    return BIFATTN_EHIP;
+  }
   TimedSection comb(P, BIFATTN_KERNEL_COMBINE, stream, true);
   CombineParams C = combine_params(P, has_dec ? decode_lens : nullptr, k_scale, v_scale, out);
   C.S_c = P->S_c;
   C.S_d = P->S_d * kWaves;
-  e = launch_combine(C, P->dims.d, stream, comb.both());
+  const LaunchEvents cev = comb.both();
+  e = launch_combine(C, P->dims.d, stream, last_launch(P, cev));
   comb.end();
   whole.end();
+  if (cev.stop) mark_done(P, stream);
   return e == hipSuccess ? BIFATTN_OK : BIFATTN_EHIP;
 }
 
@@ -556,14 +657,19 @@ bifattn_status_t bifattn_decode_replicated_scaled(bifattn_plan_t P, const void* 
   hipError_t e = launch_partials(K, P->dims.d, P->dims.kv_type, kCtxNone, P->dec_tiles, stream,
                                  part.both());
   part.end();
-  if (e != hipSuccess) return BIFATTN_EHIP;
+  if (e != hipSuccess) {
+    mark_done(P, stream);
+    return BIFATTN_EHIP;
+  }
   TimedSection comb(P, BIFATTN_KERNEL_COMBINE, stream, true);
   CombineParams C = combine_params(P, has_dec ? decode_lens : nullptr, k_scale, v_scale, out);
   C.S_c = 0;
   C.S_d = P->S_r * kWaves;
-  e = launch_combine(C, P->dims.d, stream, comb.both());
+  const LaunchEvents cev = comb.both();
+  e = launch_combine(C, P->dims.d, stream, last_launch(P, cev));
   comb.end();
   whole.end();
+  if (cev.stop) mark_done(P, stream);
   return e == hipSuccess ? BIFATTN_OK : BIFATTN_EHIP;
 }
 
@@ -593,8 +699,9 @@ bifattn_status_t bifattn_append_kv(bifattn_plan_t P, const void* k_new, const vo
   A.g = P->dims.g;
   A.n = P->ntok;
   A.m_d_max = P->dims.m_d_max;
-  return launch_append(A, P->dims.d, P->dims.kv_type, stream) == hipSuccess ? BIFATTN_OK
-                                                                              : BIFATTN_EHIP;
+  const hipError_t e = launch_append(A, P->dims.d, P->dims.kv_type, stream,
+                                     last_launch(P, LaunchEvents{}));
+  return e == hipSuccess ? BIFATTN_OK : BIFATTN_EHIP;
 }
 
 bifattn_status_t bifattn_plan_status(bifattn_plan_t P, hipStream_t stream) {
@@ -612,9 +719,9 @@ bifattn_status_t bifattn_plan_status(bifattn_plan_t P, hipStream_t stream) {
 
 bifattn_status_t bifattn_plan_set_timing(bifattn_plan_t P, bifattn_kernel_t kernel,
                                          int32_t capacity) {
-  if (!P || capacity < 0 || (int)kernel < 0 || (int)kernel > BIFATTN_KERNEL_CALL)
+  if (!P || capacity < 0 || (int)kernel < 0 || (int)kernel > BIFATTN_KERNEL_DECODE)
     return BIFATTN_EINVAL;
-  if (hipDeviceSynchronize() != hipSuccess) return BIFATTN_EHIP;
+  if (!wait_done(P)) return BIFATTN_EHIP;  // the events to be freed may still be pending
   free_events(P);
   if (capacity == 0) return BIFATTN_OK;
   P->events.reserve(2 * (size_t)capacity);

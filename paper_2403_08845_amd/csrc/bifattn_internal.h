@@ -115,7 +115,8 @@ hipError_t launch_partials(const PartialsParams& P, int d, int kv, int ctx_mode,
 hipError_t launch_combine(const CombineParams& C, int d, hipStream_t stream,
                           const LaunchEvents& ev = {});
 // Launch the decode-cache append (one work-group per sample).
-hipError_t launch_append(const AppendParams& A, int d, int kv, hipStream_t stream);
+hipError_t launch_append(const AppendParams& A, int d, int kv, hipStream_t stream,
+                         const LaunchEvents& ev = {});
 // Launch the standard (unsplit) attention kernel: one work-group per
 // (sample, group), `tiles` 16-row query tiles per wave, output written directly.
 hipError_t launch_standard(const PartialsParams& P, int d, int kv, int tiles, hipStream_t stream,

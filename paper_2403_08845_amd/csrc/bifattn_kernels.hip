@@ -1304,14 +1304,14 @@ __global__ __launch_bounds__(256) void append_kernel(AppendParams A) {
 
 }  // namespace
 
-hipError_t launch_append(const AppendParams& A, int d, int kv, hipStream_t stream) {
+hipError_t launch_append(const AppendParams& A, int d, int kv, hipStream_t stream,
+                         const LaunchEvents& ev) {
   switch (d * kv_bytes(kv)) {
-    case 256: append_kernel<256><<<A.b, 256, 0, stream>>>(A); break;
-    case 128: append_kernel<128><<<A.b, 256, 0, stream>>>(A); break;
-    case 64: append_kernel<64><<<A.b, 256, 0, stream>>>(A); break;
+    case 256: return launch(append_kernel<256>, A.b, 256, stream, ev, A);
+    case 128: return launch(append_kernel<128>, A.b, 256, stream, ev, A);
+    case 64: return launch(append_kernel<64>, A.b, 256, stream, ev, A);
     default: return hipErrorInvalidValue;
   }
-  return hipGetLastError();
 }
 hipError_t launch_ctx_large(const PartialsParams& P, int d, int kv, hipStream_t stream,
                             const LaunchEvents& ev) {

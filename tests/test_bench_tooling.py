@@ -90,8 +90,37 @@ def test_profile_summary_scales_counters_by_the_copy(tmp_path):
     assert rec["hbm_fetch_bytes_per_launch"] == pytest.approx(1001.0 * 1024 * 2)
     assert rec["hbm_write_bytes_per_launch"] == pytest.approx(10.0 * 1024)
     assert rec["kernel_source_sha256_16"] == bench.kernel_source_hash()
-    # the event-timed launches are the second pass of `steps` dispatches: 72 us each
-    assert rec["trace_avg_us_event_timed_launches"] == pytest.approx(72.0)
+    # the average over every launch of the kernel in the run
+    n = warmup + 2 * steps
+    exp = (70.0 * (warmup + steps) + 72.0 * steps) / n
+    assert rec["trace_avg_us_all_launches"] == pytest.approx(exp)
+
+
+def test_profile_summary_of_the_context_kernel(tmp_path):
+    """--kernel ctx_large records the many-row context kernel's counters under
+    its own name."""
+    root = str(tmp_path)
+    ctx = "void bifattn::ctx_large_kernel<128, KvBf16>(bifattn::PartialsParams)"
+    _write_csv(os.path.join(root, "stats", "run_kernel_stats.csv"),
+               ["Name", "Calls", "AverageNs", "MinNs", "MaxNs", "Percentage"],
+               [[ctx, 2, 50000, 50000, 50000, 60.0], [PART, 2, 20000, 20000, 20000, 40.0]])
+    _write_csv(os.path.join(root, "stats", "run_kernel_trace.csv"),
+               ["Kernel_Name", "Start_Timestamp", "End_Timestamp"],
+               [[ctx, 0, 50000], [PART, 0, 20000], [ctx, 100000, 150000], [PART, 100000, 120000]])
+    kib = bench.COPY_BYTES / 1024.0
+    _write_csv(os.path.join(root, "fetch", "run_counter_collection.csv"),
+               ["Kernel_Name", "Counter_Name", "Counter_Value"],
+               [[COPY, "FETCH_SIZE", kib / 2], [PART, "FETCH_SIZE", 7.0], [ctx, "FETCH_SIZE", 4096.0]])
+    _write_csv(os.path.join(root, "write", "run_counter_collection.csv"),
+               ["Kernel_Name", "Counter_Name", "Counter_Value"],
+               [[COPY, "WRITE_SIZE", kib], [PART, "WRITE_SIZE", 1.0], [ctx, "WRITE_SIZE", 64.0]])
+    out = tmp_path / "out"
+    bench.summarize_profile(str(tmp_path / "stats"), str(tmp_path / "fetch"), str(tmp_path / "write"),
+                            "mqa_b128_mc16k_md512", str(out), 0, 1, kernel="ctx_large")
+    rec = json.load(open(out / "traffic_ctx_large_mqa_b128_mc16k_md512.json"))
+    assert "ctx_large_kernel" in rec["kernel"]
+    assert rec["hbm_fetch_bytes_per_launch"] == pytest.approx(4096.0 * 1024 * 2)
+    assert rec["trace_avg_us_all_launches"] == pytest.approx(50.0)
 
 
 def test_stats_summary_names_its_command(tmp_path):
