@@ -26,6 +26,13 @@ to the per-entry bound and get 5e-3 (measured up to 3.6e-3):
     groups' logits up to 2x larger than the bf16 workloads'.
 Tests that sharpen the softmax further on purpose (key scales up to 8x) may
 pass the contract bound itself; the relative-L2 gate is never raised.
+
+The gates are stated for values of unit spread, as the bf16 workloads draw
+them. 8-bit caches carry per-group value scales that spread the groups'
+values by up to 2x either way, and the rounding error of an output entry
+scales with its group's values; so for a full output of an 8-bit problem
+both sides are first divided, per head, by the spread of its group's values
+(value_units).
 """
 import numpy as np
 
@@ -57,6 +64,21 @@ def gate_errors(out, ref):
     return max_abs, rel_l2
 
 
+def value_units(x):
+    """Per query head: the value scale of its group times the standard
+    deviation of the group's value codes (context and valid decode rows)."""
+    from .pins_kvquant import code_table
+    b, h = x["q"].shape[:2]
+    g = x["Vc"].shape[0]
+    table = code_table(x["kv"])
+    units = np.empty(g)
+    for gam in range(g):
+        vals = [table[x["Vc"][gam]].ravel()]
+        vals += [table[x["Vd"][i, gam, :x["lens"][i]]].ravel() for i in range(b)]
+        units[gam] = float(x["v_scale"][gam]) * float(np.std(np.concatenate(vals)))
+    return np.repeat(units, h // g)
+
+
 def assert_parity(out, ref, what="", gate_max_abs=None, x=None):
     """The gate is gate_max_abs_for(x) when the problem x is given, else
     GATE_MAX_ABS; gate_max_abs overrides it (a test whose softmax is much
@@ -66,6 +88,11 @@ def assert_parity(out, ref, what="", gate_max_abs=None, x=None):
         gate_max_abs = GATE_MAX_ABS if x is None else gate_max_abs_for(x)
     assert gate_max_abs <= CONTRACT_MAX_ABS
     out = np.asarray(out, np.float64)
+    ref = np.asarray(ref, np.float64)
+    if (x is not None and x.get("kv", "bf16") != "bf16" and x.get("v_scale") is not None
+            and out.shape == np.asarray(x["q"]).shape):
+        u = value_units(x).reshape((1, -1) + (1,) * (out.ndim - 2))
+        out, ref = out / u, ref / u
     assert np.all(np.isfinite(out)), f"{what}: non-finite GPU output"
     max_abs, rel_l2 = gate_errors(out, ref)
     print(f"[gate] {what}: max_abs={max_abs:.3e} rel_l2={rel_l2:.3e}", flush=True)

@@ -9,7 +9,7 @@ import paper_2403_08845_amd as bif
 import workloads
 
 from .gpu_util import run_decode, run_replicated, to_device
-from .parity import assert_parity
+from .parity import assert_parity, value_units
 from .pins_kvquant import KVS, code_table
 
 pytestmark = pytest.mark.gpu
@@ -20,20 +20,8 @@ def _report(name, max_abs, rel):
 
 
 def _value_units(x):
-    """Per output head: v_scale of its group times the standard deviation of
-    the group's value codes (context and valid decode rows). The parity gates
-    are stated for values of unit spread; outputs are divided by this before
-    they are compared."""
-    b, h = x["q"].shape[:2]
-    g = x["Vc"].shape[0]
-    table = code_table(x["kv"])
-    units = np.empty(g)
-    for gam in range(g):
-        vals = [table[x["Vc"][gam]].ravel()]
-        vals += [table[x["Vd"][i, gam, :x["lens"][i]]].ravel() for i in range(b)]
-        units[gam] = float(x["v_scale"][gam]) * float(np.std(np.concatenate(vals)))
-    shape = (1, h) + (1,) * (x["q"].ndim - 2)
-    return np.repeat(units, h // g).reshape(shape)
+    """Per output head, broadcast over samples and head dims."""
+    return value_units(x)[None, :, None]
 
 
 @pytest.mark.parametrize("kv", KVS)
@@ -211,7 +199,5 @@ def test_generation_loop_with_codes(kv):
             y = dict(x, q=q, Kd=Kd_host, Vd=Vd_host, lens=lens_host)
             ref = oracle.attention(**y)
             got = out.cpu().double().numpy()
-            u = _value_units(y)
-            _report(f"{kv} loop step {step}",
-                    *assert_parity(got / u, ref / u, f"{kv} loop step {step}", x=y))
+            _report(f"{kv} loop step {step}", *assert_parity(got, ref, f"{kv} loop step {step}", x=y))
         assert bif.bifattn_plan_status(plan) == bif.OK
