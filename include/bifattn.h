@@ -81,7 +81,8 @@ typedef enum {
   BIFATTN_ENOMEM = -4,       /* workspace or event allocation failed */
   BIFATTN_EHIP = -5,         /* a HIP runtime call or kernel launch failed */
   BIFATTN_ELENS = -6,        /* a decode length was outside [0, m_d_max] */
-  BIFATTN_ESCALE = -7        /* a key or value scale was not a positive normal float */
+  BIFATTN_ESCALE = -7,       /* a key or value scale was not a positive normal float */
+  BIFATTN_ESCRATCH = -8      /* bifattn_decode_noalloc: workspace beyond its fixed scratch */
 } bifattn_status_t;
 
 /* Which computation bifattn_decode runs (bifattn_dims_t.path). The FAQ on
@@ -289,6 +290,37 @@ bifattn_status_t bifattn_plan_set_timing(bifattn_plan_t plan, bifattn_kernel_t k
  * sum of their durations in milliseconds; then rewind the recorder.
  */
 bifattn_status_t bifattn_plan_read_timing(bifattn_plan_t plan, int32_t *calls, double *total_ms);
+
+/*
+ * bifattn_decode_scaled for callers that cannot allocate device memory:
+ * code under HIP graph capture, tight serving loops, harnesses that forbid
+ * allocation. It takes the dimensions instead of a plan (creating a plan
+ * allocates), computes the same work split on the host (the decode launch
+ * always on `stream`, never on a side stream), and keeps its partials and
+ * status word in a fixed scratch buffer of BIFATTN_NOALLOC_SCRATCH_BYTES
+ * (64 MiB) that the library holds on each GPU from its load to the end of
+ * the process. It calls no allocator, creates no stream or event, and
+ * enqueues only kernel launches on `stream`. Arguments, layouts, scale and
+ * length handling are those of bifattn_decode_scaled.
+ * Every call on one GPU shares that GPU's scratch buffer, which keeps the
+ * last call's partials: calls that may overlap on one GPU (two streams, or
+ * one stream and a graph replay) race on it and must be serialised by the
+ * caller. Device-side checks still clamp out-of-range lengths, but their
+ * flags are not reported (there is no plan to query).
+ * Errors: those of bifattn_plan_create's validation and of
+ * bifattn_decode_scaled's argument checks; BIFATTN_ESCRATCH (nothing is
+ * enqueued) when the problem's workspace exceeds the scratch buffer: it
+ * holds g*S_c*b*(h/g)*n context partials and b*g*S_d*4*(h/g)*n decode
+ * partials of (d + 2)*4 bytes each (S_c context splits and S_d decode
+ * chunks of the work split without a side stream), about 4.3 MB for the
+ * 32-sample 7B-shaped MHA layer and 51 MB for the 256-sample GQA layer over
+ * a 32k context. The size check comes before any HIP call.
+ */
+#define BIFATTN_NOALLOC_SCRATCH_BYTES (64u << 20)
+bifattn_status_t bifattn_decode_noalloc(const bifattn_dims_t *dims, const void *q, const void *Kc,
+                                        const void *Vc, const void *Kd, const void *Vd,
+                                        const int32_t *decode_lens, const float *k_scale,
+                                        const float *v_scale, float *out, hipStream_t stream);
 
 /* Static text for a status code. Never NULL. */
 const char *bifattn_status_string(bifattn_status_t status);

@@ -16,7 +16,9 @@ import os
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libbifattn.so")
 
-OK, EINVAL, EUNSUPPORTED, EALIGN, ENOMEM, EHIP, ELENS, ESCALE = 0, -1, -2, -3, -4, -5, -6, -7
+OK, EINVAL, EUNSUPPORTED, EALIGN, ENOMEM, EHIP, ELENS, ESCALE, ESCRATCH = 0, -1, -2, -3, -4, -5, -6, -7, -8
+#: Size of the fixed device scratch of bifattn_decode_noalloc (BIFATTN_NOALLOC_SCRATCH_BYTES).
+NOALLOC_SCRATCH_BYTES = 64 << 20
 KERNEL_PARTIALS, KERNEL_COMBINE, KERNEL_CALL, KERNEL_CONTEXT, KERNEL_DECODE = 0, 1, 2, 3, 4
 #: Cache element types (bifattn_kv_type_t).
 KV_TYPES = {"bf16": 0, "fp8_e4m3": 1, "int8": 2}
@@ -28,6 +30,7 @@ EXPORTED = (
     "bifattn_decode_scaled", "bifattn_decode_replicated", "bifattn_decode_replicated_scaled",
     "bifattn_append_kv", "bifattn_plan_status", "bifattn_plan_set_timing",
     "bifattn_plan_read_timing", "bifattn_status_string", "bifattn_version",
+    "bifattn_decode_noalloc",
 )
 
 
@@ -81,6 +84,8 @@ def lib() -> ctypes.CDLL:
         L.bifattn_decode_replicated.argtypes = [vp, vp, vp, vp, vp, vp, vp]
         L.bifattn_decode_replicated_scaled.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp]
         L.bifattn_append_kv.argtypes = [vp, vp, vp, vp, vp, vp, vp]
+        L.bifattn_decode_noalloc.argtypes = [ctypes.POINTER(Dims), vp, vp, vp, vp, vp, vp, vp, vp,
+                                             vp, vp]
         L.bifattn_plan_status.argtypes = [vp, vp]
         L.bifattn_plan_set_timing.argtypes = [vp, st, i32]
         L.bifattn_plan_read_timing.argtypes = [vp, ctypes.POINTER(i32), ctypes.POINTER(ctypes.c_double)]
@@ -261,6 +266,50 @@ def bifattn_decode_scaled(plan: Plan, q, Kc, Vc, Kd, Vd, decode_lens, k_scale, v
     ]
     _check(lib().bifattn_decode_scaled(plan.handle, *args, _stream_ptr(stream, dev)),
            "bifattn_decode_scaled")
+
+
+class _Unplanned:
+    """Dimensions and device of a call that has no plan (the allocation-free
+    entry point): what the tensor checks compare against."""
+
+    def __init__(self, dims, device):
+        self.dims = dims
+        self.device = device
+
+
+def noalloc_dims(b, h, g, d, m_c, m_d_max, scale=0.0, n=1, kv="bf16", path="auto") -> Dims:
+    """The bifattn_dims_t of a bifattn_decode_noalloc call."""
+    if kv not in KV_TYPES:
+        raise ValueError(f"kv must be one of {sorted(KV_TYPES)}")
+    if path not in PATHS:
+        raise ValueError(f"path must be one of {sorted(PATHS)}")
+    return Dims(b, h, g, d, m_c, m_d_max, scale, n, KV_TYPES[kv], PATHS[path])
+
+
+def bifattn_decode_noalloc(dims: Dims, q, Kc, Vc, Kd, Vd, decode_lens, k_scale, v_scale, out,
+                           stream=None):
+    """bifattn_decode_scaled without a plan and without any device
+    allocation (see include/bifattn.h): the partials live in the library's
+    fixed per-GPU scratch buffer, so calls on one GPU must not overlap.
+    dims: from noalloc_dims(); tensors as for bifattn_decode_scaled, on the
+    current device."""
+    import torch
+    dev = torch.device("cuda", torch.cuda.current_device())
+    shape = _Unplanned(dims, dev)
+    cd = _cache_dtypes(shape)
+    D = dims
+    args = [
+        _tensor(q, _query_shapes(D), torch.bfloat16, dev, "q"),
+        _tensor(Kc, (D.g, D.m_c, D.d), cd, dev, "Kc"),
+        _tensor(Vc, (D.g, D.m_c, D.d), cd, dev, "Vc"),
+        _tensor(Kd, (D.b, D.g, D.m_d_max, D.d), cd, dev, "Kd"),
+        _tensor(Vd, (D.b, D.g, D.m_d_max, D.d), cd, dev, "Vd"),
+        _tensor(decode_lens, (D.b,), torch.int32, dev, "decode_lens"),
+        *_scales(shape, k_scale, v_scale, dev),
+        _tensor(out, [tuple(q.shape)], torch.float32, dev, "out"),
+    ]
+    _check(lib().bifattn_decode_noalloc(ctypes.byref(dims), *args, _stream_ptr(stream, dev)),
+           "bifattn_decode_noalloc")
 
 
 def bifattn_decode_replicated(plan: Plan, q, K, V, decode_lens, out, stream=None):

@@ -129,7 +129,9 @@ int seq_keys(int64_t units, int64_t rows, int start) {
   return keys;
 }
 
-bifattn_status_t plan_splits(bifattn_plan_s* P) {
+// allow_fork: the many-row path may run the decode launch on the plan's own
+// stream (off for the allocation-free entry point, which owns no stream).
+bifattn_status_t plan_splits(bifattn_plan_s* P, bool allow_fork = true) {
   const bifattn_dims_t& d = P->dims;
   P->ntok = d.n > 0 ? d.n : 1;
   // The n tokens of a head are consecutive rows of q and out, so a unit's
@@ -162,7 +164,8 @@ bifattn_status_t plan_splits(bifattn_plan_s* P) {
     P->ctx_row_blocks = (int)ceil_div(M, kLargeRowsPerBlock);
     const double dec_bytes = 2.0 * d.b * d.g * (double)d.m_d_max * d.d * kv_bytes(d.kv_type);
     const int fork_env = env_switch("BIFATTN_FORK");
-    P->fork = d.m_d_max > 0 && (fork_env == -1 ? dec_bytes >= 16.0 * (1 << 20) : fork_env == 1);
+    P->fork = allow_fork && d.m_d_max > 0 &&
+              (fork_env == -1 ? dec_bytes >= 16.0 * (1 << 20) : fork_env == 1);
     int64_t splits = ceil_div(env_int("BIFATTN_CTX_WGS", P->fork ? kCUs : 2 * kCUs),
                               (int64_t)d.g * P->ctx_row_blocks);
     if (splits < 1) splits = 1;
@@ -213,6 +216,44 @@ bifattn_status_t plan_splits(bifattn_plan_s* P) {
   return BIFATTN_OK;
 }
 
+// Byte offsets of the workspace parts (256-byte aligned) and its size: the
+// context partials, the decode partials (sized for the replicated ablation's
+// splits too when `replicated`), and the status word.
+struct WorkspaceLayout {
+  size_t ctx_acc = 0, ctx_ml = 0, dec_acc = 0, dec_ml = 0, status = 0, bytes = 0;
+};
+WorkspaceLayout workspace_layout(const bifattn_plan_s* P, bool replicated) {
+  const bifattn_dims_t& d = P->dims;
+  const size_t D = (size_t)d.d;
+  const size_t ctx_rows = (size_t)d.g * P->S_c * P->M;
+  const int s_dec = replicated && P->S_r > P->S_d ? P->S_r : P->S_d;
+  const size_t dec_rows = (size_t)d.b * d.g * (size_t)s_dec * kWaves * P->p;
+  WorkspaceLayout L;
+  size_t off = 0;
+  L.ctx_acc = off;
+  off = align256(off + ctx_rows * D * 4);
+  L.ctx_ml = off;
+  off = align256(off + ctx_rows * 8);
+  L.dec_acc = off;
+  off = align256(off + dec_rows * D * 4);
+  L.dec_ml = off;
+  off = align256(off + dec_rows * 8);
+  L.status = off;
+  L.bytes = align256(off + 4);
+  return L;
+}
+
+void set_workspace(bifattn_plan_s* P, void* base_ptr, const WorkspaceLayout& L) {
+  char* base = static_cast<char*>(base_ptr);
+  P->ws = base_ptr;
+  P->ws_bytes = L.bytes;
+  P->ctx_acc = reinterpret_cast<float*>(base + L.ctx_acc);
+  P->ctx_ml = reinterpret_cast<float2*>(base + L.ctx_ml);
+  P->dec_acc = reinterpret_cast<float*>(base + L.dec_acc);
+  P->dec_ml = reinterpret_cast<float2*>(base + L.dec_ml);
+  P->status = reinterpret_cast<int*>(base + L.status);
+}
+
 bifattn_status_t check_dims(const bifattn_dims_t* d) {
   if (!d) return BIFATTN_EINVAL;
   if (d->b < 1 || d->h < 1 || d->g < 1 || d->m_c < 1 || d->m_d_max < 0 || d->n < 0)
@@ -245,6 +286,7 @@ bifattn_status_t check_dims(const bifattn_dims_t* d) {
 
 // Mark the end of a call's work on its stream.
 void mark_done(bifattn_plan_s* P, hipStream_t stream) {
+  if (!P->done_ev) return;
   if (hipEventRecord(P->done_ev, stream) == hipSuccess)
     P->done_recorded = true;
   else
@@ -255,7 +297,7 @@ void mark_done(bifattn_plan_s* P, hipStream_t stream) {
 // launch records the plan's done event itself at the kernel's end (no
 // separate marker on the stream), unless it already records a timing stop.
 LaunchEvents last_launch(bifattn_plan_s* P, LaunchEvents ev) {
-  if (!ev.stop) {
+  if (!ev.stop && P->done_ev) {
     ev.stop = P->done_ev;
     P->done_recorded = true;
   }
@@ -407,6 +449,9 @@ const char* bifattn_status_string(bifattn_status_t s) {
     case BIFATTN_EHIP: return "HIP runtime error";
     case BIFATTN_ELENS: return "a decode length was outside [0, m_d_max] and was clamped";
     case BIFATTN_ESCALE: return "a key or value scale was not a positive normal float";
+    case BIFATTN_ESCRATCH:
+      return "the workspace of this problem exceeds the fixed scratch buffer of "
+             "bifattn_decode_noalloc (64 MiB)";
   }
   return "unknown status";
 }
@@ -432,22 +477,8 @@ bifattn_status_t bifattn_plan_create(const bifattn_dims_t* dims, bifattn_plan_t*
     delete P;
     return BIFATTN_EHIP;
   }
-  const bifattn_dims_t& d = P->dims;
-  const size_t D = (size_t)d.d;
-  const size_t ctx_rows = (size_t)d.g * P->S_c * P->M;
-  const size_t dec_rows =
-      (size_t)d.b * d.g * (size_t)(P->S_d > P->S_r ? P->S_d : P->S_r) * kWaves * P->p;
-  size_t off = 0;
-  const size_t o_ctx_acc = off;
-  off = align256(off + ctx_rows * D * 4);
-  const size_t o_ctx_ml = off;
-  off = align256(off + ctx_rows * 8);
-  const size_t o_dec_acc = off;
-  off = align256(off + dec_rows * D * 4);
-  const size_t o_dec_ml = off;
-  off = align256(off + dec_rows * 8);
-  const size_t o_status = off;
-  off = align256(off + 4);
+  const WorkspaceLayout L = workspace_layout(P, true);
+  const size_t off = L.bytes;
   if (hipStreamCreateWithFlags(&P->side, hipStreamNonBlocking) != hipSuccess) {
     (void)hipGetLastError();
     delete P;
@@ -465,13 +496,7 @@ bifattn_status_t bifattn_plan_create(const bifattn_dims_t* dims, bifattn_plan_t*
       return BIFATTN_ENOMEM;
     }
   }
-  P->ws_bytes = off;
-  char* base = static_cast<char*>(P->ws);
-  P->ctx_acc = reinterpret_cast<float*>(base + o_ctx_acc);
-  P->ctx_ml = reinterpret_cast<float2*>(base + o_ctx_ml);
-  P->dec_acc = reinterpret_cast<float*>(base + o_dec_acc);
-  P->dec_ml = reinterpret_cast<float2*>(base + o_dec_ml);
-  P->status = reinterpret_cast<int*>(base + o_status);
+  set_workspace(P, P->ws, L);
   if (hipMemsetAsync(P->status, 0, 4, P->side) != hipSuccess ||
       hipStreamSynchronize(P->side) != hipSuccess ||
       hipEventCreateWithFlags(&P->done_ev, kOrderEventFlags) != hipSuccess) {
@@ -513,10 +538,14 @@ bifattn_status_t bifattn_plan_get_info(bifattn_plan_t P, bifattn_plan_info_t* in
   return BIFATTN_OK;
 }
 
-bifattn_status_t bifattn_decode_scaled(bifattn_plan_t P, const void* q, const void* Kc,
-                                       const void* Vc, const void* Kd, const void* Vd,
-                                       const int32_t* decode_lens, const float* k_scale,
-                                       const float* v_scale, float* out, hipStream_t stream) {
+namespace {
+
+// One decode step of plan P (a created plan, or the allocation-free entry
+// point's plan on the stack, whose workspace is the fixed scratch buffer).
+bifattn_status_t decode_impl(bifattn_plan_s* P, const void* q, const void* Kc, const void* Vc,
+                             const void* Kd, const void* Vd, const int32_t* decode_lens,
+                             const float* k_scale, const float* v_scale, float* out,
+                             hipStream_t stream) {
   if (!P || !q || !Kc || !Vc || !out || !on_plan_device(P, stream)) return BIFATTN_EINVAL;
   if (!aligned(k_scale, 4) || !aligned(v_scale, 4)) return BIFATTN_EALIGN;
   const bool has_dec = P->dims.m_d_max > 0;
@@ -622,6 +651,46 @@ bifattn_status_t bifattn_decode_scaled(bifattn_plan_t P, const void* q, const vo
   whole.end();
   if (cev.stop) mark_done(P, stream);
   return e == hipSuccess ? BIFATTN_OK : BIFATTN_EHIP;
+}
+
+}  // namespace
+
+bifattn_status_t bifattn_decode_scaled(bifattn_plan_t P, const void* q, const void* Kc,
+                                       const void* Vc, const void* Kd, const void* Vd,
+                                       const int32_t* decode_lens, const float* k_scale,
+                                       const float* v_scale, float* out, hipStream_t stream) {
+  return decode_impl(P, q, Kc, Vc, Kd, Vd, decode_lens, k_scale, v_scale, out, stream);
+}
+
+bifattn_status_t bifattn_decode_noalloc(const bifattn_dims_t* dims, const void* q, const void* Kc,
+                                        const void* Vc, const void* Kd, const void* Vd,
+                                        const int32_t* decode_lens, const float* k_scale,
+                                        const float* v_scale, float* out, hipStream_t stream) {
+  bifattn_status_t st = check_dims(dims);
+  if (st != BIFATTN_OK) return st;
+  // A plan on the stack: the same splits as bifattn_plan_create's (the
+  // decode launch always on the call's stream), no events, no streams, no
+  // device allocation.
+  bifattn_plan_s P;
+  P.dims = *dims;
+  P.scale = dims->scale != 0.f ? dims->scale : 1.0f / std::sqrt((float)dims->d);
+  st = plan_splits(&P, false);
+  if (st != BIFATTN_OK) return st;
+  const WorkspaceLayout L = workspace_layout(&P, false);
+  if (L.bytes > kScratchBytes) return BIFATTN_ESCRATCH;
+  if (hipGetDevice(&P.device) != hipSuccess) {
+    (void)hipGetLastError();
+    return BIFATTN_EHIP;
+  }
+  void* scratch = nullptr;
+  if (scratch_address(P.device, &scratch) != hipSuccess) {
+    (void)hipGetLastError();
+    return BIFATTN_EHIP;
+  }
+  set_workspace(&P, scratch, L);
+  st = decode_impl(&P, q, Kc, Vc, Kd, Vd, decode_lens, k_scale, v_scale, out, stream);
+  P.ws = nullptr;  // the scratch buffer is not the plan's to free
+  return st;
 }
 
 bifattn_status_t bifattn_decode(bifattn_plan_t P, const void* q, const void* Kc, const void* Vc,

@@ -121,6 +121,13 @@ hipError_t launch_append(const AppendParams& A, int d, int kv, hipStream_t strea
 // (sample, group), `tiles` 16-row query tiles per wave, output written directly.
 hipError_t launch_standard(const PartialsParams& P, int d, int kv, int tiles, hipStream_t stream,
                            const LaunchEvents& ev = {});
+// Fixed device scratch of the allocation-free entry point: one copy per
+// device, held from the library's load to the end of the process.
+constexpr size_t kScratchBytes = size_t(64) << 20;
+// Device address of `device`'s scratch copy (looked up once per device, with
+// that device current; later calls return the cached address).
+hipError_t scratch_address(int device, void** ptr);
+
 // Launch the many-row context kernel over n_ctx_blocks work-groups.
 hipError_t launch_ctx_large(const PartialsParams& P, int d, int kv, hipStream_t stream,
                             const LaunchEvents& ev = {});

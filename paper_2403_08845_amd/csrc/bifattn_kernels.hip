@@ -35,6 +35,8 @@
 #include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 
+#include <mutex>
+
 #include "bifattn_internal.h"
 
 namespace bifattn {
@@ -1313,6 +1315,33 @@ hipError_t launch_append(const AppendParams& A, int d, int kv, hipStream_t strea
     default: return hipErrorInvalidValue;
   }
 }
+// Scratch of the allocation-free entry point (partials and the status word
+// of one call). In host code `scratch` names a host-side stand-in, not the
+// device memory: its device address comes from hipGetSymbolAddress, per
+// device, and only that address is handed to kernels.
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+hipError_t scratch_address(int device, void** ptr) {
+  constexpr int kMaxDevices = 64;
+  static std::mutex mu;
+  static void* addr[kMaxDevices] = {};
+  if (device < 0 || device >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(mu);
+  if (!addr[device]) {
+    int cur = -1;
+    hipError_t e = hipGetDevice(&cur);
+    if (e != hipSuccess) return e;
+    if (cur != device) return hipErrorInvalidDevice;  // looked up with its device current
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    if (!p) return hipErrorInvalidSymbol;
+    addr[device] = p;
+  }
+  *ptr = addr[device];
+  return hipSuccess;
+}
+
 hipError_t launch_ctx_large(const PartialsParams& P, int d, int kv, hipStream_t stream,
                             const LaunchEvents& ev) {
   if (P.n_ctx_blocks == 0) return hipSuccess;
