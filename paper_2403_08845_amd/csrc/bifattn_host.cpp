@@ -23,6 +23,7 @@ struct bifattn_plan_s {
   int ctx_mode = kCtxNone;
   int dec_tiles = 1;
   int ctx_keys = 0, S_c = 0, ctx_row_blocks = 1, n_ctx_blocks = 0, n_ctx_small_blocks = 0;
+  int ctx_wide = 0;  // many-row path: waves per work-group of the 32x32 kernel, or 0
   int dec_keys = 0, S_d = 0, n_dec_blocks = 0;
   int rep_keys = 0, S_r = 0, n_rep_blocks = 0;
   int fused = 1;
@@ -121,6 +122,13 @@ int dec_chunk_keys(int64_t units, int64_t rows) {
   while (keys > 128 && units * ceil_div(rows, keys) < kCUs / 2) keys /= 2;
   return keys;
 }
+// Rounding of the many-row context chunk: the wide kernel runs 128-key
+// stages when its chunks are multiples of 128 keys, so chunks of at least
+// 1024 keys are rounded to 128.
+int ck_step(int key_step, int64_t m_c, int64_t splits) {
+  return key_step == 64 && ceil_div(m_c, splits) >= 1024 ? 128 : key_step;
+}
+
 // Keys one replicated-ablation work-group reads: `start` by default, halved
 // (down to 128) while fewer than two work-groups per CU would exist.
 int seq_keys(int64_t units, int64_t rows, int start) {
@@ -161,16 +169,39 @@ bifattn_status_t plan_splits(bifattn_plan_s* P, bool allow_fork = true) {
     // decode work-groups (the context part is bound by the matrix cores, the
     // decode part by HBM). BIFATTN_FORK=0/1 forces it off/on.
     P->ctx_mode = kCtxLarge;
-    P->ctx_row_blocks = (int)ceil_div(M, kLargeRowsPerBlock);
+    //
+    // The decode launch goes to the plan's side stream, beside the context
+    // kernel (eight 16-row waves per work-group, at two per CU, leaving room
+    // for decode work-groups), when the decode part is large (16 MiB or more)
+    // and comparable to the context part: its HBM time at ~5 TB/s above half
+    // the context's matrix time at ~1 PFLOP/s. Otherwise both parts run one
+    // after the other on the call's stream, and bf16 caches with d = 128 take
+    // the 32x32 MFMA context kernel (work-groups of eight waves of 32 rows,
+    // one per CU, from 256 rows per group, else of four, two per CU), which
+    // fills its CUs' registers and so leaves no room for decode work beside
+    // it. BIFATTN_FORK=0/1 and BIFATTN_CTX_WIDE=0/1 force either choice (d = 64
+    // and 8-bit caches always take the kernel of 16-row waves).
     const double dec_bytes = 2.0 * d.b * d.g * (double)d.m_d_max * d.d * kv_bytes(d.kv_type);
+    const double ctx_flops = 4.0 * d.h * P->ntok * d.d * (double)d.b * d.m_c;
     const int fork_env = env_switch("BIFATTN_FORK");
-    P->fork = allow_fork && d.m_d_max > 0 &&
-              (fork_env == -1 ? dec_bytes >= 16.0 * (1 << 20) : fork_env == 1);
-    int64_t splits = ceil_div(env_int("BIFATTN_CTX_WGS", P->fork ? kCUs : 2 * kCUs),
-                              (int64_t)d.g * P->ctx_row_blocks);
+    const bool big_decode = dec_bytes >= 16.0 * (1 << 20) && dec_bytes / 5e12 > 0.5 * ctx_flops / 1e15;
+    P->fork = allow_fork && d.m_d_max > 0 && (fork_env == -1 ? big_decode : fork_env == 1);
+    const int wide_env = env_switch("BIFATTN_CTX_WIDE");
+    const bool wide = d.d == 128 && d.kv_type == BIFATTN_KV_BF16 &&
+                      (wide_env == -1 ? !P->fork : wide_env == 1);
+    P->ctx_wide = wide ? (M >= 256 ? 8 : 4) : 0;
+    const int block_rows = wide ? 32 * P->ctx_wide : kLargeRowsPerBlock;
+    const int key_step = wide ? 64 : kTileKeys;  // keys per stage of the kernel's loop
+    P->ctx_row_blocks = (int)ceil_div(M, block_rows);
+    // About one work-group per CU for eight-wave work-groups, two for
+    // four-wave ones; with the side stream, one per CU either way (the
+    // decode work-groups take the rest of each CU).
+    const int per_cu = P->ctx_wide == 8 ? 1 : 2;
+    const int target = P->fork ? kCUs : per_cu * kCUs;
+    int64_t splits = ceil_div(env_int("BIFATTN_CTX_WGS", target), (int64_t)d.g * P->ctx_row_blocks);
     if (splits < 1) splits = 1;
-    const int64_t ck = round_up(ceil_div(d.m_c, splits), kTileKeys);
-    P->ctx_keys = (int)round_up(env_int("BIFATTN_CTX_KEYS", (int)ck), kTileKeys);
+    const int64_t ck = round_up(ceil_div(d.m_c, splits), ck_step(key_step, d.m_c, splits));
+    P->ctx_keys = (int)round_up(env_int("BIFATTN_CTX_KEYS", (int)ck), key_step);
   }
   P->S_c = (int)ceil_div(d.m_c, P->ctx_keys);
   P->n_ctx_blocks = P->ctx_mode == kCtxLarge ? d.g * P->S_c * P->ctx_row_blocks : 0;
@@ -565,6 +596,7 @@ bifattn_status_t decode_impl(bifattn_plan_s* P, const void* q, const void* Kc, c
   K.ctx_keys = P->ctx_keys;
   K.S_c = P->S_c;
   K.ctx_row_blocks = P->ctx_row_blocks;
+  K.ctx_wide = P->ctx_wide;
   K.dec_keys = P->dec_keys;
   K.S_d = P->S_d;
   TimedSection whole(P, BIFATTN_KERNEL_CALL, stream);

@@ -63,6 +63,8 @@ struct PartialsParams {
   int ctx_keys;           // keys per context work-group (many-row path)
   int S_c;
   int ctx_row_blocks;
+  int ctx_wide;           // many-row path: waves of 32 rows per work-group (32x32 MFMA
+                          // kernel), or 0 for the kernel of eight 16-row waves
   int dec_keys;           // keys per decode work-group
   int S_d;
   int n_ctx_blocks;       // work-groups of the many-row context path

@@ -1042,6 +1042,262 @@ ctx_large_kernel(PartialsParams P) {
 }
 
 
+// ---------------------------------------------------------------------------
+// Context part, many query rows per group, bf16 caches with d = 128, on
+// v_mfma_f32_32x32x16_bf16 (lane l, j = l % 32, h = l / 32):
+//   A (32 x 16): lane holds A[j][8h .. 8h+7]
+//   B (16 x 32): lane holds B[8h .. 8h+7][j]
+//   C (32 x 32): element v of lane l is C[8(v/4) + 4h + v%4][j]
+// Work-group (group gam, key split s, row block rb) of NW waves, each with
+// 32 query rows. Logits are computed transposed, S^T = K Q^T (A: 32 keys of
+// K, B: Q^T from registers), so a lane's 16 accumulator elements are logits
+// of its own query row j, keys 8(v/4) + 4h + v%4 of the 32-key block. The
+// value product is O^T += V^T P^T over two 16-key steps: k-step s uses the
+// lane's elements v = 8s .. 8s+7 as its P^T operand, i.e. MFMA k-slot 8h + e
+// stands for key 16s + 8(e/4) + 4h + e%4, and the V^T operand of dims
+// 32t .. 32t+31 holds the same keys, read from key-major value rows with two
+// transposing LDS reads (ds_read_b64_tr_b16: in each group of 16 lanes,
+// lane i receives element i % 4 of the 4-element chunks that lanes i/4,
+// 4 + i/4, 8 + i/4, 12 + i/4 address; lane i' of group q addresses key
+// 16s + 8r + 4(q/2) + i'/4, dims 32t + 16(q%2) + 4(i'%4), read r = 0, 1).
+// Keys stream in stages of SK (64 or 128: two or four 32-key blocks)
+// through a ring of NB stage buffers in LDS, each filled straight from memory by buffer loads to
+// LDS (lane l's 16 bytes land at the instruction's base + 16 l, so the lane
+// chooses which chunk of which row to fetch). Rows are padded in LDS, key
+// rows to 272 bytes and value rows to 288, which keeps both kinds of operand
+// reads free of bank conflicts (16 key rows of one read start 16 bytes
+// apart in the banks, the 4 value rows of one transposing read 32 bytes
+// apart) while every read address stays a per-lane base plus a constant;
+// the lanes that fill padding load from beyond the buffer's range, which
+// writes zeros without a memory access. One barrier per stage hands a
+// filled buffer to every wave and releases the oldest for refilling.
+namespace wide {
+constexpr int D = 128;
+constexpr int RB = D * 2;             // bytes per bf16 row in memory
+constexpr int KSTEPS = D / 16;        // k-steps of the logits
+constexpr int DB = D / 32;            // 32-dim blocks of the output
+constexpr int KROW = RB + 16;         // padded key row in LDS
+constexpr int VROW = RB + 32;         // padded value row in LDS
+constexpr int KSLOTS = KROW / 16;     // 17 sixteen-byte slots per key row
+constexpr int VSLOTS = VROW / 16;     // 18 per value row
+constexpr uint32_t kBeyond = 0x80000000u;  // a byte offset past any cache chunk
+}  // namespace wide
+
+typedef __attribute__((address_space(3))) void lds_void;
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef short v4i16 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ f32x16 mfma32(const u32x4& a, const u32x4& b, const f32x16& c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a),
+                                                 __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
+}
+
+template <int NW, int NB, int SK>
+__device__ __forceinline__ void ctx_wide_body(const PartialsParams& P) {
+  using wide::D;
+  using wide::RB;
+  using wide::KSTEPS;
+  using wide::DB;
+  using wide::KROW;
+  using wide::VROW;
+  using wide::KSLOTS;
+  using wide::VSLOTS;
+  using wide::kBeyond;
+  constexpr int KAREA = SK * KROW;
+  constexpr int VAREA = SK * VROW;
+  constexpr int STAGE = KAREA + VAREA;
+  constexpr int LOADS = STAGE / 1024;
+  constexpr int LPW = (LOADS + NW - 1) / NW;   // loads per wave per stage (the last ones fewer)
+  constexpr int FULL = LOADS - (LPW - 1) * NW;  // waves with LPW loads; the rest have LPW - 1
+  static_assert(STAGE % 1024 == 0 && KAREA % 1024 == 0, "stage areas are whole loads");
+  __shared__ __attribute__((aligned(1024))) unsigned char lds[NB * STAGE];
+  const int blk = xcd_logical(blockIdx.x, P.n_ctx_blocks);
+  const int rb = blk % P.ctx_row_blocks;
+  const int sg = blk / P.ctx_row_blocks;
+  const int s = sg % P.S_c, gam = sg / P.S_c;
+  const int k0 = s * P.ctx_keys;
+  const int nkeys = min(P.m_c, k0 + P.ctx_keys) - k0;
+  const int lane = threadIdx.x & 63, wave = wave_id();
+  const int j = lane & 31, h = lane >> 5;
+  const uint8_t* kchunk = P.Kc + ((size_t)gam * P.m_c + k0) * RB;
+  const uint8_t* vchunk = P.Vc + ((size_t)gam * P.m_c + k0) * RB;
+  const float sl2 = unit_scale_log2(P, gam);
+  const int M = P.M, p = P.p;
+  const int row0 = rb * (32 * NW) + wave * 32;
+  const int nload = wave < FULL ? LPW : LPW - 1;  // wave-uniform
+
+  // Byte offset, from a stage's first key, of the 16 bytes this lane loads
+  // in its u-th load of every stage (load i = wave + NW u fills LDS bytes
+  // [1024 i, 1024 i + 1024) of the stage: key rows, then value rows).
+  uint32_t loff[LPW];
+#pragma unroll
+  for (int u = 0; u < LPW; ++u) {
+    const int slot = 64 * (wave + NW * u) + lane;  // 16-byte slot of the stage
+    const bool is_v = slot >= KAREA / 16;
+    const int vs = slot - KAREA / 16;
+    const int row = is_v ? vs / VSLOTS : slot / KSLOTS;
+    const int c = is_v ? vs % VSLOTS : slot % KSLOTS;
+    loff[u] = c < 16 ? (uint32_t)(row * RB + c * 16) : kBeyond;
+  }
+  auto fetch = [&](int key0, int buf) {
+    const int rows = nkeys - key0;  // rows from the stage's first key to the chunk's end
+    const __amdgpu_buffer_rsrc_t rk = rows_rsrc(kchunk + (size_t)key0 * RB, rows, RB);
+    const __amdgpu_buffer_rsrc_t rv = rows_rsrc(vchunk + (size_t)key0 * RB, rows, RB);
+#pragma unroll
+    for (int u = 0; u < LPW; ++u) {
+      if (u < nload) {
+        const int i = wave + NW * u;  // wave-uniform
+        lds_void* dst = (lds_void*)(lds + buf * STAGE + i * 1024);
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(i < KAREA / 1024 ? rk : rv, dst, 16,
+                                                 boff(loff[u]), 0, 0, 0);
+      }
+    }
+  };
+  // This wave's loads of stage st are complete once at most the loads of
+  // the one stage issued after it are in flight (or none, at the end).
+  auto wait_stage = [&](bool last) {
+    if (last || NB == 2)
+      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    else if (nload == LPW)
+      asm volatile("s_waitcnt vmcnt(%0)" ::"n"(LPW) : "memory");
+    else
+      asm volatile("s_waitcnt vmcnt(%0)" ::"n"(LPW - 1) : "memory");
+  };
+
+  // Q^T operands: k-step ks holds dims 16ks + 8h .. +7 of query row j.
+  u32x4 qop[KSTEPS];
+  {
+    const int row = row0 + j;
+    const uint16_t* qr = nullptr;
+    if (row < M) {
+      const int i = row / p, jp = row - i * p;
+      qr = P.q + ((size_t)i * P.h + (size_t)gam * p + jp) * D;
+    }
+#pragma unroll
+    for (int ks = 0; ks < KSTEPS; ++ks)
+      qop[ks] = qr ? load16(qr + 16 * ks + 8 * h) ^ P.q_sign : u32x4{0, 0, 0, 0};
+  }
+  const int nstages = (nkeys + SK - 1) / SK;
+#pragma unroll
+  for (int t = 0; t < NB - 1; ++t)
+    if (t < nstages) fetch(t * SK, t);
+
+  // Per-lane LDS read bases (from a stage buffer's start): key operand of row
+  // j, half h; value chunk of key 4(q/2) + i'/4, dims 16(q%2) + 4(i'%4).
+  const int q4 = lane >> 4, ip = lane & 15;
+  const int kbase = j * KROW + h * 16;
+  const int vbase = KAREA + (4 * (q4 >> 1) + (ip >> 2)) * VROW + (16 * (q4 & 1) + 4 * (ip & 3)) * 2;
+
+  f32x16 acc[DB];
+#pragma unroll
+  for (int t = 0; t < DB; ++t)
+#pragma unroll
+    for (int v = 0; v < 16; ++v) acc[t][v] = 0.f;
+  float mref = kNegInf, thr = kNegInf, lsum = 0.f;
+  const bool active = row0 < M;  // wave-uniform
+
+  for (int st = 0; st < nstages; ++st) {
+    const int buf = st % NB;
+    // After this wave's wait, the barrier hands every wave's part of stage st
+    // to all waves and frees buffer (st - 1) % NB, which all have read.
+    wait_stage(st + 1 >= nstages);
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+    if (st + NB - 1 < nstages) fetch((st + NB - 1) * SK, (st + NB - 1) % NB);
+    if (!active) continue;
+    const unsigned char* kb = lds + buf * STAGE + kbase;
+    const unsigned char* vb = lds + buf * STAGE + vbase;
+    const int rem = nkeys - st * SK;  // valid keys from the stage's first
+#pragma unroll
+    for (int b = 0; b < SK / 32; ++b) {
+      // S^T block: keys 32b .. 32b+31 of the stage
+      f32x16 sacc;
+#pragma unroll
+      for (int v = 0; v < 16; ++v) sacc[v] = 0.f;
+#pragma unroll
+      for (int ks = 0; ks < KSTEPS; ++ks) {
+        const u32x4 kop = *(const lds_u32x4*)(kb + 32 * b * KROW + 32 * ks);
+        sacc = mfma32(kop, qop[ks], sacc);
+      }
+      float x[16];
+#pragma unroll
+      for (int v = 0; v < 16; ++v) x[v] = sacc[v];
+      if (rem < 32 * (b + 1)) {
+        const int nv = __builtin_amdgcn_readfirstlane(rem) - 32 * b;
+#pragma unroll
+        for (int v = 0; v < 16; ++v)
+          if (8 * (v / 4) + 4 * h + (v & 3) >= nv) x[v] = kNegInf;
+      }
+      float lmax = x[0];
+#pragma unroll
+      for (int v = 1; v < 16; ++v) lmax = fmaxf(lmax, x[v]);
+      if (__any(lmax > thr)) {
+        const float tmax = xor32_max(lmax) * sl2;  // the row's maximum over the block
+        const bool raise = tmax > mref + kRescaleSlack;
+        const float alpha = raise ? exp2_fast(mref - tmax) : 1.f;
+        lsum *= alpha;
+#pragma unroll
+        for (int t = 0; t < DB; ++t) acc[t] *= alpha;
+        mref = raise ? tmax : mref;
+        thr = (mref + kRescaleSlack) / sl2;
+      }
+      const float nbase = mref == kNegInf ? 0.f : -mref;
+      float pr[16];
+#pragma unroll
+      for (int v = 0; v < 16; ++v) pr[v] = exp2_fast(__builtin_fmaf(x[v], sl2, nbase));
+      float ps = pr[0];
+#pragma unroll
+      for (int v = 1; v < 16; ++v) ps += pr[v];
+      lsum += ps;
+      u32x4 pb[2];
+#pragma unroll
+      for (int ss = 0; ss < 2; ++ss)
+#pragma unroll
+        for (int w = 0; w < 4; ++w) pb[ss][w] = pack_bf16(pr[8 * ss + 2 * w], pr[8 * ss + 2 * w + 1]);
+      // O^T += V^T P^T, dims 32t .. 32t+31, keys of k-step ss
+#pragma unroll
+      for (int ss = 0; ss < 2; ++ss) {
+#pragma unroll
+        for (int t = 0; t < DB; ++t) {
+          u32x4 vop;
+#pragma unroll
+          for (int r = 0; r < 2; ++r) {
+            const v4i16 y = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                (__attribute__((address_space(3))) v4i16*)(const_cast<unsigned char*>(
+                    vb + (32 * b + 16 * ss + 8 * r) * VROW + 64 * t)));
+            const u32x2 w2 = __builtin_bit_cast(u32x2, y);
+            vop[2 * r] = w2[0];
+            vop[2 * r + 1] = w2[1];
+          }
+          acc[t] = mfma32(vop, pb[ss], acc[t]);
+        }
+      }
+    }
+  }
+
+  if (!active) return;
+  const float ltot = xor32_sum(lsum);
+  const int row = row0 + j;
+  if (row < M) {
+    const size_t prow = ((size_t)gam * P.S_c + s) * P.M + row;
+    float* dst = P.ctx_acc + prow * D;
+#pragma unroll
+    for (int t = 0; t < DB; ++t)
+#pragma unroll
+      for (int g4 = 0; g4 < 4; ++g4)
+        *reinterpret_cast<f32x4*>(dst + 32 * t + 8 * g4 + 4 * h) =
+            f32x4{acc[t][4 * g4], acc[t][4 * g4 + 1], acc[t][4 * g4 + 2], acc[t][4 * g4 + 3]};
+    if (h == 0) P.ctx_ml[prow] = float2{mref, ltot};
+  }
+}
+
+template <int NW, int NB, int SK>
+__global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(2))) void
+ctx_wide_kernel(PartialsParams P) {
+  ctx_wide_body<NW, NB, SK>(P);
+}
+
+
 // Grid: n_ctx_small_blocks work-groups of the few-row context path, then
 // n_dec_blocks decode work-groups (the many-row context path has a kernel of
 // its own).
@@ -1345,6 +1601,17 @@ hipError_t scratch_address(int device, void** ptr) {
 hipError_t launch_ctx_large(const PartialsParams& P, int d, int kv, hipStream_t stream,
                             const LaunchEvents& ev) {
   if (P.n_ctx_blocks == 0) return hipSuccess;
+  if (P.ctx_wide) {
+    if (d != 128 || kv != kKvBf16) return hipErrorInvalidValue;
+    // eight waves: 128-key stages, two in LDS (fewer barriers than 64-key
+    // stages, measured 3-5% faster); chunks of a multiple of 64 keys
+    if (P.ctx_wide == 8)
+      return P.ctx_keys % 128 == 0
+                 ? launch(ctx_wide_kernel<8, 2, 128>, P.n_ctx_blocks, 512, stream, ev, P)
+                 : launch(ctx_wide_kernel<8, 3, 64>, P.n_ctx_blocks, 512, stream, ev, P);
+    if (P.ctx_wide == 4) return launch(ctx_wide_kernel<4, 2, 64>, P.n_ctx_blocks, 256, stream, ev, P);
+    return hipErrorInvalidValue;
+  }
   if (d == 128) return launch_ctx_large_d<128>(P, kv, stream, ev);
   if (d == 64) return launch_ctx_large_d<64>(P, kv, stream, ev);
   return hipErrorInvalidValue;

@@ -279,6 +279,9 @@ def test_side_stream_decode(case, monkeypatch):
     x = workloads.make_inputs(b, h, g, d, m_c, m_d, seed=1200 + m_c, ragged=True, n=n)
     ref = oracle.attention(**x)
     runs = []
+    # the same context kernel both ways (by default a plan without the side
+    # stream may take the 32x32 MFMA kernel instead)
+    monkeypatch.setenv("BIFATTN_CTX_WIDE", "0")
     for fork in ("0", "1"):
         monkeypatch.setenv("BIFATTN_FORK", fork)
         with bif.Plan(b, h, g, d, m_c, m_d, n=n) as plan:
@@ -342,3 +345,33 @@ def test_split_launch_equals_fused(case, monkeypatch):
     split = run_decode(x)
     assert np.array_equal(fused, split)
     _report(f"split launch {case}", *assert_parity(split, oracle.attention(**x), str(case), x=x))
+
+
+# Many-row context shapes for both context kernels (the 32x32 MFMA kernel of
+# 32-row waves, and the kernel of 16-row waves): 128- and 64-key stages,
+# ragged last chunks, row blocks whose last waves hold no rows, several
+# tokens, grouped heads, and four-wave work-groups (fewer than 256 rows).
+WIDE_CASES = [
+    # b, h, g, d, m_c, m_d_max, n
+    (48, 32, 1, 128, 50000, 64, 1),   # 1280-key chunks: 128-key stages, ragged last chunk
+    (48, 32, 1, 128, 4000, 64, 1),    # 128-key chunks: 64-key stages
+    (37, 16, 2, 128, 3000, 50, 1),    # 296 rows per group: an idle wave in the last row block
+    (20, 16, 1, 128, 2500, 40, 2),    # two tokens per sample
+    (64, 32, 8, 128, 6000, 200, 1),   # grouped heads, 256 rows per group
+    (5, 32, 1, 128, 1777, 30, 1),     # 160 rows: four-wave work-groups
+]
+
+
+@pytest.mark.parametrize("case", WIDE_CASES, ids=lambda c: "b%d_h%d_g%d_d%d_mc%d_md%d_n%d" % c)
+def test_many_row_context_kernels(case, monkeypatch):
+    b, h, g, d, m_c, m_d, n = case
+    x = workloads.make_inputs(b, h, g, d, m_c, m_d, seed=1600 + m_c, ragged=True, n=n)
+    ref = oracle.attention(**x)
+    monkeypatch.setenv("BIFATTN_FORK", "0")
+    for wide in ("1", "0"):
+        monkeypatch.setenv("BIFATTN_CTX_WIDE", wide)
+        with bif.Plan(b, h, g, d, m_c, m_d, n=n, path="bifurcated") as plan:
+            info = plan.info()
+            print(f"[case] many-row {case} wide={wide} {info}", flush=True)
+            out = run_decode(x, plan=plan)
+        _report(f"many-row {case} wide={wide}", *assert_parity(out, ref, f"{case} wide={wide}", x=x))
