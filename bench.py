@@ -164,7 +164,8 @@ def calibrate_copy(reps: int = 5):
     log(f"[bench] copy-equivalent kernel over {COPY_BYTES} bytes, {reps} times")
 
 
-KERNEL_NAMES = {"partials": "partials_kernel", "ctx_large": "ctx_large_kernel"}
+KERNEL_NAMES = {"partials": "partials_kernel", "ctx_large": "ctx_large_kernel",
+                "ctx_wide": "ctx_wide_kernel"}
 
 
 def summarize_profile(stats_dir: str, fetch_dir: str, write_dir: str, workload: str, out_dir: str,
@@ -236,8 +237,48 @@ def summarize_profile(stats_dir: str, fetch_dir: str, write_dir: str, workload: 
     lines += ["", f"HBM traffic of `{pname}` per launch (FETCH_SIZE / WRITE_SIZE, scaled by a "
               f"{COPY_BYTES}-byte copy: fetch x{f_scale:.4f}, write x{w_scale:.4f}): "
               f"{fetch_b / 1e6:.2f} MB read, {write_b / 1e6:.2f} MB written."]
+    alg = algorithmic_read_bytes(workload, kernel)
+    if alg:
+        what, nbytes = alg
+        lines += ["", f"Algorithmic bytes this kernel must read ({what}): {nbytes / 1e6:.2f} MB; "
+                  f"measured read / algorithmic = {fetch_b / nbytes:.3f}."]
+    head = [f"# {kname}, {workload}", "",
+            "Commands (repository root, one MI355X, after `cd /tmp && export TMPDIR=/tmp`; "
+            "the directories hold the raw rocprofv3 output):", "", "```",
+            f"rocprofv3 --kernel-trace --stats -d {stats_dir} -o run --output-format csv "
+            f"-- python -u bench.py --workload {workload} --steps {steps} --warmup {warmup} "
+            f"--no-cpu-baseline --no-ablation",
+            f"rocprofv3 --pmc FETCH_SIZE -d {fetch_dir} -o run --output-format csv -- python -u "
+            f"bench.py --workload {workload} --steps 5 --warmup 2 --no-cpu-baseline --no-ablation "
+            f"--calibrate-copy",
+            f"rocprofv3 --pmc WRITE_SIZE -d {write_dir} -o run --output-format csv -- python -u "
+            f"bench.py --workload {workload} --steps 5 --warmup 2 --no-cpu-baseline --no-ablation "
+            f"--calibrate-copy",
+            f"python bench.py --workload {workload} --steps {steps} --warmup {warmup} --kernel {kernel} "
+            f"--summarize-profile {stats_dir} {fetch_dir} {write_dir} {out_dir}",
+            "```", ""]
+    open(os.path.join(out_dir, f"{kernel}_{workload}.md"), "w").write("\n".join(head + lines) + "\n")
     print("\n".join(lines))
     return lines
+
+
+def algorithmic_read_bytes(workload: str, kernel: str):
+    """(description, bytes) of the KV a kernel must read once for the
+    workload: the context chunk of every group for the many-row context
+    kernels, the valid decode rows for the decode launch of a many-row plan,
+    both for the few-row partial launch; None for unknown workloads."""
+    w = workloads.WORKLOADS.get(workload)
+    if w is None:
+        return None
+    es = workloads.KV_BYTES[w.kv]
+    ctx = 2 * es * w.g * w.d * w.m_c
+    if kernel in ("ctx_large", "ctx_wide"):
+        return "one copy of the context K and V", ctx
+    lens = workloads.make_workload_lens(w)
+    dec = 2 * es * w.g * w.d * int(np.sum(lens, dtype=np.int64))
+    if w.b * (w.h // w.g) * w.n > 64:
+        return "every sample's valid decode K and V", dec
+    return "one copy of the context K and V plus every sample's valid decode K and V", ctx + dec
 
 
 def summarize_stats(stats_dir: str, workload: str, out_dir: str):
@@ -437,10 +478,11 @@ def main():
     if many_rows and (dec_us is None or ctx_us >= dec_us):
         # The many-row context kernel: a contraction over b*p*n rows per group.
         tflops = ctx_flops / (ctx_us * 1e-6) / 1e12
-        roofline = {"kernel": "ctx_large_kernel (many-row context partials)", "bound": "mfma",
+        ck = "ctx_wide" if info.get("ctx_kernel") == 2 else "ctx_large"
+        roofline = {"kernel": f"{KERNEL_NAMES[ck]} (many-row context partials)", "bound": "mfma",
                     "achieved": round(tflops, 1), "peak": MFMA_PEAK_TFLOPS, "unit": "TFLOP/s",
                     "frac": round(tflops / MFMA_PEAK_TFLOPS, 4),
-                    "traffic": measured_traffic(w.name, "ctx_large"),
+                    "traffic": measured_traffic(w.name, ck),
                     "avg_launch_us": round(ctx_us, 3), "flops_per_launch": ctx_flops,
                     "bytes_per_launch": ctx_bytes}
     elif many_rows:

@@ -132,6 +132,10 @@ typedef struct {
   int32_t path;               /* the path bifattn_decode runs: BIFATTN_PATH_BIFURCATED or
                                  BIFATTN_PATH_STANDARD */
   size_t workspace_bytes;     /* device memory the plan owns */
+  int32_t ctx_kernel;         /* context work-groups: 0 in the partial launch (few rows per
+                                 group, or none), 1 many-row kernel of 16-row waves, 2 many-row
+                                 32x32 MFMA kernel of 32-row waves */
+  int32_t side_stream;        /* 1 when the decode launch runs on the plan's side stream */
 } bifattn_plan_info_t;
 
 /* Kernels a plan launches; used to select what bifattn_plan_set_timing times. */

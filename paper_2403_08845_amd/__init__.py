@@ -53,7 +53,8 @@ class PlanInfo(ctypes.Structure):
                 ("dec_keys_per_block", ctypes.c_int32), ("dec_splits", ctypes.c_int32),
                 ("dec_blocks", ctypes.c_int32),
                 ("fused", ctypes.c_int32), ("path", ctypes.c_int32),
-                ("workspace_bytes", ctypes.c_size_t)]
+                ("workspace_bytes", ctypes.c_size_t), ("ctx_kernel", ctypes.c_int32),
+                ("side_stream", ctypes.c_int32)]
 
     def as_dict(self):
         return {name: getattr(self, name) for name, _ in self._fields_}

@@ -566,6 +566,8 @@ bifattn_status_t bifattn_plan_get_info(bifattn_plan_t P, bifattn_plan_info_t* in
   info->fused = P->fused;
   info->path = P->path;
   info->workspace_bytes = P->ws_bytes;
+  info->ctx_kernel = P->ctx_mode != kCtxLarge ? 0 : (P->ctx_wide ? 2 : 1);
+  info->side_stream = P->fork;
   return BIFATTN_OK;
 }
 

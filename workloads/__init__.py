@@ -186,6 +186,14 @@ def make_workload_inputs(w: Workload, *, seed=None, poison_tail=False):
                        poison_tail=poison_tail, n=w.n, kv=w.kv)
 
 
+def make_workload_lens(w: Workload) -> np.ndarray:
+    """The workload's decode lengths (ragged ones come after the tensors in
+    the draw order, so those are drawn in full)."""
+    if not w.ragged:
+        return np.full(w.b, w.m_d_max, dtype=np.int32)
+    return make_workload_inputs(w)["lens"]
+
+
 def first_samples(x, nb):
     """The inputs of the first nb samples (the shared context unchanged)."""
     y = dict(x)
