@@ -682,6 +682,11 @@ __device__ void decode_block(const PartialsParams& P, int blk, int wave, int lan
   A.load(rk, rv, k0, lane);  // first tile in flight before the length is known
   const int total = P.len_offset + clamp_len(P.lens, i, P.m_d_max);
   const int k1 = min(total, kcap);
+  // Now that the length is known, later loads (the prefetch of each wave's
+  // next tile included) stop at the sample's last valid row: past it they
+  // return zeros without touching memory, so the masked tail is never read.
+  const __amdgpu_buffer_rsrc_t rk1 = rows_rsrc(P.Kd + cache, k1, RB);
+  const __amdgpu_buffer_rsrc_t rv1 = rows_rsrc(P.Vd + cache, k1, RB);
   const uint16_t* qbase = P.q + ((size_t)i * P.h + (size_t)gam * P.p) * D;
   const int p = P.p;
   stage_q<D, NT>(qw, [&](int r) -> const uint16_t* { return r < p ? qbase + (size_t)r * D : nullptr; },
@@ -690,7 +695,7 @@ __device__ void decode_block(const PartialsParams& P, int blk, int wave, int lan
   st.init();
   // Keys [k0, k1) of this chunk; the causal limits of the tokens count from
   // the end of the sequence (total), which may lie in a later chunk.
-  stream_keys<D, NT, KV>(st, qw, kl, rk, rv, A, k0, k1, total, kWaves * kTileKeys, P.ntok,
+  stream_keys<D, NT, KV>(st, qw, kl, rk1, rv1, A, k0, k1, total, kWaves * kTileKeys, P.ntok,
                          P.len_offset, unit_scale_log2(P, gam), lane);
   const size_t prow = ((size_t)blk * kWaves + wave) * P.p;
   store_partials<D, NT>(st, p, P.dec_acc + prow * D, P.dec_ml + prow, lane);
