@@ -5,8 +5,8 @@
 
 A step is one bifattn_decode call (context partials, decode partials and the
 combine) over one batch of seeded synthetic inputs that are already resident
-in HBM (bifattn_decode_scaled for the workloads with 8-bit KV caches, whose
-bytes count one per element). Steps rotate over several device copies of the inputs (about 1.2 GB
+in HBM (bifattn_decode_scaled for the workloads with 8-bit or 4-bit KV
+caches, whose bytes count one or one half per element). Steps rotate over several device copies of the inputs (about 1.2 GB
 or more in total) so that no step finds its KV cache in the 256 MB Infinity
 Cache left behind by the previous one. The timed region is bracketed by
 torch.cuda.synchronize() on both sides.
@@ -270,12 +270,12 @@ def algorithmic_read_bytes(workload: str, kernel: str):
     w = workloads.WORKLOADS.get(workload)
     if w is None:
         return None
-    es = workloads.KV_BYTES[w.kv]
-    ctx = 2 * es * w.g * w.d * w.m_c
+    rb = workloads.row_bytes(w.d, w.kv)
+    ctx = 2 * rb * w.g * w.m_c
     if kernel in ("ctx_large", "ctx_wide"):
         return "one copy of the context K and V", ctx
     lens = workloads.make_workload_lens(w)
-    dec = 2 * es * w.g * w.d * int(np.sum(lens, dtype=np.int64))
+    dec = 2 * rb * w.g * int(np.sum(lens, dtype=np.int64))
     if w.b * (w.h // w.g) * w.n > 64:
         return "every sample's valid decode K and V", dec
     return "one copy of the context K and V plus every sample's valid decode K and V", ctx + dec
@@ -440,7 +440,7 @@ def main():
     if not args.no_ablation:
         # Replicated cache built on the device: every sample's own copy of the context.
         rows = w.m_c + w.m_d_max
-        rep_bytes = 2 * w.b * w.g * rows * w.d * workloads.KV_BYTES[w.kv]
+        rep_bytes = 2 * w.b * w.g * rows * workloads.row_bytes(w.d, w.kv)
         if rep_bytes < 40e9:
             K = torch.cat([dev0["Kc"].unsqueeze(0).expand(w.b, -1, -1, -1), dev0["Kd"]], dim=2).contiguous()
             V = torch.cat([dev0["Vc"].unsqueeze(0).expand(w.b, -1, -1, -1), dev0["Vd"]], dim=2).contiguous()
@@ -471,8 +471,7 @@ def main():
         cpu = cpu_baseline(x, w, args.cpu_seconds)
 
     value = B_kv / (ms_per_step * 1e-3) / 1e9
-    es = workloads.KV_BYTES[w.kv]
-    ctx_bytes = 2 * es * w.g * w.d * w.m_c
+    ctx_bytes = 2 * workloads.row_bytes(w.d, w.kv) * w.g * w.m_c
     dec_bytes = B_kv - ctx_bytes
     ctx_flops = 4 * w.h * w.n * w.d * w.b * w.m_c
     if many_rows and (dec_us is None or ctx_us >= dec_us):

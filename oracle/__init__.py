@@ -17,9 +17,12 @@ Their agreement to ~1e-12 is the paper's exactness claim (Section 4.2,
 Appendix E.1), checked in ``tests/test_oracle_pins.py``.
 
 Caches may hold 8-bit codes (``kv="fp8_e4m3"`` or ``kv="int8"``, arrays of
-uint8 bit patterns) with per-group fp32 ``k_scale`` / ``v_scale`` [g]: the
-key of a row is ``k_scale[gam]`` times the code's value (the FAQ on
-attention quantization; the reading is spelled out in ``oracle.c``).
+uint8 bit patterns) or 4-bit codes (``kv="int4"``, two per byte: uint8
+arrays whose last axis is d/2, element 2u in the low nibble of byte u and
+element 2u+1 in the high nibble) with per-group fp32 ``k_scale`` /
+``v_scale`` [g]: the key of a row is ``k_scale[gam]`` times the code's value
+(the FAQ on attention quantization; the reading is spelled out in
+``oracle.c``).
 """
 from __future__ import annotations
 
@@ -37,8 +40,10 @@ _lib = None
 _ERRORS = {-1: "invalid dimensions or row index", -4: "out of memory",
            -6: "decode length outside [0, m_d_max]"}
 
-#: Cache element types: name -> (code of oracle.c, numpy dtype of the stored bits).
-KV_TYPES = {"bf16": (0, np.uint16), "fp8_e4m3": (1, np.uint8), "int8": (2, np.uint8)}
+#: Cache element types: name -> (code of oracle.c, numpy dtype of the stored
+#: bits, elements per stored item).
+KV_TYPES = {"bf16": (0, np.uint16, 1), "fp8_e4m3": (1, np.uint8, 1), "int8": (2, np.uint8, 1),
+            "int4": (3, np.uint8, 2)}
 
 
 def build(force: bool = False) -> str:
@@ -83,7 +88,7 @@ def _prep(q, Kc, Vc, Kd, Vd, lens, kv="bf16", k_scale=None, v_scale=None):
     """q is [b, h, d] (one new token per sample) or [b, h, n, d] (n new tokens)."""
     if kv not in KV_TYPES:
         raise ValueError(f"unknown cache type {kv!r}")
-    code, dt = KV_TYPES[kv]
+    code, dt, per = KV_TYPES[kv]
     q = np.ascontiguousarray(q, dtype=np.uint16)
     caches = []
     for x in (Kc, Vc, Kd, Vd):
@@ -100,7 +105,7 @@ def _prep(q, Kc, Vc, Kd, Vd, lens, kv="bf16", k_scale=None, v_scale=None):
         b, h, n, d = q.shape
     g, m_c, d2 = Kc.shape
     b2, g2, m_d_max, d3 = Kd.shape
-    if not (d == d2 == d3 and b == b2 and g == g2 and Vc.shape == Kc.shape
+    if not (d == d2 * per == d3 * per and b == b2 and g == g2 and Vc.shape == Kc.shape
             and Vd.shape == Kd.shape and lens.shape == (b,)):
         raise ValueError("inconsistent shapes")
     scales = []
@@ -191,12 +196,18 @@ def widen_bf16(bits) -> np.ndarray:
 def widen_codes(codes, kv: str) -> np.ndarray:
     """Cache codes -> exact unscaled fp64 values (numpy; independent of
     oracle.c's decoder). fp8 e4m3 follows the OCP definition: bias 7,
-    exponent 0 subnormal, S.1111.111 NaN, no infinities."""
+    exponent 0 subnormal, S.1111.111 NaN, no infinities. int4 unpacks the
+    last axis (d/2 bytes -> d values, low nibble first), each nibble two's
+    complement."""
     if kv == "bf16":
         return widen_bf16(codes)
     c = np.asarray(codes).view(np.uint8)
     if kv == "int8":
         return c.view(np.int8).astype(np.float64)
+    if kv == "int4":
+        nib = np.stack([c & 15, c >> 4], axis=-1).astype(np.int64)  # [..., d/2, 2]
+        vals = np.where(nib >= 8, nib - 16, nib).astype(np.float64)
+        return vals.reshape(c.shape[:-1] + (2 * c.shape[-1],))
     if kv != "fp8_e4m3":
         raise ValueError(f"unknown cache type {kv!r}")
     e = ((c >> 3) & 15).astype(np.int64)

@@ -25,7 +25,7 @@ concatenated values (an empty part has ``mu = -inf`` and drops out). Rows a
 token does not see are excluded before any arithmetic, so whatever they hold
 (NaN included) cannot reach the result. Scale: ``1/sqrt(k)`` by default.
 
-With 8-bit caches (the FAQ on attention quantization) every cache is first
+With 8-bit or 4-bit caches (the FAQ on attention quantization) every cache is first
 widened to its values: code value times the per-group scale of keys or
 values (``widen_codes``, a numpy decoder of its own).
 

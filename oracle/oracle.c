@@ -36,13 +36,17 @@
  * a token does not see are never read. Outputs are fp64.
  *
  * Quantized caches (the FAQ on attention quantization: 8-bit KV halves the
- * KV bytes and leaves the method unchanged). Reading: a cache may hold 8-bit
- * codes instead of bf16, with one fp32 scale per KV group for keys and one
- * for values, shared by the context and decode caches of that group (the
- * decode cache continues the context's sequence, so one static scale serves
- * both). The key (value) of a row is k_scale[gam] (v_scale[gam]) times the
- * code's value:
+ * KV bytes, 4-bit KV quarters them, and the method is unchanged). Reading: a
+ * cache may hold 8-bit or 4-bit codes instead of bf16, with one fp32 scale
+ * per KV group for keys and one for values, shared by the context and
+ * decode caches of that group (the decode cache continues the context's
+ * sequence, so one static scale serves both). The key (value) of a row is
+ * k_scale[gam] (v_scale[gam]) times the code's value:
  *   int8      two's complement integer in [-128, 127]
+ *   int4      two's complement integer in [-8, 7], two codes per byte:
+ *             element u of a row is in byte u/2 of the row, even u in the
+ *             low nibble (bits 0-3), odd u in the high nibble (bits 4-7);
+ *             a row of d elements is d/2 bytes (d even)
  *   fp8 e4m3  OCP 8-bit float E4M3 (sign, 4-bit exponent with bias 7, 3-bit
  *             mantissa; exponent 0 is subnormal, m/8 * 2^-6; all-ones
  *             exponent and mantissa is NaN; no infinities; largest 448)
@@ -53,7 +57,9 @@
  * Parity pins for this file live in tests/test_oracle_pins.py (closed forms,
  * invariants, brute force, and agreement with an independent numpy
  * evaluation of the bifurcated Eq. 3-4) and tests/test_oracle_kvquant.py
- * (code tables against torch's float8 conversion, scale identities).
+ * (code tables against torch's float8 conversion, numpy's int8 view and an
+ * unpackbits table of the int4 codes; scale identities; int4 against int8 of
+ * sixteen times the codes).
  */
 #include <math.h>
 #include <stdint.h>
@@ -71,6 +77,7 @@
 #define KV_BF16 0
 #define KV_FP8_E4M3 1
 #define KV_INT8 2
+#define KV_INT4 3
 
 static double widen_bf16(uint16_t bits) {
   uint32_t u = (uint32_t)bits << 16;
@@ -88,16 +95,28 @@ static double fp8_e4m3_value(uint8_t c) {
   return sgn ? -mag : mag;
 }
 
-/* Unscaled value of element idx of a cache stored as kv_type. */
+/* Two's complement value of a 4-bit code (its bit 3 weighs -8). */
+static double int4_value(unsigned nibble) {
+  const int v = (int)(nibble & 7u) - ((nibble & 8u) ? 8 : 0);
+  return (double)v;
+}
+
+/* Unscaled value of element idx of a cache stored as kv_type (idx counts
+ * elements; for int4 it selects a nibble of byte idx/2). */
 static double code_value(int kv_type, const void *base, size_t idx) {
   switch (kv_type) {
     case KV_FP8_E4M3: return fp8_e4m3_value(((const uint8_t *)base)[idx]);
     case KV_INT8: return (double)(int8_t)((const uint8_t *)base)[idx];
+    case KV_INT4: {
+      const uint8_t byte = ((const uint8_t *)base)[idx >> 1];
+      return int4_value((idx & 1) ? (unsigned)(byte >> 4) : (unsigned)(byte & 15u));
+    }
     default: return widen_bf16(((const uint16_t *)base)[idx]);
   }
 }
 
-/* Decoded value of one code (for the pins of the code tables). */
+/* Decoded value of one code (for the pins of the code tables); an int4 code
+ * is the low nibble of `code`. */
 double oracle_code_value(int kv_type, int code) {
   if (kv_type == KV_BF16) return widen_bf16((uint16_t)code);
   return code_value(kv_type, &(uint8_t){(uint8_t)code}, 0);
@@ -157,7 +176,9 @@ static int visible(int len, int n, int r) {
 static int check_dims(int b, int h, int g, int d, int m_c, int m_d_max, int n, int kv_type,
                       const int32_t *lens) {
   if (b < 1 || h < 1 || g < 1 || d < 1 || m_c < 0 || m_d_max < 0 || n < 1) return ORACLE_EINVAL;
-  if (kv_type != KV_BF16 && kv_type != KV_FP8_E4M3 && kv_type != KV_INT8) return ORACLE_EINVAL;
+  if (kv_type != KV_BF16 && kv_type != KV_FP8_E4M3 && kv_type != KV_INT8 && kv_type != KV_INT4)
+    return ORACLE_EINVAL;
+  if (kv_type == KV_INT4 && d % 2) return ORACLE_EINVAL; /* whole bytes per row */
   if (h % g) return ORACLE_EINVAL;
   for (int i = 0; i < b; ++i)
     if (lens[i] < 0 || lens[i] > m_d_max) return ORACLE_ELENS;

@@ -48,34 +48,44 @@ static int failures = 0;
     }                                 \
   } while (0)
 
+/* Bytes that hold n elements of cache type kv. */
+static size_t cache_bytes(int kv, size_t n) { return kv == 0 ? 2 * n : (kv == 3 ? n / 2 : n); }
+
+/* Value of element idx of a cache of type kv (int4: nibble idx % 2 of byte idx / 2). */
+static double elem_value(int kv, const unsigned char *base, size_t idx) {
+  if (kv == 0) return oracle_code_value(0, ((const uint16_t *)base)[idx]);
+  if (kv == 3) return oracle_code_value(3, (base[idx / 2] >> (4 * (idx % 2))) & 15);
+  return oracle_code_value(kv, base[idx]);
+}
+
 /* One problem: fills the inputs, runs the full and the row evaluations. */
 static void run_case(int b, int h, int g, int d, int m_c, int m_d, int n, int kv, int zero_q) {
-  const int es = kv == 0 ? 2 : 1;
   const size_t nq = (size_t)b * h * n * d, nc = (size_t)g * m_c * d,
                nd = (size_t)b * g * m_d * d;
+  const size_t bc = cache_bytes(kv, nc), bd = cache_bytes(kv, nd);
   uint16_t *q = malloc(nq * 2);
-  unsigned char *Kc = malloc(nc * es + 1), *Vc = malloc(nc * es + 1);
-  unsigned char *Kd = malloc(nd * es + 1), *Vd = malloc(nd * es + 1);
+  unsigned char *Kc = malloc(bc + 1), *Vc = malloc(bc + 1);
+  unsigned char *Kd = malloc(bd + 1), *Vd = malloc(bd + 1);
   int32_t *lens = malloc(sizeof(int32_t) * b);
   float *ks = malloc(sizeof(float) * g), *vs = malloc(sizeof(float) * g);
   double *out = malloc(sizeof(double) * nq);
   for (size_t i = 0; i < nq; ++i) q[i] = zero_q ? 0 : bf16_of(rnd());
-  for (size_t i = 0; i < nc; ++i) {
+  for (size_t i = 0; i < (kv == 0 ? nc : bc); ++i) {
     if (kv == 0) {
       ((uint16_t *)Kc)[i] = bf16_of(rnd());
       ((uint16_t *)Vc)[i] = bf16_of(rnd());
     } else {
-      Kc[i] = (unsigned char)(next() % 120);
-      Vc[i] = (unsigned char)(next() % 120);
+      Kc[i] = (unsigned char)(next() % (kv == 3 ? 256 : 120));
+      Vc[i] = (unsigned char)(next() % (kv == 3 ? 256 : 120));
     }
   }
-  for (size_t i = 0; i < nd; ++i) {
+  for (size_t i = 0; i < (kv == 0 ? nd : bd); ++i) {
     if (kv == 0) {
       ((uint16_t *)Kd)[i] = bf16_of(rnd());
       ((uint16_t *)Vd)[i] = bf16_of(rnd());
     } else {
-      Kd[i] = (unsigned char)(next() % 120);
-      Vd[i] = (unsigned char)(next() % 120);
+      Kd[i] = (unsigned char)(next() % (kv == 3 ? 256 : 120));
+      Vd[i] = (unsigned char)(next() % (kv == 3 ? 256 : 120));
     }
   }
   for (int i = 0; i < b; ++i) lens[i] = m_d ? (int)(next() % (m_d + 1)) : 0;
@@ -100,13 +110,10 @@ static void run_case(int b, int h, int g, int d, int m_c, int m_d, int n, int kv
           for (int u = 0; u < d; ++u) {
             double s = 0.0;
             for (int t = 0; t < m_c; ++t)
-              s += (vp ? vp[gam] : 1.0) *
-                   (kv ? oracle_code_value(kv, Vc[((size_t)gam * m_c + t) * d + u])
-                       : oracle_code_value(0, ((uint16_t *)Vc)[((size_t)gam * m_c + t) * d + u]));
+              s += (vp ? vp[gam] : 1.0) * elem_value(kv, Vc, ((size_t)gam * m_c + t) * d + u);
             for (int t = 0; t < vis; ++t) {
               const size_t idx = (((size_t)i * g + gam) * m_d + t) * d + u;
-              s += (vp ? vp[gam] : 1.0) *
-                   (kv ? oracle_code_value(kv, Vd[idx]) : oracle_code_value(0, ((uint16_t *)Vd)[idx]));
+              s += (vp ? vp[gam] : 1.0) * elem_value(kv, Vd, idx);
             }
             const double mean = s / (m_c + vis);
             const double got = out[(((size_t)i * h + j) * n + r) * d + u];
@@ -157,6 +164,8 @@ int main(void) {
   run_case(2, 6, 3, 8, 7, 0, 1, 0, 1);    /* no decode cache */
   run_case(3, 4, 4, 8, 9, 5, 2, 1, 0);    /* fp8 codes with scales */
   run_case(3, 4, 2, 8, 9, 5, 2, 2, 1);    /* int8 codes with scales */
+  run_case(3, 4, 2, 8, 9, 5, 2, 3, 0);    /* int4 codes with scales */
+  run_case(2, 6, 3, 6, 7, 3, 1, 3, 1);    /* int4, mean pin */
   for (int c = 0; c < 256; ++c) {
     const double v = oracle_code_value(1, c);
     CHECK(isnan(v) == ((c & 0x7f) == 0x7f), "fp8 code %d", c);

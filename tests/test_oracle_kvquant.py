@@ -1,5 +1,5 @@
-"""Oracle over 8-bit KV caches against its pins (CPU only); planted mistakes in
-the decoding or the scales each fail a pin."""
+"""Oracle over 8-bit and 4-bit KV caches against its pins (CPU only); planted
+mistakes in the decoding or the scales each fail a pin."""
 import numpy as np
 import pytest
 
@@ -8,20 +8,37 @@ import workloads
 from oracle import widen_bf16
 from oracle.bifurcated import bifurcated_attention
 
-from .pins_kvquant import KVS, QUANT_PINS, code_table
+from .pins_kvquant import KVS, QUANT_PINS, code_table, elements, stored
 
 
 def test_code_tables_match_library():
     """Both decoders against torch's float8_e4m3fn cast and numpy's int8
-    view, over all 256 codes (NaN where the library gives NaN)."""
-    codes = np.arange(256, dtype=np.uint8)
+    view over all 256 codes (NaN where the library gives NaN), and against
+    the int4 table from numpy's unpackbits over all 16 codes."""
     for kv in KVS:
         ref = code_table(kv)
+        codes = np.arange(ref.size, dtype=np.uint8)
         c_side = np.array([oracle.code_value(kv, int(c)) for c in codes])
-        np_side = oracle.widen_codes(codes, kv)
+        np_side = oracle.widen_codes(stored(codes, kv), kv)
         for got in (c_side, np_side):
             assert np.array_equal(np.isnan(got), np.isnan(ref))
             assert np.array_equal(got[~np.isnan(ref)], ref[~np.isnan(ref)])
+
+
+def test_int4_every_byte_unpacks_low_nibble_first():
+    """All 256 bytes: the numpy decoder yields (value of the low nibble,
+    value of the high nibble) per byte, as the unpackbits table says."""
+    b = np.arange(256, dtype=np.uint8).reshape(16, 16)
+    got = oracle.widen_codes(b, "int4")
+    assert got.shape == (16, 32)
+    assert np.array_equal(got, code_table("int4")[elements(b, "int4")])
+    assert np.array_equal(got[:, 0::2], code_table("int4")[np.arange(256).reshape(16, 16) & 15])
+
+
+def test_int4_anchors():
+    """Two's complement 4-bit values: 0..7 as they are, 8 -> -8, 15 -> -1."""
+    for c, v in {0: 0.0, 1: 1.0, 7: 7.0, 8: -8.0, 9: -7.0, 14: -2.0, 15: -1.0}.items():
+        assert oracle.code_value("int4", c) == v
 
 
 def test_fp8_spec_anchors():
@@ -86,7 +103,11 @@ def test_generator_recipe():
 def test_bad_arguments():
     x = workloads.make_inputs(2, 4, 2, 8, 4, 3, seed=460, kv="int8")
     with pytest.raises(ValueError):
+        oracle.attention(**dict(x, kv="int2"))
+    with pytest.raises(ValueError):  # 8-bit arrays (d bytes a row) handed over as int4 (d/2)
         oracle.attention(**dict(x, kv="int4"))
+    with pytest.raises(ValueError):
+        workloads.make_inputs(2, 4, 2, 7, 4, 3, seed=460, kv="int4")  # odd d
     with pytest.raises(ValueError):
         oracle.attention(**dict(x, k_scale=np.ones(3, np.float32)))
     with pytest.raises(ValueError):  # 8-bit codes handed over as bf16 bit patterns
@@ -98,6 +119,12 @@ def _mutant(kind):
     mistake in the decoding or the scales."""
     def decode(codes, kv):
         c = np.asarray(codes).astype(np.int64)
+        if kv == "int4":
+            lo, hi = c & 15, c >> 4
+            if kind == "int4_nibbles_swapped":
+                lo, hi = hi, lo
+            nib = np.stack([lo, hi], axis=-1).reshape(c.shape[:-1] + (2 * c.shape[-1],))
+            return (nib if kind == "int4_unsigned" else nib - 16 * (nib >= 8)).astype(np.float64)
         if kv == "int8":
             return (c if kind == "int8_unsigned" else c - 256 * (c >= 128)).astype(np.float64)
         e, m = (c >> 3) & 15, (c & 7).astype(np.float64)
@@ -146,6 +173,7 @@ def test_unmutated_evaluator_passes():
 
 
 @pytest.mark.parametrize("kind", ["fp8_bias8", "fp8_no_subnormals", "int8_unsigned",
+                                  "int4_unsigned", "int4_nibbles_swapped",
                                   "swap_kv_scales", "no_scale_on_decode",
                                   "head_major_scale_index"])
 def test_mutation_fails_some_pin(kind):

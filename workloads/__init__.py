@@ -15,6 +15,7 @@ Layouts (row-major, bf16 stored as uint16 bit patterns):
     Kc, Vc  [g, m_c, d]            one shared copy of the context cache
     Kd, Vd  [b, g, m_d_max, d]     per-sample decode cache
     lens    [b] int32              valid decode rows per sample
+(int4 caches hold two codes per byte: their last axis is d/2 bytes.)
 
 Recipe: numpy PCG64 seeded per workload, draws in the order q, Kc, Vc, Kd, Vd,
 each ``standard_normal(float32)`` rounded to bf16 with round-to-nearest-even;
@@ -24,7 +25,9 @@ then ``lens`` (``integers(1, m_d_max + 1)`` when ragged, else all ``m_d_max``).
 same draws, multiplied by ``qmax / 4.5`` (4.5 standard deviations map to the
 largest code: 448 for OCP fp8 E4M3, 127 for int8), saturated at +-qmax and
 encoded with round-to-nearest-even (fp8 through torch's ``float8_e4m3fn``
-cast, int8 through ``numpy.rint``). After ``lens``, per-group factors
+cast, int8 through ``numpy.rint``). 4-bit caches (``kv="int4"``): the same
+with qmax = 7, the codes then packed two per byte, element 2u in the low
+nibble of byte u and element 2u+1 in the high nibble. After ``lens``, per-group factors
 ``c = 2**uniform(-1, 1)`` are drawn for keys, then for values, and the
 scales are ``k_scale = c_k * 4.5 / qmax`` (``v_scale`` likewise), so a
 group's dequantized keys are close to its draws times ``c_k``: heads of
@@ -37,13 +40,23 @@ import dataclasses
 import numpy as np
 
 BF16_NAN = np.uint16(0x7FC0)
-KV_TYPES = ("bf16", "fp8_e4m3", "int8")
-KV_BYTES = {"bf16": 2, "fp8_e4m3": 1, "int8": 1}
-KV_QMAX = {"fp8_e4m3": 448.0, "int8": 127.0}
+KV_TYPES = ("bf16", "fp8_e4m3", "int8", "int4")
+KV_BITS = {"bf16": 16, "fp8_e4m3": 8, "int8": 8, "int4": 4}
+KV_QMAX = {"fp8_e4m3": 448.0, "int8": 127.0, "int4": 7.0}
 KV_CLIP_SIGMA = 4.5
-# A code that poisons rows past a sample's length: NaN in fp8 E4M3, the
-# largest value in int8.
-KV_POISON = {"fp8_e4m3": np.uint8(0x7F), "int8": np.uint8(0x7F)}
+# A byte that poisons rows past a sample's length: NaN in fp8 E4M3, the
+# largest value in int8 and (in both nibbles) in int4.
+KV_POISON = {"fp8_e4m3": np.uint8(0x7F), "int8": np.uint8(0x7F), "int4": np.uint8(0x77)}
+
+
+def row_bytes(d: int, kv: str) -> int:
+    """Bytes of one cache row of d elements."""
+    return d * KV_BITS[kv] // 8
+
+
+def cache_cols(d: int, kv: str) -> int:
+    """Length of a cache array's last axis: d elements, or d/2 bytes for int4."""
+    return d // 2 if kv == "int4" else d
 
 
 @dataclasses.dataclass(frozen=True)
@@ -58,7 +71,7 @@ class Workload:
     ragged: bool
     seed: int
     n: int = 1  # new tokens per sample (draft tokens verified together when > 1)
-    kv: str = "bf16"  # cache element type: bf16, or 8-bit codes with per-group scales
+    kv: str = "bf16"  # cache element type: bf16, or 8-/4-bit codes with per-group scales
 
     @property
     def p(self) -> int:
@@ -113,11 +126,19 @@ def _normal_bf16(rng: np.random.Generator, shape) -> np.ndarray:
     return out.reshape(shape)
 
 
+def pack_int4(codes: np.ndarray) -> np.ndarray:
+    """Integer codes in [-8, 7] (last axis even) -> bytes, two codes each:
+    element 2u in the low nibble of byte u, element 2u+1 in the high one."""
+    c = np.asarray(codes).astype(np.int64) & 15
+    return (c[..., 0::2] | (c[..., 1::2] << 4)).astype(np.uint8)
+
+
 def _encode(y: np.ndarray, kv: str) -> np.ndarray:
-    """float32 values already in code units -> saturated 8-bit codes (RNE)."""
+    """float32 values already in code units -> saturated codes (RNE); int4
+    codes come out one per element, unpacked."""
     qmax = KV_QMAX[kv]
     y = np.clip(y, -qmax, qmax)
-    if kv == "int8":
+    if kv in ("int8", "int4"):
         return np.rint(y).astype(np.int8).view(np.uint8)
     import torch
     return torch.from_numpy(np.ascontiguousarray(y)).to(torch.float8_e4m3fn) \
@@ -126,13 +147,15 @@ def _encode(y: np.ndarray, kv: str) -> np.ndarray:
 
 def _normal_codes(rng: np.random.Generator, shape, kv: str) -> np.ndarray:
     n = int(np.prod(shape))
-    out = np.empty(n, dtype=np.uint8)
+    per = 2 if kv == "int4" else 1  # codes per stored byte
+    out = np.empty(n // per, dtype=np.uint8)
     mult = np.float32(KV_QMAX[kv] / KV_CLIP_SIGMA)
-    step = 1 << 24
+    step = 1 << 24  # even, so int4 pairs never straddle two steps
     for s in range(0, n, step):
         e = min(n, s + step)
-        out[s:e] = _encode(rng.standard_normal(e - s, dtype=np.float32) * mult, kv)
-    return out.reshape(shape)
+        codes = _encode(rng.standard_normal(e - s, dtype=np.float32) * mult, kv)
+        out[s // per:e // per] = pack_int4(codes.view(np.int8)) if per == 2 else codes
+    return out.reshape(tuple(shape[:-1]) + (shape[-1] // per,))
 
 
 def make_inputs(b, h, g, d, m_c, m_d_max, *, seed, ragged=False, lens=None,
@@ -144,13 +167,16 @@ def make_inputs(b, h, g, d, m_c, m_d_max, *, seed, ragged=False, lens=None,
     with bf16 NaN, so any read of them shows up in the output. With ``n > 1``
     new tokens per sample, q is [b, h, n, d] and ragged lengths are drawn in
     [n, m_d_max] (the n tokens are the last n valid decode rows). With an
-    8-bit ``kv`` the caches are uint8 codes and the dict also holds ``kv``,
+    8-bit ``kv`` the caches are uint8 codes, with ``"int4"`` uint8 bytes of
+    two codes each (last axis d/2), and the dict also holds ``kv``,
     ``k_scale`` and ``v_scale`` (float32 [g]).
     """
     if h % g:
         raise ValueError("h must be a multiple of g")
     if kv not in KV_TYPES:
         raise ValueError(f"unknown cache type {kv!r}")
+    if kv == "int4" and d % 2:
+        raise ValueError("int4 caches need an even head dimension")
     rng = np.random.Generator(np.random.PCG64(seed))
     q = _normal_bf16(rng, (b, h, d) if n == 1 else (b, h, n, d))
     cache = _normal_bf16 if kv == "bf16" else (lambda r, shp: _normal_codes(r, shp, kv))
@@ -205,13 +231,13 @@ def first_samples(x, nb):
 def kv_bytes(g, d, m_c, lens, kv="bf16") -> int:
     """Algorithmic KV bytes of one bifurcated step: one copy of context K and
     V plus every sample's valid decode K and V (Section 4.3), at the cache's
-    element size (2 bytes bf16, 1 byte for 8-bit codes)."""
-    return 2 * KV_BYTES[kv] * g * d * (int(m_c) + int(np.sum(lens, dtype=np.int64)))
+    element size (2 bytes bf16, 1 byte for 8-bit codes, 1/2 byte for int4)."""
+    return 2 * g * row_bytes(d, kv) * (int(m_c) + int(np.sum(lens, dtype=np.int64)))
 
 
 def replicated_kv_bytes(b, g, d, m_c, lens, kv="bf16") -> int:
     """KV bytes when the context is read once per sample (Section 4.3)."""
-    return 2 * KV_BYTES[kv] * g * d * (b * int(m_c) + int(np.sum(lens, dtype=np.int64)))
+    return 2 * g * row_bytes(d, kv) * (b * int(m_c) + int(np.sum(lens, dtype=np.int64)))
 
 
 def attention_flops(h, d, b, m_c, lens, n=1) -> int:
