@@ -22,13 +22,14 @@
  *   q       bf16 [b][h][n][d]       token r of head j of sample i at ((i*h + j)*n + r)*d
  *                                   ([b][h][d] when n = 1)
  *   Kc, Vc  kv  [g][m_c][d]         one shared copy of the context cache
- *   Kd, Vd  kv  [b][g][m_d_max][d]  per-sample decode cache
+ *   Kd, Vd  kv  [b][g][m_d_max][d]  per-sample decode cache (int4: d/2 bytes a row)
  *   decode_lens int32 [b]           valid decode rows per sample
  *   k_scale, v_scale fp32 [g]       per-group key / value scales (optional)
  *   out     fp32 [b][h][n][d]
- * kv is the plan's cache element type (dims.kv_type): bf16, or 8-bit codes
- * (OCP fp8 E4M3, or two's complement int8), one byte each. The FAQ on
- * attention quantization notes that 8-bit KV halves the KV bytes and leaves
+ * kv is the plan's cache element type (dims.kv_type): bf16, 8-bit codes
+ * (OCP fp8 E4M3, or two's complement int8), one byte each, or two's
+ * complement int4 codes, two per byte. The FAQ on attention quantization
+ * notes that 8-bit KV halves the KV bytes (4-bit KV quarters them) and leaves
  * the method unchanged; here the key of a cache row is k_scale[gam] times
  * its codes' values and its value v_scale[gam] times its codes' values, the
  * same scales for the group's context and decode caches (NULL scales mean
@@ -100,7 +101,9 @@ typedef enum {
 typedef enum {
   BIFATTN_KV_BF16 = 0,     /* bf16 keys and values */
   BIFATTN_KV_FP8_E4M3 = 1, /* OCP 8-bit float E4M3 codes (bias 7, no infinities, max 448) */
-  BIFATTN_KV_INT8 = 2      /* two's complement 8-bit integer codes */
+  BIFATTN_KV_INT8 = 2,     /* two's complement 8-bit integer codes */
+  BIFATTN_KV_INT4 = 3      /* two's complement 4-bit integer codes, two per byte: element u
+                              of a row in byte u/2, even u in the low nibble; rows d/2 bytes */
 } bifattn_kv_type_t;
 
 /* Problem dimensions (Section 3.1 notation; d is the head dimension). */
@@ -246,8 +249,9 @@ bifattn_status_t bifattn_decode_replicated_scaled(bifattn_plan_t plan, const voi
  *   Kd[i, gam, len_i + r, :] = k_new[i, gam, r, :]   (r < n; Vd likewise)
  *   decode_lens[i] += n
  * k_new, v_new [b][g][n][d] of the plan's cache element type (the step's n
- * new tokens per sample, n from the plan; 8-bit codes are copied as they
- * are, encoded by the caller with the group's scales); Kd, Vd, decode_lens
+ * new tokens per sample, n from the plan; 8-bit codes, and int4 bytes of
+ * two codes, are copied as they are, encoded by the caller with the group's
+ * scales); Kd, Vd, decode_lens
  * as in bifattn_decode, updated in place on
  * `stream`. Rows that would pass m_d_max are dropped (the length stops at
  * m_d_max), a length outside [0, m_d_max] is clamped first; both raise the

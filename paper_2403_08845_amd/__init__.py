@@ -21,7 +21,7 @@ OK, EINVAL, EUNSUPPORTED, EALIGN, ENOMEM, EHIP, ELENS, ESCALE, ESCRATCH = 0, -1,
 NOALLOC_SCRATCH_BYTES = 64 << 20
 KERNEL_PARTIALS, KERNEL_COMBINE, KERNEL_CALL, KERNEL_CONTEXT, KERNEL_DECODE = 0, 1, 2, 3, 4
 #: Cache element types (bifattn_kv_type_t).
-KV_TYPES = {"bf16": 0, "fp8_e4m3": 1, "int8": 2}
+KV_TYPES = {"bf16": 0, "fp8_e4m3": 1, "int8": 2, "int4": 3}
 #: Paths of bifattn_decode (bifattn_path_t): "auto" lets the plan choose.
 PATHS = {"auto": 0, "bifurcated": 1, "standard": 2}
 
@@ -214,11 +214,18 @@ def _tensor(t, shape, dtype, device, name):
 
 def _cache_dtypes(plan):
     """torch dtypes accepted for the plan's cache tensors: bf16, or any
-    one-byte type holding the 8-bit codes."""
+    one-byte type holding the 8-bit codes (int4: bytes of two codes)."""
     import torch
     if plan.dims.kv_type == KV_TYPES["bf16"]:
         return torch.bfloat16
+    if plan.dims.kv_type == KV_TYPES["int4"]:
+        return (torch.uint8, torch.int8)
     return (torch.uint8, torch.int8, torch.float8_e4m3fn)
+
+
+def _cols(D):
+    """Last axis of a cache tensor: d elements, or d/2 bytes for int4."""
+    return D.d // 2 if D.kv_type == KV_TYPES["int4"] else D.d
 
 
 def _scales(plan, k_scale, v_scale, dev):
@@ -241,7 +248,8 @@ def bifattn_decode(plan: Plan, q, Kc, Vc, Kd, Vd, decode_lens, out, stream=None)
     """Enqueue one bifurcated decode step (see include/bifattn.h).
 
     q bf16 [b,h,n,d] ([b,h,d] when n = 1); Kc, Vc [g,m_c,d] and Kd, Vd
-    [b,g,m_d_max,d] of the plan's cache type (bf16, or one-byte codes);
+    [b,g,m_d_max,d] of the plan's cache type (bf16, or one-byte codes;
+    int4 caches hold two codes a byte, last axis d/2);
     decode_lens int32 [b]; out fp32 shaped like q; all on the same GPU.
     """
     bifattn_decode_scaled(plan, q, Kc, Vc, Kd, Vd, decode_lens, None, None, out, stream)
@@ -257,10 +265,10 @@ def bifattn_decode_scaled(plan: Plan, q, Kc, Vc, Kd, Vd, decode_lens, k_scale, v
     cd = _cache_dtypes(plan)
     args = [
         _tensor(q, _query_shapes(D), torch.bfloat16, dev, "q"),
-        _tensor(Kc, (D.g, D.m_c, D.d), cd, dev, "Kc"),
-        _tensor(Vc, (D.g, D.m_c, D.d), cd, dev, "Vc"),
-        _tensor(Kd, (D.b, D.g, D.m_d_max, D.d), cd, dev, "Kd"),
-        _tensor(Vd, (D.b, D.g, D.m_d_max, D.d), cd, dev, "Vd"),
+        _tensor(Kc, (D.g, D.m_c, _cols(D)), cd, dev, "Kc"),
+        _tensor(Vc, (D.g, D.m_c, _cols(D)), cd, dev, "Vc"),
+        _tensor(Kd, (D.b, D.g, D.m_d_max, _cols(D)), cd, dev, "Kd"),
+        _tensor(Vd, (D.b, D.g, D.m_d_max, _cols(D)), cd, dev, "Vd"),
         _tensor(decode_lens, (D.b,), torch.int32, dev, "decode_lens"),
         *_scales(plan, k_scale, v_scale, dev),
         _tensor(out, [tuple(q.shape)], torch.float32, dev, "out"),
@@ -301,10 +309,10 @@ def bifattn_decode_noalloc(dims: Dims, q, Kc, Vc, Kd, Vd, decode_lens, k_scale, 
     D = dims
     args = [
         _tensor(q, _query_shapes(D), torch.bfloat16, dev, "q"),
-        _tensor(Kc, (D.g, D.m_c, D.d), cd, dev, "Kc"),
-        _tensor(Vc, (D.g, D.m_c, D.d), cd, dev, "Vc"),
-        _tensor(Kd, (D.b, D.g, D.m_d_max, D.d), cd, dev, "Kd"),
-        _tensor(Vd, (D.b, D.g, D.m_d_max, D.d), cd, dev, "Vd"),
+        _tensor(Kc, (D.g, D.m_c, _cols(D)), cd, dev, "Kc"),
+        _tensor(Vc, (D.g, D.m_c, _cols(D)), cd, dev, "Vc"),
+        _tensor(Kd, (D.b, D.g, D.m_d_max, _cols(D)), cd, dev, "Kd"),
+        _tensor(Vd, (D.b, D.g, D.m_d_max, _cols(D)), cd, dev, "Vd"),
         _tensor(decode_lens, (D.b,), torch.int32, dev, "decode_lens"),
         *_scales(shape, k_scale, v_scale, dev),
         _tensor(out, [tuple(q.shape)], torch.float32, dev, "out"),
@@ -329,8 +337,8 @@ def bifattn_decode_replicated_scaled(plan: Plan, q, K, V, decode_lens, k_scale, 
     cd = _cache_dtypes(plan)
     args = [
         _tensor(q, _query_shapes(D), torch.bfloat16, dev, "q"),
-        _tensor(K, (D.b, D.g, rows, D.d), cd, dev, "K"),
-        _tensor(V, (D.b, D.g, rows, D.d), cd, dev, "V"),
+        _tensor(K, (D.b, D.g, rows, _cols(D)), cd, dev, "K"),
+        _tensor(V, (D.b, D.g, rows, _cols(D)), cd, dev, "V"),
         _tensor(decode_lens, (D.b,), torch.int32, dev, "decode_lens"),
         *_scales(plan, k_scale, v_scale, dev),
         _tensor(out, [tuple(q.shape)], torch.float32, dev, "out"),
@@ -350,10 +358,10 @@ def bifattn_append_kv(plan: Plan, k_new, v_new, Kd, Vd, decode_lens, stream=None
     n = max(1, D.n)
     cd = _cache_dtypes(plan)
     args = [
-        _tensor(k_new, (D.b, D.g, n, D.d), cd, dev, "k_new"),
-        _tensor(v_new, (D.b, D.g, n, D.d), cd, dev, "v_new"),
-        _tensor(Kd, (D.b, D.g, D.m_d_max, D.d), cd, dev, "Kd"),
-        _tensor(Vd, (D.b, D.g, D.m_d_max, D.d), cd, dev, "Vd"),
+        _tensor(k_new, (D.b, D.g, n, _cols(D)), cd, dev, "k_new"),
+        _tensor(v_new, (D.b, D.g, n, _cols(D)), cd, dev, "v_new"),
+        _tensor(Kd, (D.b, D.g, D.m_d_max, _cols(D)), cd, dev, "Kd"),
+        _tensor(Vd, (D.b, D.g, D.m_d_max, _cols(D)), cd, dev, "Vd"),
         _tensor(decode_lens, (D.b,), torch.int32, dev, "decode_lens"),
     ]
     _check(lib().bifattn_append_kv(plan.handle, *args, _stream_ptr(stream, dev)),

@@ -181,7 +181,7 @@ bifattn_status_t plan_splits(bifattn_plan_s* P, bool allow_fork = true) {
     // fills its CUs' registers and so leaves no room for decode work beside
     // it. BIFATTN_FORK=0/1 and BIFATTN_CTX_WIDE=0/1 force either choice (d = 64
     // and 8-bit caches always take the kernel of 16-row waves).
-    const double dec_bytes = 2.0 * d.b * d.g * (double)d.m_d_max * d.d * kv_bytes(d.kv_type);
+    const double dec_bytes = 2.0 * d.b * d.g * (double)d.m_d_max * kv_row_bytes(d.d, d.kv_type);
     const double ctx_flops = 4.0 * d.h * P->ntok * d.d * (double)d.b * d.m_c;
     const int fork_env = env_switch("BIFATTN_FORK");
     const bool big_decode = dec_bytes >= 16.0 * (1 << 20) && dec_bytes / 5e12 > 0.5 * ctx_flops / 1e15;
@@ -292,7 +292,7 @@ bifattn_status_t check_dims(const bifattn_dims_t* d) {
   if (d->h % d->g) return BIFATTN_EINVAL;
   if (!(std::isfinite(d->scale))) return BIFATTN_EINVAL;
   if (d->kv_type != BIFATTN_KV_BF16 && d->kv_type != BIFATTN_KV_FP8_E4M3 &&
-      d->kv_type != BIFATTN_KV_INT8)
+      d->kv_type != BIFATTN_KV_INT8 && d->kv_type != BIFATTN_KV_INT4)
     return BIFATTN_EINVAL;
   if (d->path != BIFATTN_PATH_AUTO && d->path != BIFATTN_PATH_BIFURCATED &&
       d->path != BIFATTN_PATH_STANDARD)
@@ -310,7 +310,7 @@ bifattn_status_t check_dims(const bifattn_dims_t* d) {
     return BIFATTN_EINVAL;
   // Kernels address one cache (a group's context, a sample's decode rows, or
   // both in the replicated ablation) with 32-bit byte offsets.
-  if (((double)d->m_c + d->m_d_max) * dd * kv_bytes(d->kv_type) > INT32_MAX)
+  if (((double)d->m_c + d->m_d_max) * kv_row_bytes(d->d, d->kv_type) > INT32_MAX)
     return BIFATTN_EUNSUPPORTED;
   return BIFATTN_OK;
 }

@@ -31,17 +31,19 @@ constexpr float kRescaleSlack = 8.0f;
 constexpr int kStatusLens = 1;
 constexpr int kStatusScale = 2;
 
-// Cache element types: bf16, or 8-bit codes (OCP fp8 E4M3, int8) with
-// per-group scales.
-enum KvType { kKvBf16 = 0, kKvFp8 = 1, kKvInt8 = 2 };
-constexpr int kv_bytes(int kv) { return kv == kKvBf16 ? 2 : 1; }
+// Cache element types: bf16, or 8-bit codes (OCP fp8 E4M3, int8) or 4-bit
+// codes (int4, two per byte) with per-group scales.
+enum KvType { kKvBf16 = 0, kKvFp8 = 1, kKvInt8 = 2, kKvInt4 = 3 };
+constexpr int kv_bits(int kv) { return kv == kKvBf16 ? 16 : (kv == kKvInt4 ? 4 : 8); }
+// Bytes of one cache row of d elements (d even).
+constexpr int kv_row_bytes(int d, int kv) { return d * kv_bits(kv) / 8; }
 
 // Partial result of one query row over one key range, relative to 2^m:
 // m  = reference maximum of scale*log2(e)*(q.k) over the range (or -inf),
 // l  = sum of 2^(logit - m), acc[d] = sum of 2^(logit - m) * v.
 struct PartialsParams {
   const uint16_t* q;
-  const uint8_t* Kc;      // caches as bytes: bf16 or 8-bit codes
+  const uint8_t* Kc;      // caches as bytes: bf16, 8-bit or 4-bit codes
   const uint8_t* Vc;
   const uint8_t* Kd;      // decode cache (replicated cache in ablation mode)
   const uint8_t* Vd;

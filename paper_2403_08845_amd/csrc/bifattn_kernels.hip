@@ -27,10 +27,10 @@
 // dims DV*m + t on MFMA row m (DV = d/16), so lane (n, G) ends up owning
 // output dims [4*DV*G, 4*DV*G + 4*DV) of query row n.
 //
-// Caches may hold 8-bit codes (OCP fp8 E4M3 or int8, one scale per KV group
-// for keys and one for values): every code value is exactly a bf16 value, so
-// codes are widened to bf16 on the way from memory to the operands and the
-// matrix products stay bf16. The key scale folds into the softmax scale of
+// Caches may hold 8-bit codes (OCP fp8 E4M3 or int8) or 4-bit codes (int4,
+// two per byte), with one scale per KV group for keys and one for values:
+// every code value is exactly a bf16 value, so codes are widened to bf16 on
+// the way from memory to the operands and the matrix products stay bf16. The key scale folds into the softmax scale of
 // the group's units and the value scale into the combine.
 #include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
@@ -172,6 +172,15 @@ template <> struct Raw<2> {
   static __device__ __forceinline__ type zero() { return 0u; }
   static __device__ __forceinline__ uint32_t word(const type& v, int) { return v; }
 };
+template <> struct Raw<1> {
+  typedef uint32_t type;
+  template <int AUX = 0>
+  static __device__ __forceinline__ type load(__amdgpu_buffer_rsrc_t r, int off) {
+    return __builtin_amdgcn_raw_buffer_load_b8(r, off, 0, AUX);
+  }
+  static __device__ __forceinline__ type zero() { return 0u; }
+  static __device__ __forceinline__ uint32_t word(const type& v, int) { return v; }
+};
 
 // Pack element t of two bf16 value rows (even key, odd key) into one word.
 __device__ __forceinline__ uint32_t pair_elem(uint32_t even_w, uint32_t odd_w, int t) {
@@ -179,19 +188,22 @@ __device__ __forceinline__ uint32_t pair_elem(uint32_t even_w, uint32_t odd_w, i
                  : ((even_w & 0xffffu) | (odd_w << 16));
 }
 
-// Cache element codecs. ES: bytes per element. For the 8-bit codes, lo(w) /
-// hi(w) widen codes 0-1 / 2-3 of a word to a bf16 pair (code 0 or 2 in the
-// low half) and pair(e, o, t) widens code t of word e and code t of word o.
-// Both conversions are exact: an fp8 E4M3 value has 4 significant bits and
-// an int8 value 8, and both lie inside bf16's exponent range.
-struct KvBf16 {
-  static constexpr int ES = 2;
+// Cache element codecs. BITS: bits per element; bytes(n): bytes of n
+// elements. For the 8-bit codes, lo(w) / hi(w) widen codes 0-1 / 2-3 of a
+// word to a bf16 pair (code 0 or 2 in the low half); for every code type
+// pair(e, o, t) widens code t of word e and code t of word o. The
+// conversions are exact: an fp8 E4M3 value has 4 significant bits, an int8
+// value 8 and an int4 value 4, all inside bf16's exponent range.
+template <int B> struct KvBits {
+  static constexpr int BITS = B;
+  static constexpr int bytes(int n) { return n * B / 8; }
+};
+struct KvBf16 : KvBits<16> {
   static __device__ __forceinline__ uint32_t pair(uint32_t e, uint32_t o, int t) {
     return pair_elem(e, o, t);
   }
 };
-struct KvFp8 {
-  static constexpr int ES = 1;
+struct KvFp8 : KvBits<8> {
   static __device__ __forceinline__ uint32_t lo(uint32_t w) {
     return __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(w, 1.f, false));
   }
@@ -204,8 +216,7 @@ struct KvFp8 {
     return lo(__builtin_amdgcn_perm(o, e, 0x0C0C0000u | ((4u + t) << 8) | (uint32_t)t));
   }
 };
-struct KvInt8 {
-  static constexpr int ES = 1;
+struct KvInt8 : KvBits<8> {
   static __device__ __forceinline__ float code(uint32_t w, int t) {
     return (float)(signed char)(w >> (8 * t));
   }
@@ -218,6 +229,17 @@ struct KvInt8 {
   static __device__ __forceinline__ uint32_t hi(uint32_t w) { return two(code(w, 2), code(w, 3)); }
   static __device__ __forceinline__ uint32_t pair(uint32_t e, uint32_t o, int t) {
     return two(code(e, t), code(o, t));
+  }
+};
+// Two's complement 4-bit codes, eight to a word: element 2u of a row in the
+// low nibble of its byte u, so nibble t of a word is element t of the word's
+// eight.
+struct KvInt4 : KvBits<4> {
+  static __device__ __forceinline__ float code(uint32_t w, int t) {
+    return (float)((int)(w << (28 - 4 * t)) >> 28);  // sign-extended nibble t
+  }
+  static __device__ __forceinline__ uint32_t pair(uint32_t e, uint32_t o, int t) {
+    return KvInt8::two(code(e, t), code(o, t));
   }
 };
 
@@ -234,11 +256,19 @@ template <typename C> struct Widen8Codes {
 };
 template <> struct Widen8<KvFp8> : Widen8Codes<KvFp8> {};
 template <> struct Widen8<KvInt8> : Widen8Codes<KvInt8> {};
+template <> struct Widen8<KvInt4> {  // one word of eight nibbles
+  static __device__ __forceinline__ u32x4 run(uint32_t w) {
+    u32x4 v;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) v[k] = KvInt8::two(KvInt4::code(w, 2 * k), KvInt4::code(w, 2 * k + 1));
+    return v;
+  }
+};
 
 // bf16 pair of element t of two value slices (even key, odd key).
 template <typename KV, typename S>
 __device__ __forceinline__ uint32_t value_pair(const S& e, const S& o, int t) {
-  constexpr int PER = 4 / KV::ES;  // elements per 32-bit word
+  constexpr int PER = 32 / KV::BITS;  // elements per 32-bit word
   typedef Raw<sizeof(S) < 4 ? 4 : (int)sizeof(S)> R;
   return KV::pair(R::word(e, t / PER), R::word(o, t / PER), t % PER);
 }
@@ -449,7 +479,7 @@ __device__ __forceinline__ void load_q(u32x4 (&qop)[NT][D / 32], RowPtr row_ptr,
 
 // Register path: one wave loads a whole 32-key tile, every load instruction
 // reading whole consecutive rows (1 KB contiguous for d = 128 bf16):
-//   K: lane l holds row RPI*e + l/CPR, 16-byte chunk l%CPR (CPR = d*ES/16
+//   K: lane l holds row RPI*e + l/CPR, 16-byte chunk l%CPR (CPR = 16-byte
 //      chunks per row, RPI = 64/CPR rows per instruction); widened to bf16
 //      and staged through a per-wave LDS tile to reach the MFMA operand
 //      layout, whose 16 lanes each want a different row (XOR-swizzled so
@@ -460,15 +490,14 @@ __device__ __forceinline__ void load_q(u32x4 (&qop)[NT][D / 32], RowPtr row_ptr,
 // Loads go through buffer resources whose range ends at the item's last key,
 // so rows past it read as zero without a branch and without a memory access.
 template <int D, typename KV> struct TileRegs {
-  static constexpr int ES = KV::ES;
   static constexpr int KS = D / 32;
   static constexpr int DV = D / 16;
-  static constexpr int RB = D * ES;       // bytes per cache row
+  static constexpr int RB = KV::bytes(D);  // bytes per cache row
   static constexpr int CPR = RB / 16;     // raw 16-byte chunks per row
   static constexpr int RPI = 64 / CPR;
   static constexpr int KI = kTileKeys / RPI;
   static constexpr int BPR = D / 8;       // bf16 16-byte chunks per row in LDS
-  typedef Raw<DV * ES> VR;
+  typedef Raw<KV::bytes(DV)> VR;
   typedef typename VR::type VS;
   u32x4 kraw[KI];
   VS vrow[8];
@@ -488,7 +517,7 @@ template <int D, typename KV> struct TileRegs {
     for (int e = 0; e < KI; ++e)
       kraw[e] = Raw<16>::load<AUX>(rk, boff(koff + (uint32_t)(e * RPI * RB)));
     const int c = lane & 15, G = lane >> 4;
-    const uint32_t voff = (uint32_t)(key0 + G) * RB + (uint32_t)(DV * c * ES);
+    const uint32_t voff = (uint32_t)(key0 + G) * RB + (uint32_t)KV::bytes(DV * c);
 #pragma unroll
     for (int e = 0; e < 8; ++e)
       vrow[e] = VR::template load<AUX>(rv, boff(voff + (uint32_t)(4 * e * RB)));
@@ -503,13 +532,18 @@ template <int D, typename KV> struct TileRegs {
 #pragma unroll
     for (int e = 0; e < KI; ++e) {
       const int row = RPI * e + lane / CPR, c = lane % CPR;
-      if constexpr (ES == 2) {
-        *(lds_u32x4*)(kl + kslot(row, c)) = kraw[e];
-      } else {
+      const u32x4& w = kraw[e];
+      if constexpr (KV::BITS == 16) {
+        *(lds_u32x4*)(kl + kslot(row, c)) = w;
+      } else if constexpr (KV::BITS == 8) {
         // 16 codes: bf16 chunks 2c and 2c + 1 of the row.
-        const u32x4& w = kraw[e];
         *(lds_u32x4*)(kl + kslot(row, 2 * c)) = Widen8<KV>::run(u32x2{w[0], w[1]});
         *(lds_u32x4*)(kl + kslot(row, 2 * c + 1)) = Widen8<KV>::run(u32x2{w[2], w[3]});
+      } else {
+        // 32 codes: bf16 chunks 4c .. 4c + 3 of the row.
+#pragma unroll
+        for (int k = 0; k < 4; ++k)
+          *(lds_u32x4*)(kl + kslot(row, 4 * c + k)) = Widen8<KV>::run(w[k]);
       }
     }
     __builtin_amdgcn_wave_barrier();
@@ -668,7 +702,7 @@ __device__ __forceinline__ int clamp_len(const int32_t* lens, int i, int m_d_max
 template <int D, int NT, typename KV>
 __device__ void decode_block(const PartialsParams& P, int blk, int wave, int lane, u32x4* qw,
                              u32x4* kl) {
-  constexpr int RB = D * KV::ES;
+  constexpr int RB = KV::bytes(D);
   const int s = blk % P.S_d;
   const int ig = blk / P.S_d;
   const int gam = ig % P.g, i = ig / P.g;
@@ -780,7 +814,7 @@ template <int D, int NT> struct MergeLds {
 template <int D, int NT, typename KV>
 __device__ void ctx_small_block(const PartialsParams& P, int blk, int wave, int lane, u32x4* qw,
                                 u32x4* kl, float* merge_lds) {
-  constexpr int RB = D * KV::ES;
+  constexpr int RB = KV::bytes(D);
   const int s = blk % P.S_c, gam = blk / P.S_c;
   const size_t cache = (size_t)gam * P.m_c * RB;
   const __amdgpu_buffer_rsrc_t rk = rows_rsrc(P.Kc + cache, P.m_c, RB);
@@ -818,7 +852,7 @@ __device__ void ctx_small_block(const PartialsParams& P, int blk, int wave, int 
 template <int D, int NT, typename KV>
 __device__ void standard_block(const PartialsParams& P, int blk, int wave, int lane, u32x4* qw,
                                u32x4* kl, float* merge_lds) {
-  constexpr int RB = D * KV::ES;
+  constexpr int RB = KV::bytes(D);
   constexpr int LD = D + 4;
   constexpr int ROWS = NT * kRowsPerTile;
   const int gam = blk % P.g, i = blk / P.g;
@@ -916,13 +950,12 @@ template <int D, typename KV>
 __device__ __forceinline__ void ctx_large_body(const PartialsParams& P) {
   constexpr int KS = D / 32;
   constexpr int DV = D / 16;
-  constexpr int ES = KV::ES;
-  constexpr int RB = D * ES;      // bytes per cache row
+  constexpr int RB = KV::bytes(D);  // bytes per cache row
   constexpr int KOPS = 2 * KS;    // K operands per tile
   constexpr int OPS = KOPS + DV;  // operands per tile (16 B per lane each)
   constexpr int HW = DV / 2;      // V^T operands one wave stages a word of
-  typedef Raw<8 * ES> KR;         // a lane's 8 elements of its K operand
-  typedef Raw<HW * ES> VR;        // a lane's HW elements of a value row
+  typedef Raw<KV::bytes(8)> KR;   // a lane's 8 elements of its K operand
+  typedef Raw<KV::bytes(HW)> VR;  // a lane's HW elements of a value row
   typedef typename VR::type VH;
   __shared__ __attribute__((aligned(16))) u32x4 lds[2 * OPS * 64];
   const int blk = xcd_logical(blockIdx.x, P.n_ctx_blocks);
@@ -953,11 +986,12 @@ __device__ __forceinline__ void ctx_large_body(const PartialsParams& P) {
   };
   auto fetch = [&](Stage& g, int key0) {  // keys past the chunk load as zero
     if (has_k)
-      g.k = KR::load(rk, boff((uint32_t)(key0 + qk_key(ka, r)) * RB + (uint32_t)((kss * 32 + G * 8) * ES)));
+      g.k = KR::load(rk, boff((uint32_t)(key0 + qk_key(ka, r)) * RB +
+                              (uint32_t)KV::bytes(kss * 32 + G * 8)));
 #pragma unroll
     for (int c = 0; c < 2; ++c)
       g.v[c] = VR::load(rv, boff((uint32_t)(key0 + 4 * (2 * vw + c) + G) * RB +
-                                 (uint32_t)((DV * r + vh * HW) * ES)));
+                                 (uint32_t)KV::bytes(DV * r + vh * HW)));
   };
   auto stage = [&](const Stage& g, int buf) {
     if (has_k) slot(buf, wave)[lane] = Widen8<KV>::run(g.k);
@@ -1494,6 +1528,7 @@ hipError_t launch_partials_d(const PartialsParams& P, int kv, int ctx_mode, int 
     case kKvBf16: return launch_partials_dk<D, KvBf16>(P, ctx_mode, dec_tiles, stream, ev);
     case kKvFp8: return launch_partials_dk<D, KvFp8>(P, ctx_mode, dec_tiles, stream, ev);
     case kKvInt8: return launch_partials_dk<D, KvInt8>(P, ctx_mode, dec_tiles, stream, ev);
+    case kKvInt4: return launch_partials_dk<D, KvInt4>(P, ctx_mode, dec_tiles, stream, ev);
     default: return hipErrorInvalidValue;
   }
 }
@@ -1517,6 +1552,7 @@ hipError_t launch_standard_d(const PartialsParams& P, int kv, int tiles, hipStre
     case kKvBf16: return launch_standard_dk<D, KvBf16>(P, tiles, stream, ev);
     case kKvFp8: return launch_standard_dk<D, KvFp8>(P, tiles, stream, ev);
     case kKvInt8: return launch_standard_dk<D, KvInt8>(P, tiles, stream, ev);
+    case kKvInt4: return launch_standard_dk<D, KvInt4>(P, tiles, stream, ev);
     default: return hipErrorInvalidValue;
   }
 }
@@ -1529,6 +1565,7 @@ hipError_t launch_ctx_large_d(const PartialsParams& P, int kv, hipStream_t strea
     case kKvBf16: return launch(ctx_large_kernel<D, KvBf16>, grid, kLargeThreads, stream, ev, P);
     case kKvFp8: return launch(ctx_large_kernel<D, KvFp8>, grid, kLargeThreads, stream, ev, P);
     case kKvInt8: return launch(ctx_large_kernel<D, KvInt8>, grid, kLargeThreads, stream, ev, P);
+    case kKvInt4: return launch(ctx_large_kernel<D, KvInt4>, grid, kLargeThreads, stream, ev, P);
     default: return hipErrorInvalidValue;
   }
 }
@@ -1569,10 +1606,11 @@ __global__ __launch_bounds__(256) void append_kernel(AppendParams A) {
 
 hipError_t launch_append(const AppendParams& A, int d, int kv, hipStream_t stream,
                          const LaunchEvents& ev) {
-  switch (d * kv_bytes(kv)) {
+  switch (kv_row_bytes(d, kv)) {
     case 256: return launch(append_kernel<256>, A.b, 256, stream, ev, A);
     case 128: return launch(append_kernel<128>, A.b, 256, stream, ev, A);
     case 64: return launch(append_kernel<64>, A.b, 256, stream, ev, A);
+    case 32: return launch(append_kernel<32>, A.b, 256, stream, ev, A);
     default: return hipErrorInvalidValue;
   }
 }

@@ -9,7 +9,8 @@ def kv_of(x):
 
 
 def cache_to_device(a, kv):
-    """bf16 bit patterns -> torch bf16, 8-bit codes -> torch uint8, on the GPU."""
+    """bf16 bit patterns -> torch bf16, 8-bit codes (int4: bytes of two
+    codes) -> torch uint8, on the GPU."""
     import torch
     if kv == "bf16":
         return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).cuda()
@@ -68,10 +69,12 @@ def run_decode(x, scale=0.0, plan=None, dev=None, check_status=True):
 
 
 def replicate(x):
-    """Physically replicated cache [b, g, m_c + m_d_max, d] (ablation input)."""
+    """Physically replicated cache [b, g, m_c + m_d_max, d] (ablation input;
+    the last axis as stored: d/2 bytes for int4)."""
     b, h, g, d, m_c, m_d_max = dims_of(x)
-    K = np.concatenate([np.broadcast_to(x["Kc"][None], (b, g, m_c, d)), x["Kd"]], axis=2)
-    V = np.concatenate([np.broadcast_to(x["Vc"][None], (b, g, m_c, d)), x["Vd"]], axis=2)
+    cols = x["Kc"].shape[-1]
+    K = np.concatenate([np.broadcast_to(x["Kc"][None], (b, g, m_c, cols)), x["Kd"]], axis=2)
+    V = np.concatenate([np.broadcast_to(x["Vc"][None], (b, g, m_c, cols)), x["Vd"]], axis=2)
     return np.ascontiguousarray(K), np.ascontiguousarray(V)
 
 

@@ -67,14 +67,15 @@ def gate_errors(out, ref):
 def value_units(x):
     """Per query head: the value scale of its group times the standard
     deviation of the group's value codes (context and valid decode rows)."""
-    from .pins_kvquant import code_table
+    from .pins_kvquant import code_table, elements
     b, h = x["q"].shape[:2]
     g = x["Vc"].shape[0]
-    table = code_table(x["kv"])
+    kv = x["kv"]
+    table = code_table(kv)
     units = np.empty(g)
     for gam in range(g):
-        vals = [table[x["Vc"][gam]].ravel()]
-        vals += [table[x["Vd"][i, gam, :x["lens"][i]]].ravel() for i in range(b)]
+        vals = [table[elements(x["Vc"][gam], kv)].ravel()]
+        vals += [table[elements(x["Vd"][i, gam, :x["lens"][i]], kv)].ravel() for i in range(b)]
         units[gam] = float(x["v_scale"][gam]) * float(np.std(np.concatenate(vals)))
     return np.repeat(units, h // g)
 

@@ -65,6 +65,7 @@ int main() {
   const bifattn_dims_t unsupported[] = {
       dims(4, 4, 4, 96, 128, 16), dims(4, 128, 1, 128, 128, 16), dims(4, 32, 1, 128, 128, 16, 0, 4),
       dims(2, 4, 1, 128, (1 << 23), 0),
+      dims(2, 4, 1, 128, (1 << 25), 0, 0, 1, BIFATTN_KV_INT4),  // 2^31 bytes of int4 rows
   };
   for (const auto& x : unsupported) EXPECT(bifattn_plan_create(&x, &plan), BIFATTN_EUNSUPPORTED);
   // Valid dims: the plan needs a device (none here, or a real one).
@@ -73,6 +74,8 @@ int main() {
       dims(256, 32, 8, 128, 32768, 1024), dims(4, 4, 4, 64, 128, 16, 0, 1, 0, 2),
       dims(32, 32, 32, 128, 8192, 512, -0.1f, 4, BIFATTN_KV_FP8_E4M3, BIFATTN_PATH_BIFURCATED),
       dims(1, 1, 1, 64, 1, 0, 0, 1, BIFATTN_KV_INT8, BIFATTN_PATH_STANDARD),
+      dims(32, 32, 32, 128, 8192, 512, 0, 1, BIFATTN_KV_INT4, BIFATTN_PATH_AUTO),
+      dims(2, 4, 1, 128, (1 << 23), 0, 0, 1, BIFATTN_KV_INT4),  // 2^29 bytes of int4 rows
   };
   for (const auto& x : good) {
     plan = nullptr;

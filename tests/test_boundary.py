@@ -62,10 +62,11 @@ def _create(L, *dims):
     ((1, 32, 32, 128, 2**23 - 64, 64, 0.0), bif.EUNSUPPORTED),  # context + decode rows
     ((2, 4, 2, 64, 128, 16, 0.0, -1), bif.EINVAL),          # negative token count
     ((2, 32, 1, 64, 128, 16, 0.0, 3), bif.EUNSUPPORTED),    # p * n = 96 query rows per unit
-    ((2, 4, 2, 64, 128, 16, 0.0, 1, 3), bif.EINVAL),        # unknown cache type
+    ((2, 4, 2, 64, 128, 16, 0.0, 1, 4), bif.EINVAL),        # unknown cache type
     ((2, 4, 2, 64, 128, 16, 0.0, 1, -1), bif.EINVAL),
     ((1, 32, 32, 128, 2**24, 0, 0.0, 1, 1), bif.EUNSUPPORTED),  # fp8 cache past 2^31 bytes
     ((1, 32, 32, 128, 2**24 - 64, 64, 0.0, 1, 2), bif.EUNSUPPORTED),  # int8, both parts
+    ((1, 32, 32, 128, 2**25, 0, 0.0, 1, 3), bif.EUNSUPPORTED),  # int4 cache past 2^31 bytes
 ])
 def test_plan_create_rejects_bad_dims_without_a_device(L, dims, expect):
     st, handle = _create(L, *dims)

@@ -1,6 +1,6 @@
-"""GPU parity over 8-bit KV caches (OCP fp8 E4M3 and int8 codes with per-group
-scales): bifattn_decode_scaled through the C ABI against the fp64 oracle on
-the same seeded codes (MI355X only)."""
+"""GPU parity over quantized KV caches (OCP fp8 E4M3, int8 and int4 codes
+with per-group scales): bifattn_decode_scaled through the C ABI against the
+fp64 oracle on the same seeded codes (MI355X only)."""
 import numpy as np
 import pytest
 
@@ -10,7 +10,7 @@ import workloads
 
 from .gpu_util import run_decode, run_replicated, to_device
 from .parity import assert_parity, value_units
-from .pins_kvquant import KVS, code_table
+from .pins_kvquant import KVS, code_table, elements, fill_code, stored
 
 pytestmark = pytest.mark.gpu
 
@@ -38,14 +38,15 @@ def test_every_code_widens_exactly(kv, d):
     x = workloads.make_inputs(b, h, g, d, 1, 4, seed=900, kv=kv, lens=[0, 0])
     vc = np.zeros(g * d, np.uint8)
     vc[:codes.size] = codes
-    x["Vc"] = vc.reshape(g, 1, d)
+    x["Vc"] = stored(vc.reshape(g, 1, d), kv)
     x["q"][:] = 0
     x["v_scale"] = np.linspace(0.5, 3.0, g).astype(np.float32)
     print(f"[case] {kv} d={d} value table", flush=True)
     out = run_decode(x)
     for j in range(h):
         gam = j // (h // g)
-        exp = (table[x["Vc"][gam, 0]].astype(np.float32) * x["v_scale"][gam]).astype(np.float64)
+        vals = table[elements(x["Vc"], kv)[gam, 0]]
+        exp = (vals.astype(np.float32) * x["v_scale"][gam]).astype(np.float64)
         assert np.array_equal(out[:, j], np.broadcast_to(exp, out[:, j].shape)), (kv, j)
 
 
@@ -53,7 +54,7 @@ def test_every_code_widens_exactly(kv, d):
 def test_every_key_code(kv):
     """Two keys, one of them a decode key holding the code under test, q
     one-hot: the weight of the decode key is a sigmoid of the code's value,
-    for all 256 codes (NaN codes replaced by 0)."""
+    for every code (fp8 NaN codes replaced by 0)."""
     table = code_table(kv)
     b, h, d = 4, 64, 64
     x = workloads.make_inputs(b, h, 1, d, 1, 1, seed=901, kv=kv, lens=[1] * b)
@@ -61,10 +62,10 @@ def test_every_key_code(kv):
                                                         (b, h, d)).copy())
     x["Kc"][:] = 0
     x["Vc"][:] = 0
-    x["Vd"][:] = 0x38 if kv == "fp8_e4m3" else 1
-    kd = np.arange(256, dtype=np.uint8).reshape(b, d)
-    kd = np.where(np.isfinite(table[kd]), kd, np.uint8(0))
-    x["Kd"] = kd.reshape(b, 1, 1, d).astype(np.uint8)
+    x["Vd"][:] = fill_code(kv, 0x38 if kv == "fp8_e4m3" else 1)
+    kd = (np.arange(b * d) % table.size).reshape(b, d)
+    kd = np.where(np.isfinite(table[kd]), kd, 0)
+    x["Kd"] = stored(kd.reshape(b, 1, 1, d), kv)
     x["k_scale"] = np.array([2.0 ** -7], np.float32)
     x["v_scale"] = np.array([0.7], np.float32)
     print(f"[case] {kv} key table", flush=True)
@@ -181,8 +182,9 @@ def test_generation_loop_with_codes(kv):
     with bif.Plan(b, h, g, d, m_c, m_d, n=n, kv=kv) as plan:
         for step in range(m_d // n):
             q = workloads.f32_to_bf16_bits(rng.standard_normal((b, h, n, d), dtype=np.float32))
-            k_new = rng.integers(0, 256, (b, g, n, d), dtype=np.uint8)
-            v_new = rng.integers(0, 256, (b, g, n, d), dtype=np.uint8)
+            cols = workloads.cache_cols(d, kv)
+            k_new = rng.integers(0, 256, (b, g, n, cols), dtype=np.uint8)
+            v_new = rng.integers(0, 256, (b, g, n, cols), dtype=np.uint8)
             if kv == "fp8_e4m3":  # finite codes only
                 k_new[(k_new & 0x7F) == 0x7F] = 0
                 v_new[(v_new & 0x7F) == 0x7F] = 0

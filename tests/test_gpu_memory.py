@@ -53,6 +53,8 @@ CASES = [
     (40, 32, 1, 128, 1000, 64, 1, "bf16", "bifurcated", "1"),  # many-row, side stream
     (8, 32, 32, 128, 600, 120, 4, "fp8_e4m3", "bifurcated", None),
     (5, 16, 4, 64, 300, 40, 1, "int8", "standard", None),      # standard path
+    (40, 32, 1, 128, 1000, 64, 2, "int4", "bifurcated", "1"),  # int4 many-row, side stream
+    (5, 16, 4, 64, 300, 40, 1, "int4", "standard", None),
 ]
 
 
@@ -91,7 +93,7 @@ def test_canaries_around_output_and_caches(case, monkeypatch):
         if m_d >= n:
             room = torch.from_numpy(np.minimum(x["lens"], m_d - n)).cuda()
             rng = np.random.default_rng(3)
-            codes = rng.integers(0, 127, (b, g, n, d), dtype=np.uint8)
+            codes = rng.integers(0, 127, (b, g, n, workloads.cache_cols(d, kv)), dtype=np.uint8)
             new = (workloads.f32_to_bf16_bits(rng.standard_normal((b, g, n, d), dtype=np.float32))
                    if kv == "bf16" else codes)
             bif.bifattn_append_kv(plan, cache_to_device(new, kv), cache_to_device(new, kv), Kd, Vd,

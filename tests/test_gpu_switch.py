@@ -33,7 +33,7 @@ def run_path(x, path, scale=0.0, expect=bif.OK):
 
 
 # b, h, g, d, m_c, m_d_max, n, kv: every tile count (p*n = 1..64 rows), both
-# head dims, ragged tails, context-only samples, several tokens, 8-bit caches.
+# head dims, ragged tails, context-only samples, several tokens, 8-/4-bit caches.
 STD_CASES = [
     (4, 4, 4, 64, 128, 16, 1, "bf16"),
     (3, 8, 8, 128, 1000, 77, 1, "bf16"),
@@ -46,6 +46,8 @@ STD_CASES = [
     (2, 4, 2, 128, 96, 0, 1, "bf16"),         # no decode cache
     (4, 16, 4, 128, 400, 60, 2, "fp8_e4m3"),
     (5, 32, 1, 64, 333, 50, 1, "int8"),
+    (6, 32, 1, 128, 300, 40, 1, "int4"),      # two query tiles
+    (4, 8, 2, 64, 600, 90, 3, "int4"),
 ]
 
 

@@ -40,13 +40,14 @@ def _run_plan(x, case, path="auto"):
 
 # Calls in a row on one GPU, each smaller than the one before: the few-row
 # path of a 7B-shaped MHA layer, the many-row path (MQA), fp8 caches with
-# draft tokens, a grouped layer, and the standard path of a tiny layer.
+# draft tokens, a grouped layer, int4 caches, and a tiny layer.
 SEQUENCE = [
     # b, h, g, d, m_c, m_d, n, kv, path
     (16, 32, 32, 128, 4096, 256, 1, "bf16", "auto"),            # few-row, one launch
     (24, 32, 1, 128, 2000, 64, 1, "bf16", "bifurcated"),        # many-row context kernel
     (8, 32, 32, 128, 600, 120, 4, "fp8_e4m3", "bifurcated"),    # draft tokens, fp8
     (7, 32, 8, 128, 700, 129, 1, "int8", "auto"),               # standard path
+    (3, 8, 2, 64, 200, 30, 1, "int4", "bifurcated"),            # int4 codes
     (4, 4, 4, 64, 128, 16, 1, "bf16", "bifurcated"),
 ]
 

@@ -83,7 +83,8 @@ class Workload:
 # samples over 16k; and a GQA layer (8 KV groups) with 256 samples over 32k
 # and ragged decode lengths uniform in [1, 1024]. Then the 32-sample MHA layer
 # verifying 4 draft tokens per sample in one step (speculative decoding), and
-# the 32-sample MHA and the MQA layer with 8-bit KV caches.
+# the 32-sample MHA and the MQA layer with 8-bit KV caches, and the 32-sample
+# MHA layer with int4 caches.
 WORKLOADS = {
     w.name: w
     for w in (
@@ -98,6 +99,7 @@ WORKLOADS = {
         Workload("mha7b_b32_mc8k_md512_int8", 32, 32, 32, 128, 8192, 512, False, 1008, 1, "int8"),
         Workload("mqa_b128_mc16k_md512_fp8", 128, 32, 1, 128, 16384, 512, False, 1009, 1,
                  "fp8_e4m3"),
+        Workload("mha7b_b32_mc8k_md512_int4", 32, 32, 32, 128, 8192, 512, False, 1010, 1, "int4"),
     )
 }
 WORKLOAD_ORDER = list(WORKLOADS)
