@@ -112,6 +112,22 @@ struct LaunchEvents {
   hipEvent_t stop = nullptr;
 };
 
+// XCD-aware order of the many-row context work-groups. Logical id
+// chunk * rows + rb is work-group (key chunk, row block rb); the row blocks
+// of one chunk read the same keys and should share one XCD's L2. The
+// hardware hands dispatch ids to the kXcds XCDs round robin (id % kXcds), so
+// XCD x's k-th work-group (id kXcds*k + x) takes row block k % rows of its
+// (k / rows)-th chunk among the whole chunks every XCD gets (chunks /
+// kXcds of them, consecutive); the ids past those take the remaining chunks
+// in order. A bijection of [0, chunks * rows).
+constexpr int kXcds = 8;
+__host__ __device__ constexpr int xcd_logical(int bid, int chunks, int rows) {
+  const int full = chunks / kXcds;  // whole chunks per XCD
+  const int x = bid % kXcds, k = bid / kXcds;
+  if (k < full * rows) return ((x * full + k / rows) * rows) + k % rows;
+  return bid;  // ids from kXcds * full * rows on: the remaining chunks in order
+}
+
 // Launch the partial kernel over n_ctx_blocks + n_ctx_small_blocks +
 // n_dec_blocks work-groups.
 hipError_t launch_partials(const PartialsParams& P, int d, int kv, int ctx_mode, int dec_tiles,

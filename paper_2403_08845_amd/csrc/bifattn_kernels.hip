@@ -924,15 +924,6 @@ __global__ __launch_bounds__(kThreads) void standard_kernel(PartialsParams P) {
                               reinterpret_cast<float*>(lds + QSLOTS));
 }
 
-// XCD-aware order for the large context path: the hardware hands work-group
-// ids to the 8 XCDs round robin, so logical ids that must share an L2 (the
-// row blocks of one key chunk) are spread with stride 8 in dispatch order.
-__device__ __forceinline__ int xcd_logical(int bid, int n) {
-  constexpr int X = 8;
-  const int per = n / X;
-  if (bid >= per * X) return bid;  // ragged remainder keeps its id
-  return (bid % X) * per + bid / X;
-}
 
 // Context part, many query rows per group: work-group (group gam, key split
 // s, row block rb) of 128 query rows, eight waves with one 16-row query
@@ -958,7 +949,7 @@ __device__ __forceinline__ void ctx_large_body(const PartialsParams& P) {
   typedef Raw<KV::bytes(HW)> VR;  // a lane's HW elements of a value row
   typedef typename VR::type VH;
   __shared__ __attribute__((aligned(16))) u32x4 lds[2 * OPS * 64];
-  const int blk = xcd_logical(blockIdx.x, P.n_ctx_blocks);
+  const int blk = xcd_logical(blockIdx.x, P.g * P.S_c, P.ctx_row_blocks);
   const int rb = blk % P.ctx_row_blocks;
   const int sg = blk / P.ctx_row_blocks;
   const int s = sg % P.S_c, gam = sg / P.S_c;
@@ -1150,7 +1141,7 @@ __device__ __forceinline__ void ctx_wide_body(const PartialsParams& P) {
   constexpr int FULL = LOADS - (LPW - 1) * NW;  // waves with LPW loads; the rest have LPW - 1
   static_assert(STAGE % 1024 == 0 && KAREA % 1024 == 0, "stage areas are whole loads");
   __shared__ __attribute__((aligned(1024))) unsigned char lds[NB * STAGE];
-  const int blk = xcd_logical(blockIdx.x, P.n_ctx_blocks);
+  const int blk = xcd_logical(blockIdx.x, P.g * P.S_c, P.ctx_row_blocks);
   const int rb = blk % P.ctx_row_blocks;
   const int sg = blk / P.ctx_row_blocks;
   const int s = sg % P.S_c, gam = sg / P.S_c;

@@ -2,7 +2,7 @@
 // and UndefinedBehaviorSanitizer, linked with launch stand-ins and run
 // without a GPU: every argument check, dimension limits up to the largest
 // values the types hold, the allocation-free entry point's size check, the
-// status strings. Exit status 0 when every call returns what the header
+// status strings, and the many-row kernels' XCD order of work-groups. Exit status 0 when every call returns what the header
 // documents.
 #include <cmath>
 #include <cstdint>
@@ -10,7 +10,10 @@
 #include <cstring>
 #include <limits>
 
+#include <vector>
+
 #include "bifattn.h"
+#include "bifattn_internal.h"
 
 static int failures = 0;
 #define EXPECT(call, ...)                                                              \
@@ -41,7 +44,45 @@ static bifattn_dims_t dims(int b, int h, int g, int d, int m_c, int m_d, float s
   return x;
 }
 
+// The many-row context kernels' dispatch-id mapping: a permutation of the
+// logical ids, every row block of each of the first kXcds * (chunks / kXcds)
+// chunks on one XCD (dispatch id % kXcds), and, when each XCD's share of ids
+// holds whole chunks, the plain strided order (id % kXcds) * share + id / kXcds.
+static void check_xcd_mapping() {
+  using bifattn::kXcds;
+  using bifattn::xcd_logical;
+  for (int chunks = 1; chunks <= 70; ++chunks)
+    for (int rows = 1; rows <= 20; ++rows) {
+      const int n = chunks * rows, whole = kXcds * (chunks / kXcds);
+      std::vector<int> seen(n, 0), xcd(chunks, -1);
+      for (int bid = 0; bid < n; ++bid) {
+        const int l = xcd_logical(bid, chunks, rows);
+        if (l < 0 || l >= n || seen[l]++) {
+          std::fprintf(stderr, "xcd mapping not a permutation: chunks %d rows %d id %d\n", chunks,
+                       rows, bid);
+          ++failures;
+          return;
+        }
+        const int c = l / rows;
+        if (c < whole) {
+          if (xcd[c] == -1) xcd[c] = bid % kXcds;
+          if (xcd[c] != bid % kXcds) {
+            std::fprintf(stderr, "chunk %d split over XCDs: chunks %d rows %d\n", c, chunks, rows);
+            ++failures;
+          }
+        }
+        const int share = n / kXcds;
+        if (n % kXcds == 0 && share % rows == 0 && l != (bid % kXcds) * share + bid / kXcds) {
+          std::fprintf(stderr, "xcd mapping not the strided order: chunks %d rows %d\n", chunks,
+                       rows);
+          ++failures;
+        }
+      }
+    }
+}
+
 int main() {
+  check_xcd_mapping();
   const int BIG = std::numeric_limits<int32_t>::max();
   bifattn_plan_t plan = reinterpret_cast<bifattn_plan_t>(1);
   EXPECT(bifattn_plan_create(nullptr, &plan), BIFATTN_EINVAL);
