@@ -175,20 +175,19 @@ bifattn_status_t plan_splits(bifattn_plan_s* P, bool allow_fork = true) {
     // for decode work-groups), when the decode part is large (16 MiB or more)
     // and comparable to the context part: its HBM time at ~5 TB/s above half
     // the context's matrix time at ~1 PFLOP/s. Otherwise both parts run one
-    // after the other on the call's stream, and bf16 caches with d = 128 take
-    // the 32x32 MFMA context kernel (work-groups of eight waves of 32 rows,
-    // one per CU, from 256 rows per group, else of four, two per CU), which
-    // fills its CUs' registers and so leaves no room for decode work beside
-    // it. BIFATTN_FORK=0/1 and BIFATTN_CTX_WIDE=0/1 force either choice (d = 64
-    // and 8-bit caches always take the kernel of 16-row waves).
+    // after the other on the call's stream, and d = 128 takes the 32x32 MFMA
+    // context kernel (work-groups of eight waves of 32 rows, one per CU, from
+    // 256 rows per group, else of four, two per CU), which fills its CUs'
+    // registers and so leaves no room for decode work beside it.
+    // BIFATTN_FORK=0/1 and BIFATTN_CTX_WIDE=0/1 force either choice (d = 64
+    // always takes the kernel of 16-row waves).
     const double dec_bytes = 2.0 * d.b * d.g * (double)d.m_d_max * kv_row_bytes(d.d, d.kv_type);
     const double ctx_flops = 4.0 * d.h * P->ntok * d.d * (double)d.b * d.m_c;
     const int fork_env = env_switch("BIFATTN_FORK");
     const bool big_decode = dec_bytes >= 16.0 * (1 << 20) && dec_bytes / 5e12 > 0.5 * ctx_flops / 1e15;
     P->fork = allow_fork && d.m_d_max > 0 && (fork_env == -1 ? big_decode : fork_env == 1);
     const int wide_env = env_switch("BIFATTN_CTX_WIDE");
-    const bool wide = d.d == 128 && d.kv_type == BIFATTN_KV_BF16 &&
-                      (wide_env == -1 ? !P->fork : wide_env == 1);
+    const bool wide = d.d == 128 && (wide_env == -1 ? !P->fork : wide_env == 1);
     P->ctx_wide = wide ? (M >= 256 ? 8 : 4) : 0;
     const int block_rows = wide ? 32 * P->ctx_wide : kLargeRowsPerBlock;
     const int key_step = wide ? 64 : kTileKeys;  // keys per stage of the kernel's loop

@@ -1122,7 +1122,7 @@ __device__ __forceinline__ f32x16 mfma32(const u32x4& a, const u32x4& b, const f
                                                  __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
 }
 
-template <int NW, int NB, int SK>
+template <int NW, int NB, int SK, typename KV>
 __device__ __forceinline__ void ctx_wide_body(const PartialsParams& P) {
   using wide::D;
   using wide::RB;
@@ -1149,8 +1149,13 @@ __device__ __forceinline__ void ctx_wide_body(const PartialsParams& P) {
   const int nkeys = min(P.m_c, k0 + P.ctx_keys) - k0;
   const int lane = threadIdx.x & 63, wave = wave_id();
   const int j = lane & 31, h = lane >> 5;
-  const uint8_t* kchunk = P.Kc + ((size_t)gam * P.m_c + k0) * RB;
-  const uint8_t* vchunk = P.Vc + ((size_t)gam * P.m_c + k0) * RB;
+  // Caches of bf16 load straight into LDS; code caches are staged through
+  // registers and widened to bf16 on the way (same LDS layout).
+  constexpr bool kDirect = KV::BITS == 16;
+  static_assert(kDirect || NB == 2, "code caches use two stage buffers");
+  constexpr int CRB = KV::bytes(D);  // bytes per cache row in memory
+  const uint8_t* kchunk = P.Kc + ((size_t)gam * P.m_c + k0) * CRB;
+  const uint8_t* vchunk = P.Vc + ((size_t)gam * P.m_c + k0) * CRB;
   const float sl2 = unit_scale_log2(P, gam);
   const int M = P.M, p = P.p;
   const int row0 = rb * (32 * NW) + wave * 32;
@@ -1171,8 +1176,8 @@ __device__ __forceinline__ void ctx_wide_body(const PartialsParams& P) {
   }
   auto fetch = [&](int key0, int buf) {
     const int rows = nkeys - key0;  // rows from the stage's first key to the chunk's end
-    const __amdgpu_buffer_rsrc_t rk = rows_rsrc(kchunk + (size_t)key0 * RB, rows, RB);
-    const __amdgpu_buffer_rsrc_t rv = rows_rsrc(vchunk + (size_t)key0 * RB, rows, RB);
+    const __amdgpu_buffer_rsrc_t rk = rows_rsrc(kchunk + (size_t)key0 * CRB, rows, CRB);
+    const __amdgpu_buffer_rsrc_t rv = rows_rsrc(vchunk + (size_t)key0 * CRB, rows, CRB);
 #pragma unroll
     for (int u = 0; u < LPW; ++u) {
       if (u < nload) {
@@ -1207,10 +1212,55 @@ __device__ __forceinline__ void ctx_wide_body(const PartialsParams& P) {
     for (int ks = 0; ks < KSTEPS; ++ks)
       qop[ks] = qr ? load16(qr + 16 * ks + 8 * h) ^ P.q_sign : u32x4{0, 0, 0, 0};
   }
-  const int nstages = (nkeys + SK - 1) / SK;
+  // Code caches: load q = tid + 64 NW u of a stage reads 16 bytes of codes
+  // (E elements, chunk c16 of row `row` of K, then of V) and writes them,
+  // widened, as E / 8 bf16 slots of that row in LDS.
+  constexpr int E = 128 / KV::BITS;        // elements per 16-byte load
+  constexpr int CPR = CRB / 16;            // loads per row
+  constexpr int SLOADS = 2 * SK * CPR;     // loads per stage
+  constexpr int SPT = kDirect ? 1 : (SLOADS + 64 * NW - 1) / (64 * NW);  // per thread
+  static_assert(kDirect || SLOADS % (64 * NW) == 0, "whole loads per thread");
+  u32x4 sreg[SPT];
+  auto stage_get = [&](int key0) {
+    const int rows = nkeys - key0;
+    const __amdgpu_buffer_rsrc_t rk = rows_rsrc(kchunk + (size_t)key0 * CRB, rows, CRB);
+    const __amdgpu_buffer_rsrc_t rv = rows_rsrc(vchunk + (size_t)key0 * CRB, rows, CRB);
 #pragma unroll
-  for (int t = 0; t < NB - 1; ++t)
-    if (t < nstages) fetch(t * SK, t);
+    for (int u = 0; u < SPT; ++u) {
+      const int q = (int)threadIdx.x + 64 * NW * u;
+      const bool is_v = q >= SK * CPR;  // wave-uniform: whole waves per half
+      const int qq = is_v ? q - SK * CPR : q;
+      sreg[u] = Raw<16>::load(is_v ? rv : rk, boff((uint32_t)qq * 16));
+    }
+  };
+  auto stage_put = [&](int buf) {
+#pragma unroll
+    for (int u = 0; u < SPT; ++u) {
+      const int q = (int)threadIdx.x + 64 * NW * u;
+      const bool is_v = q >= SK * CPR;
+      const int qq = is_v ? q - SK * CPR : q;
+      const int row = qq / CPR, c16 = qq % CPR;
+      unsigned char* dst = lds + buf * STAGE + (is_v ? KAREA + row * VROW : row * KROW) + c16 * E * 2;
+      const u32x4& w = sreg[u];
+      if constexpr (KV::BITS == 8) {
+        *(lds_u32x4*)dst = Widen8<KV>::run(u32x2{w[0], w[1]});
+        *(lds_u32x4*)(dst + 16) = Widen8<KV>::run(u32x2{w[2], w[3]});
+      } else {
+#pragma unroll
+        for (int k = 0; k < 4; ++k) *(lds_u32x4*)(dst + 16 * k) = Widen8<KV>::run(w[k]);
+      }
+    }
+  };
+  const int nstages = (nkeys + SK - 1) / SK;
+  if constexpr (kDirect) {
+#pragma unroll
+    for (int t = 0; t < NB - 1; ++t)
+      if (t < nstages) fetch(t * SK, t);
+  } else {
+    stage_get(0);
+    stage_put(0);
+    if (nstages > 1) stage_get(SK);
+  }
 
   // Per-lane LDS read bases (from a stage buffer's start): key operand of row
   // j, half h; value chunk of key 4(q/2) + i'/4, dims 16(q%2) + 4(i'%4).
@@ -1228,12 +1278,23 @@ __device__ __forceinline__ void ctx_wide_body(const PartialsParams& P) {
 
   for (int st = 0; st < nstages; ++st) {
     const int buf = st % NB;
-    // After this wave's wait, the barrier hands every wave's part of stage st
-    // to all waves and frees buffer (st - 1) % NB, which all have read.
-    wait_stage(st + 1 >= nstages);
-    __builtin_amdgcn_s_barrier();
-    asm volatile("" ::: "memory");
-    if (st + NB - 1 < nstages) fetch((st + NB - 1) * SK, (st + NB - 1) % NB);
+    if constexpr (kDirect) {
+      // After this wave's wait, the barrier hands every wave's part of stage
+      // st to all waves and frees buffer (st - 1) % NB, which all have read.
+      wait_stage(st + 1 >= nstages);
+      __builtin_amdgcn_s_barrier();
+      asm volatile("" ::: "memory");
+      if (st + NB - 1 < nstages) fetch((st + NB - 1) * SK, (st + NB - 1) % NB);
+    } else {
+      // The barrier hands stage st (written from registers) to all waves and
+      // frees the other buffer: stage st + 1 goes there from the registers
+      // loaded a stage ago, and stage st + 2 is loaded into them.
+      __syncthreads();
+      if (st + 1 < nstages) {
+        stage_put(buf ^ 1);
+        if (st + 2 < nstages) stage_get((st + 2) * SK);
+      }
+    }
     if (!active) continue;
     const unsigned char* kb = lds + buf * STAGE + kbase;
     const unsigned char* vb = lds + buf * STAGE + vbase;
@@ -1321,11 +1382,12 @@ __device__ __forceinline__ void ctx_wide_body(const PartialsParams& P) {
   }
 }
 
-template <int NW, int NB, int SK>
+template <int NW, int NB, int SK, typename KV>
 __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(2))) void
 ctx_wide_kernel(PartialsParams P) {
-  ctx_wide_body<NW, NB, SK>(P);
+  ctx_wide_body<NW, NB, SK, KV>(P);
 }
+
 
 
 // Grid: n_ctx_small_blocks work-groups of the few-row context path, then
@@ -1548,6 +1610,23 @@ hipError_t launch_standard_d(const PartialsParams& P, int kv, int tiles, hipStre
   }
 }
 
+template <typename KV>
+hipError_t launch_ctx_wide_kv(const PartialsParams& P, hipStream_t stream,
+                              const LaunchEvents& ev) {
+  constexpr bool kDirect = KV::BITS == 16;
+  // eight waves: 128-key stages, two in LDS (fewer barriers than 64-key
+  // stages, measured 3-5% faster); chunks of a multiple of 64 keys (three
+  // 64-key stages in LDS for bf16, two for code caches, which stage a
+  // third in registers)
+  if (P.ctx_wide == 8) {
+    if (P.ctx_keys % 128 == 0)
+      return launch(ctx_wide_kernel<8, 2, 128, KV>, P.n_ctx_blocks, 512, stream, ev, P);
+    return launch(ctx_wide_kernel<8, kDirect ? 3 : 2, 64, KV>, P.n_ctx_blocks, 512, stream, ev, P);
+  }
+  if (P.ctx_wide == 4) return launch(ctx_wide_kernel<4, 2, 64, KV>, P.n_ctx_blocks, 256, stream, ev, P);
+  return hipErrorInvalidValue;
+}
+
 template <int D>
 hipError_t launch_ctx_large_d(const PartialsParams& P, int kv, hipStream_t stream,
                               const LaunchEvents& ev) {
@@ -1636,15 +1715,14 @@ hipError_t launch_ctx_large(const PartialsParams& P, int d, int kv, hipStream_t 
                             const LaunchEvents& ev) {
   if (P.n_ctx_blocks == 0) return hipSuccess;
   if (P.ctx_wide) {
-    if (d != 128 || kv != kKvBf16) return hipErrorInvalidValue;
-    // eight waves: 128-key stages, two in LDS (fewer barriers than 64-key
-    // stages, measured 3-5% faster); chunks of a multiple of 64 keys
-    if (P.ctx_wide == 8)
-      return P.ctx_keys % 128 == 0
-                 ? launch(ctx_wide_kernel<8, 2, 128>, P.n_ctx_blocks, 512, stream, ev, P)
-                 : launch(ctx_wide_kernel<8, 3, 64>, P.n_ctx_blocks, 512, stream, ev, P);
-    if (P.ctx_wide == 4) return launch(ctx_wide_kernel<4, 2, 64>, P.n_ctx_blocks, 256, stream, ev, P);
-    return hipErrorInvalidValue;
+    if (d != 128) return hipErrorInvalidValue;
+    switch (kv) {
+      case kKvBf16: return launch_ctx_wide_kv<KvBf16>(P, stream, ev);
+      case kKvFp8: return launch_ctx_wide_kv<KvFp8>(P, stream, ev);
+      case kKvInt8: return launch_ctx_wide_kv<KvInt8>(P, stream, ev);
+      case kKvInt4: return launch_ctx_wide_kv<KvInt4>(P, stream, ev);
+      default: return hipErrorInvalidValue;
+    }
   }
   if (d == 128) return launch_ctx_large_d<128>(P, kv, stream, ev);
   if (d == 64) return launch_ctx_large_d<64>(P, kv, stream, ev);

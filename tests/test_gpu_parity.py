@@ -375,3 +375,25 @@ def test_many_row_context_kernels(case, monkeypatch):
             print(f"[case] many-row {case} wide={wide} {info}", flush=True)
             out = run_decode(x, plan=plan)
         _report(f"many-row {case} wide={wide}", *assert_parity(out, ref, f"{case} wide={wide}", x=x))
+
+
+
+@pytest.mark.parametrize("kv", ["fp8_e4m3", "int8", "int4"])
+@pytest.mark.parametrize("case", WIDE_CASES, ids=lambda c: "b%d_h%d_g%d_d%d_mc%d_md%d_n%d" % c)
+def test_many_row_context_kernels_code_caches(case, kv, monkeypatch):
+    """Both many-row context kernels over 8-bit and int4 caches: the 32x32
+    kernel stages the codes through registers and widens them into its LDS
+    stages, the 16x16 kernel widens them while staging its tiles."""
+    b, h, g, d, m_c, m_d, n = case
+    x = workloads.make_inputs(b, h, g, d, m_c, m_d, seed=1650 + m_c, ragged=True, n=n, kv=kv)
+    ref = oracle.attention(**x)
+    monkeypatch.setenv("BIFATTN_FORK", "0")
+    for wide in ("1", "0"):
+        monkeypatch.setenv("BIFATTN_CTX_WIDE", wide)
+        with bif.Plan(b, h, g, d, m_c, m_d, n=n, kv=kv, path="bifurcated") as plan:
+            info = plan.info()
+            assert info["ctx_kernel"] == (2 if wide == "1" else 1)
+            print(f"[case] many-row {kv} {case} wide={wide} {info}", flush=True)
+            out = run_decode(x, plan=plan)
+        _report(f"many-row {kv} {case} wide={wide}",
+                *assert_parity(out, ref, f"{kv} {case} wide={wide}", x=x))
