@@ -165,7 +165,7 @@ def calibrate_copy(reps: int = 5):
 
 
 KERNEL_NAMES = {"partials": "partials_kernel", "ctx_large": "ctx_large_kernel",
-                "ctx_wide": "ctx_wide_kernel"}
+                "ctx_wide": "ctx_wide_kernel", "standard": "standard_kernel"}
 
 
 def summarize_profile(stats_dir: str, fetch_dir: str, write_dir: str, workload: str, out_dir: str,
@@ -492,11 +492,16 @@ def main():
                     "traffic": measured_traffic(w.name, "partials"),
                     "avg_launch_us": round(dec_us, 3), "bytes_per_launch": dec_bytes}
     else:
+        # One launch: the few-row partial kernel, or the standard kernel where
+        # the plan takes the standard path.
+        standard = info["path"] == bif.PATHS["standard"]
+        kname = "standard" if standard else "partials"
+        what = "whole attention, rows written directly" if standard else "context + decode partials"
         gbs = B_kv / (part_us * 1e-6) / 1e9
-        roofline = {"kernel": "partials_kernel (context + decode partials)", "bound": "hbm",
+        roofline = {"kernel": f"{KERNEL_NAMES[kname]} ({what})", "bound": "hbm",
                     "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                     "frac": round(gbs / HBM_PEAK_GBS, 4),
-                    "traffic": measured_traffic(w.name, "partials"),
+                    "traffic": measured_traffic(w.name, kname),
                     "avg_launch_us": round(part_us, 3), "bytes_per_launch": B_kv}
     step_s = ms_per_step * 1e-3
     roofs = {"hbm_frac_step": round(B_kv / step_s / 1e9 / HBM_PEAK_GBS, 4),
