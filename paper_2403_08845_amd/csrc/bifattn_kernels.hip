@@ -1479,13 +1479,16 @@ __global__ __launch_bounds__(256) void combine_kernel(CombineParams C) {
   for (int k0 = 0; k0 < np; k0 += 64) {  // running max over chunks of 64 partials
     const int kn = min(64, np - k0);
     // Issue the first batch of value rows together with the statistics, so
-    // a chunk of up to BATCH partials costs one memory round trip.
+    // a chunk of up to BATCH partials costs one memory round trip; only the
+    // rows the chunk has are loaded (kn is wave-uniform).
     float v[BATCH][PER];
 #pragma unroll
     for (int u = 0; u < BATCH; ++u) {
-      const float* a = accp(k0 + min(u, kn - 1));
+      if (u < kn) {
+        const float* a = accp(k0 + u);
 #pragma unroll
-      for (int e = 0; e < PER; ++e) v[u][e] = a[e];
+        for (int e = 0; e < PER; ++e) v[u][e] = a[e];
+      }
     }
     const int k = k0 + lane;
     const float2 ml = k < np ? (k < C.S_c ? C.ctx_ml[idx(k)] : C.dec_ml[idx(k)])
@@ -1507,9 +1510,11 @@ __global__ __launch_bounds__(256) void combine_kernel(CombineParams C) {
       if (kb > 0) {
 #pragma unroll
         for (int u = 0; u < BATCH; ++u) {
-          const float* a = accp(k0 + min(kb + u, kn - 1));
+          if (kb + u < kn) {
+            const float* a = accp(k0 + kb + u);
 #pragma unroll
-          for (int e = 0; e < PER; ++e) v[u][e] = a[e];
+            for (int e = 0; e < PER; ++e) v[u][e] = a[e];
+          }
         }
       }
 #pragma unroll
@@ -1745,15 +1750,17 @@ hipError_t launch_combine(const CombineParams& C, int d, hipStream_t stream,
                           const LaunchEvents& ev) {
   const int rows = C.b * C.h;
   const int grid = (rows + 3) / 4;
-  // Batches of 8 value rows where a row has at most 8 partials (no loads of
-  // repeated rows; measured 0.4 us per step on the 32-sample MHA layer), else 16.
-  const bool small = C.S_c + C.S_d <= 8;
+  // One batch of value rows holds every partial of a row where it has at
+  // most 32 (one memory round trip), in the smallest of 8, 16, 32 rows.
+  const int np = C.S_c + C.S_d;
   if (d == 128)
-    return small ? launch(combine_kernel<128, 8>, grid, 256, stream, ev, C)
-                 : launch(combine_kernel<128, 16>, grid, 256, stream, ev, C);
+    return np <= 8 ? launch(combine_kernel<128, 8>, grid, 256, stream, ev, C)
+         : np <= 16 ? launch(combine_kernel<128, 16>, grid, 256, stream, ev, C)
+                    : launch(combine_kernel<128, 32>, grid, 256, stream, ev, C);
   if (d == 64)
-    return small ? launch(combine_kernel<64, 8>, grid, 256, stream, ev, C)
-                 : launch(combine_kernel<64, 16>, grid, 256, stream, ev, C);
+    return np <= 8 ? launch(combine_kernel<64, 8>, grid, 256, stream, ev, C)
+         : np <= 16 ? launch(combine_kernel<64, 16>, grid, 256, stream, ev, C)
+                    : launch(combine_kernel<64, 32>, grid, 256, stream, ev, C);
   return hipErrorInvalidValue;
 }
 
