@@ -486,7 +486,7 @@ __device__ __forceinline__ void load_q(u32x4 (&qop)[NT][D / 32], RowPtr row_ptr,
 //      those reads are bank-conflict free);
 //   V: lane (c, G) holds row 4e + G, dims DV*c .. DV*c+DV-1 (e = 0..7), which
 //      is already what its V^T operands need: formed on demand by a 16-bit
-//      transpose inside the lane (widening 8-bit codes on the way).
+//      transpose inside the lane (widening 8-bit or 4-bit codes on the way).
 // Loads go through buffer resources whose range ends at the item's last key,
 // so rows past it read as zero without a branch and without a memory access.
 template <int D, typename KV> struct TileRegs {
@@ -933,9 +933,9 @@ __global__ __launch_bounds__(kThreads) void standard_kernel(PartialsParams P) {
 // already in MFMA operand order (the V^T transpose is done once, on the way
 // in), and all eight waves read it. Each wave stages one eighth of a tile:
 // one K operand (d = 128; the first four waves for d = 64) and one 32-bit
-// word of half of the V^T operands, widening 8-bit codes to bf16 on the way. Tiles are double-buffered in LDS with
-// one barrier per tile, and fetched three tiles ahead into three rotating
-// register sets. Q^T operands stay in registers. Row blocks of one key
+// word of half of the V^T operands, widening 8-bit or 4-bit codes to bf16 on
+// the way. Tiles are double-buffered in LDS with one barrier per tile, and
+// fetched three tiles ahead into three rotating register sets. Q^T operands stay in registers. Row blocks of one key
 // chunk are scheduled on the same XCD so that they share its L2.
 template <int D, typename KV>
 __device__ __forceinline__ void ctx_large_body(const PartialsParams& P) {
@@ -1073,7 +1073,7 @@ ctx_large_kernel(PartialsParams P) {
 
 
 // ---------------------------------------------------------------------------
-// Context part, many query rows per group, bf16 caches with d = 128, on
+// Context part, many query rows per group, d = 128 (any cache type), on
 // v_mfma_f32_32x32x16_bf16 (lane l, j = l % 32, h = l / 32):
 //   A (32 x 16): lane holds A[j][8h .. 8h+7]
 //   B (16 x 32): lane holds B[8h .. 8h+7][j]
@@ -1091,9 +1091,11 @@ ctx_large_kernel(PartialsParams P) {
 // 4 + i/4, 8 + i/4, 12 + i/4 address; lane i' of group q addresses key
 // 16s + 8r + 4(q/2) + i'/4, dims 32t + 16(q%2) + 4(i'%4), read r = 0, 1).
 // Keys stream in stages of SK (64 or 128: two or four 32-key blocks)
-// through a ring of NB stage buffers in LDS, each filled straight from memory by buffer loads to
-// LDS (lane l's 16 bytes land at the instruction's base + 16 l, so the lane
-// chooses which chunk of which row to fetch). Rows are padded in LDS, key
+// through a ring of NB stage buffers in LDS of bf16 rows. bf16 caches fill
+// them straight from memory by buffer loads to LDS (lane l's 16 bytes land
+// at the instruction's base + 16 l, so the lane chooses which chunk of which
+// row to fetch); code caches load a stage into registers a stage ahead and
+// write it widened (stage_get / stage_put). Rows are padded in LDS, key
 // rows to 272 bytes and value rows to 288, which keeps both kinds of operand
 // reads free of bank conflicts (16 key rows of one read start 16 bytes
 // apart in the banks, the 4 value rows of one transposing read 32 bytes
@@ -1103,7 +1105,7 @@ ctx_large_kernel(PartialsParams P) {
 // filled buffer to every wave and releases the oldest for refilling.
 namespace wide {
 constexpr int D = 128;
-constexpr int RB = D * 2;             // bytes per bf16 row in memory
+constexpr int RB = D * 2;             // bytes per bf16 row
 constexpr int KSTEPS = D / 16;        // k-steps of the logits
 constexpr int DB = D / 32;            // 32-dim blocks of the output
 constexpr int KROW = RB + 16;         // padded key row in LDS
