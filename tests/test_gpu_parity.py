@@ -273,24 +273,43 @@ def test_draft_tokens_masked_tail_and_replicated():
 def test_side_stream_decode(case, monkeypatch):
     """Many-row plans may run the decode launch on a side stream beside the
     context kernel (the call's stream waits for it before the combine):
-    forced on and off, both outputs match the oracle, and they are bitwise
-    equal when the two plans split the context alike."""
+    forced on and off with either context kernel, every output matches the
+    oracle, and with the same kernel the two are bitwise equal when the plans
+    split the context alike."""
     b, h, g, d, m_c, m_d, n = case
     x = workloads.make_inputs(b, h, g, d, m_c, m_d, seed=1200 + m_c, ragged=True, n=n)
     ref = oracle.attention(**x)
-    runs = []
-    # the same context kernel both ways (by default a plan without the side
-    # stream may take the 32x32 MFMA kernel instead)
-    monkeypatch.setenv("BIFATTN_CTX_WIDE", "0")
-    for fork in ("0", "1"):
-        monkeypatch.setenv("BIFATTN_FORK", fork)
-        with bif.Plan(b, h, g, d, m_c, m_d, n=n) as plan:
-            splits = plan.info()["ctx_splits"]
-            out = run_decode(x, plan=plan)
-        _report(f"side stream {case} fork={fork}", *assert_parity(out, ref, f"{case} fork={fork}", x=x))
-        runs.append((splits, out))
-    if runs[0][0] == runs[1][0]:
-        assert np.array_equal(runs[0][1], runs[1][1])
+    for wide in ("0", "1"):
+        monkeypatch.setenv("BIFATTN_CTX_WIDE", wide)
+        runs = []
+        for fork in ("0", "1"):
+            monkeypatch.setenv("BIFATTN_FORK", fork)
+            with bif.Plan(b, h, g, d, m_c, m_d, n=n) as plan:
+                info = plan.info()
+                if b * (h // g) * n > 64:  # many rows per group (else the few-row launch)
+                    assert info["side_stream"] == int(fork)
+                    assert info["ctx_kernel"] == (2 if wide == "1" else 1)
+                out = run_decode(x, plan=plan)
+            _report(f"side stream {case} wide={wide} fork={fork}",
+                    *assert_parity(out, ref, f"{case} wide={wide} fork={fork}", x=x))
+            runs.append((info["ctx_splits"], out))
+        if runs[0][0] == runs[1][0]:
+            assert np.array_equal(runs[0][1], runs[1][1])
+
+
+def test_plan_rule_for_large_decode_parts(monkeypatch):
+    """Without overrides, a many-row plan whose decode part is large takes the
+    side stream; with 256 or more rows per group it keeps the 32x32 context
+    kernel on three quarters of the CUs, with fewer rows the 16x16 kernel."""
+    for var in ("BIFATTN_FORK", "BIFATTN_CTX_WIDE", "BIFATTN_CTX_WGS"):
+        monkeypatch.delenv(var, raising=False)
+    with bif.Plan(256, 32, 8, 128, 32768, 1024) as plan:  # 1024 rows per group
+        info = plan.info()
+        assert info["side_stream"] == 1 and info["ctx_kernel"] == 2
+        assert info["ctx_blocks"] <= 192
+    with bif.Plan(32, 32, 32, 128, 8192, 512, n=4) as plan:  # 128 rows per group
+        info = plan.info()
+        assert info["side_stream"] == 1 and info["ctx_kernel"] == 1
 
 
 def test_largest_context_rows_are_addressed():
