@@ -1202,17 +1202,22 @@ __device__ __forceinline__ void ctx_wide_body(const PartialsParams& P) {
   };
 
   // Q^T operands: k-step ks holds dims 16ks + 8h .. +7 of query row j.
+  // Rows past M load row M - 1 and are zeroed afterwards, so that the eight
+  // loads issue back to back (a load under a per-lane condition waits for
+  // its data before the next one issues).
   u32x4 qop[KSTEPS];
   {
     const int row = row0 + j;
-    const uint16_t* qr = nullptr;
-    if (row < M) {
-      const int i = row / p, jp = row - i * p;
-      qr = P.q + ((size_t)i * P.h + (size_t)gam * p + jp) * D;
-    }
+    const bool valid = row < M;
+    const int rr = valid ? row : M - 1;
+    const int i = rr / p, jp = rr - i * p;
+    const uint16_t* qr = P.q + ((size_t)i * P.h + (size_t)gam * p + jp) * D;
+#pragma unroll
+    for (int ks = 0; ks < KSTEPS; ++ks) qop[ks] = load16(qr + 16 * ks + 8 * h);
 #pragma unroll
     for (int ks = 0; ks < KSTEPS; ++ks)
-      qop[ks] = qr ? load16(qr + 16 * ks + 8 * h) ^ P.q_sign : u32x4{0, 0, 0, 0};
+#pragma unroll
+      for (int w = 0; w < 4; ++w) qop[ks][w] = valid ? qop[ks][w] ^ P.q_sign : 0u;
   }
   // Code caches: load q = tid + 64 NW u of a stage reads 16 bytes of codes
   // (E elements, chunk c16 of row `row` of K, then of V) and writes them,
