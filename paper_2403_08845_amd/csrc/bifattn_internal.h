@@ -26,6 +26,7 @@ constexpr int kMaxP = 64;
 // tile's maximum exceeds it by more than this many powers of two, which keeps
 // every weight below 2^kRescaleSlack.
 constexpr float kRescaleSlack = 8.0f;
+constexpr float kSumBound = 256.0f;  // 2^kRescaleSlack
 
 // Device-side status bits.
 constexpr int kStatusLens = 1;

@@ -1124,6 +1124,63 @@ __device__ __forceinline__ f32x16 mfma32(const u32x4& a, const u32x4& b, const f
                                                  __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
 }
 
+// Transposing LDS read (ds_read_b64_tr_b16) at LDS byte address addr + OFF,
+// issued as inline assembly: the compiler places a wait for every
+// buffer-to-LDS load in flight before its own form of this read (it cannot
+// tell that those loads fill the other stage buffer), which would expose the
+// next stage's load latency once per stage. The caller orders the read after
+// the stage's own loads (wait and barrier) and waits for its data with
+// lds_wait_tr before using it.
+template <int OFF>
+__device__ __forceinline__ u32x2 ds_tr16(uint32_t addr) {
+  u32x2 r;
+  asm volatile("ds_read_b64_tr_b16 %0, %1 offset:%2" : "=v"(r) : "v"(addr), "i"(OFF) : "memory");
+  return r;
+}
+// Waits until every LDS read issued so far has returned; the registers pass
+// through the statement, so no use of them can move above the wait.
+__device__ __forceinline__ void lds_wait_tr(u32x2 (&w)[16]) {
+  asm volatile("s_waitcnt lgkmcnt(0)"
+               : "+v"(w[0]), "+v"(w[1]), "+v"(w[2]), "+v"(w[3]), "+v"(w[4]), "+v"(w[5]),
+                 "+v"(w[6]), "+v"(w[7]), "+v"(w[8]), "+v"(w[9]), "+v"(w[10]), "+v"(w[11]),
+                 "+v"(w[12]), "+v"(w[13]), "+v"(w[14]), "+v"(w[15])
+               :
+               : "memory");
+}
+// Key operand read (ds_read_b128) at LDS byte address addr + OFF, by inline
+// assembly like ds_tr16 (so that its wait can be placed by the caller, with
+// lds_wait_k, after the value products it overlaps).
+template <int OFF>
+__device__ __forceinline__ u32x4 ds_b128(uint32_t addr) {
+  u32x4 r;
+  asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(r) : "v"(addr), "i"(OFF) : "memory");
+  return r;
+}
+__device__ __forceinline__ void lds_wait_k(u32x4 (&w)[8]) {
+  asm volatile("s_waitcnt lgkmcnt(0)"
+               : "+v"(w[0]), "+v"(w[1]), "+v"(w[2]), "+v"(w[3]), "+v"(w[4]), "+v"(w[5]),
+                 "+v"(w[6]), "+v"(w[7])
+               :
+               : "memory");
+}
+// The eight key operands (k-steps 0..7) of one 32-key block of key rows
+// padded to 272 bytes: read ks at 32 ks bytes from the lane's base.
+__device__ __forceinline__ void read_k_block(uint32_t a, u32x4 (&w)[8]) {
+  w[0] = ds_b128<0>(a); w[1] = ds_b128<32>(a); w[2] = ds_b128<64>(a); w[3] = ds_b128<96>(a);
+  w[4] = ds_b128<128>(a); w[5] = ds_b128<160>(a); w[6] = ds_b128<192>(a); w[7] = ds_b128<224>(a);
+}
+// The sixteen transposing reads of one 32-key block's V^T operands: read
+// (ss, t, r) of k-step ss, dims 32t .. 32t+31, half r, into w[8 ss + 2 t + r].
+template <int VROW>
+__device__ __forceinline__ void read_vt_block(uint32_t a, u32x2 (&w)[16]) {
+#define BIFATTN_TR(ss, t, r) w[8 * (ss) + 2 * (t) + (r)] = ds_tr16<(16 * (ss) + 8 * (r)) * VROW + 64 * (t)>(a)
+  BIFATTN_TR(0, 0, 0); BIFATTN_TR(0, 0, 1); BIFATTN_TR(0, 1, 0); BIFATTN_TR(0, 1, 1);
+  BIFATTN_TR(0, 2, 0); BIFATTN_TR(0, 2, 1); BIFATTN_TR(0, 3, 0); BIFATTN_TR(0, 3, 1);
+  BIFATTN_TR(1, 0, 0); BIFATTN_TR(1, 0, 1); BIFATTN_TR(1, 1, 0); BIFATTN_TR(1, 1, 1);
+  BIFATTN_TR(1, 2, 0); BIFATTN_TR(1, 2, 1); BIFATTN_TR(1, 3, 0); BIFATTN_TR(1, 3, 1);
+#undef BIFATTN_TR
+}
+
 template <int NW, int NB, int SK, typename KV>
 __device__ __forceinline__ void ctx_wide_body(const PartialsParams& P) {
   using wide::D;
@@ -1280,7 +1337,7 @@ __device__ __forceinline__ void ctx_wide_body(const PartialsParams& P) {
   for (int t = 0; t < DB; ++t)
 #pragma unroll
     for (int v = 0; v < 16; ++v) acc[t][v] = 0.f;
-  float mref = kNegInf, thr = kNegInf, lsum = 0.f;
+  float mref = kNegInf, lsum = 0.f;
   const bool active = row0 < M;  // wave-uniform
 
   for (int st = 0; st < nstages; ++st) {
@@ -1304,8 +1361,14 @@ __device__ __forceinline__ void ctx_wide_body(const PartialsParams& P) {
     }
     if (!active) continue;
     const unsigned char* kb = lds + buf * STAGE + kbase;
-    const unsigned char* vb = lds + buf * STAGE + vbase;
+    const uint32_t vaddr = (uint32_t)(uintptr_t)(lds_void*)(lds + buf * STAGE + vbase);
     const int rem = nkeys - st * SK;  // valid keys from the stage's first
+    // The key operands of block 0 of the stage; each later block's are read
+    // during the previous block's value products.
+    const uint32_t kaddr = (uint32_t)(uintptr_t)(lds_void*)(kb);
+    u32x4 kw[KSTEPS];
+    read_k_block(kaddr, kw);
+    lds_wait_k(kw);
 #pragma unroll
     for (int b = 0; b < SK / 32; ++b) {
       // S^T block: keys 32b .. 32b+31 of the stage
@@ -1313,10 +1376,12 @@ __device__ __forceinline__ void ctx_wide_body(const PartialsParams& P) {
 #pragma unroll
       for (int v = 0; v < 16; ++v) sacc[v] = 0.f;
 #pragma unroll
-      for (int ks = 0; ks < KSTEPS; ++ks) {
-        const u32x4 kop = *(const lds_u32x4*)(kb + 32 * b * KROW + 32 * ks);
-        sacc = mfma32(kop, qop[ks], sacc);
-      }
+      for (int ks = 0; ks < KSTEPS; ++ks) sacc = mfma32(kw[ks], qop[ks], sacc);
+      // this block's V^T operands, read while the weights are formed (after
+      // the key operand reads, whose waits would otherwise cover them too)
+      __builtin_amdgcn_sched_barrier(0);
+      u32x2 vw[16];
+      read_vt_block<VROW>(vaddr + 32 * b * VROW, vw);
       float x[16];
 #pragma unroll
       for (int v = 0; v < 16; ++v) x[v] = sacc[v];
@@ -1326,26 +1391,41 @@ __device__ __forceinline__ void ctx_wide_body(const PartialsParams& P) {
         for (int v = 0; v < 16; ++v)
           if (8 * (v / 4) + 4 * h + (v & 3) >= nv) x[v] = kNegInf;
       }
-      float lmax = x[0];
+      // Weights against the current reference first: while their sum stays
+      // within 2^kRescaleSlack no weight exceeds it, and the reference keeps
+      // its value (a raise needs a weight above 2^kRescaleSlack). Otherwise,
+      // and on the first block, the row's maximum decides the raise and the
+      // weights are formed again.
+      float pr[16];
+      float ps;
+      {
+        const float nbase = mref == kNegInf ? 0.f : -mref;
 #pragma unroll
-      for (int v = 1; v < 16; ++v) lmax = fmaxf(lmax, x[v]);
-      if (__any(lmax > thr)) {
+        for (int v = 0; v < 16; ++v) pr[v] = exp2_fast(__builtin_fmaf(x[v], sl2, nbase));
+        ps = pr[0];
+#pragma unroll
+        for (int v = 1; v < 16; ++v) ps += pr[v];
+      }
+      if (__any(!(ps <= kSumBound) || mref == kNegInf)) {
+        float lmax = x[0];
+#pragma unroll
+        for (int v = 1; v < 16; ++v) lmax = fmaxf(lmax, x[v]);
         const float tmax = xor32_max(lmax) * sl2;  // the row's maximum over the block
         const bool raise = tmax > mref + kRescaleSlack;
-        const float alpha = raise ? exp2_fast(mref - tmax) : 1.f;
-        lsum *= alpha;
+        if (__any(raise)) {
+          const float alpha = raise ? exp2_fast(mref - tmax) : 1.f;
+          lsum *= alpha;
 #pragma unroll
-        for (int t = 0; t < DB; ++t) acc[t] *= alpha;
-        mref = raise ? tmax : mref;
-        thr = (mref + kRescaleSlack) / sl2;
+          for (int t = 0; t < DB; ++t) acc[t] *= alpha;
+          mref = raise ? tmax : mref;
+          const float nbase = mref == kNegInf ? 0.f : -mref;
+#pragma unroll
+          for (int v = 0; v < 16; ++v) pr[v] = exp2_fast(__builtin_fmaf(x[v], sl2, nbase));
+          ps = pr[0];
+#pragma unroll
+          for (int v = 1; v < 16; ++v) ps += pr[v];
+        }
       }
-      const float nbase = mref == kNegInf ? 0.f : -mref;
-      float pr[16];
-#pragma unroll
-      for (int v = 0; v < 16; ++v) pr[v] = exp2_fast(__builtin_fmaf(x[v], sl2, nbase));
-      float ps = pr[0];
-#pragma unroll
-      for (int v = 1; v < 16; ++v) ps += pr[v];
       lsum += ps;
       u32x4 pb[2];
 #pragma unroll
@@ -1353,23 +1433,16 @@ __device__ __forceinline__ void ctx_wide_body(const PartialsParams& P) {
 #pragma unroll
         for (int w = 0; w < 4; ++w) pb[ss][w] = pack_bf16(pr[8 * ss + 2 * w], pr[8 * ss + 2 * w + 1]);
       // O^T += V^T P^T, dims 32t .. 32t+31, keys of k-step ss
+      lds_wait_tr(vw);
+      if (b + 1 < SK / 32) read_k_block(kaddr + 32 * (b + 1) * KROW, kw);
 #pragma unroll
-      for (int ss = 0; ss < 2; ++ss) {
+      for (int ss = 0; ss < 2; ++ss)
 #pragma unroll
         for (int t = 0; t < DB; ++t) {
-          u32x4 vop;
-#pragma unroll
-          for (int r = 0; r < 2; ++r) {
-            const v4i16 y = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-                (__attribute__((address_space(3))) v4i16*)(const_cast<unsigned char*>(
-                    vb + (32 * b + 16 * ss + 8 * r) * VROW + 64 * t)));
-            const u32x2 w2 = __builtin_bit_cast(u32x2, y);
-            vop[2 * r] = w2[0];
-            vop[2 * r + 1] = w2[1];
-          }
-          acc[t] = mfma32(vop, pb[ss], acc[t]);
+          const u32x2 lo = vw[8 * ss + 2 * t], hi = vw[8 * ss + 2 * t + 1];
+          acc[t] = mfma32(u32x4{lo[0], lo[1], hi[0], hi[1]}, pb[ss], acc[t]);
         }
-      }
+      if (b + 1 < SK / 32) lds_wait_k(kw);
     }
   }
 
