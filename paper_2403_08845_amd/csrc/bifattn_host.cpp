@@ -180,10 +180,12 @@ bifattn_status_t plan_splits(bifattn_plan_s* P, bool allow_fork = true) {
     // 256 rows per group, else of four, two per CU), which fills its CUs'
     // registers and LDS and so leaves no room for decode work beside it.
     // With the side stream, 256 or more rows per group still take the 32x32
-    // kernel, on a grid of three quarters of the CUs: the decode work-groups
+    // kernel, on a grid of five eighths of the CUs: the decode work-groups
     // run on the rest (measured on the ragged GQA workload: 265 vs 276 us per
-    // step with the 16x16 kernel beside the decode launch; grids of 160-192
-    // work-groups were best, 256 worse); fewer rows keep the 16x16 kernel.
+    // step with the 16x16 kernel beside the decode launch; 160 work-groups
+    // 234-236 vs 240-241 us for 192, 243 for 144, 258 for 208: the two parts
+    // take about as long either way, and fewer key splits leave the combine
+    // fewer partials); fewer rows keep the 16x16 kernel.
     // BIFATTN_FORK=0/1 and BIFATTN_CTX_WIDE=0/1 force either choice (d = 64
     // always takes the kernel of 16-row waves).
     const double dec_bytes = 2.0 * d.b * d.g * (double)d.m_d_max * kv_row_bytes(d.d, d.kv_type);
@@ -199,11 +201,10 @@ bifattn_status_t plan_splits(bifattn_plan_s* P, bool allow_fork = true) {
     P->ctx_row_blocks = (int)ceil_div(M, block_rows);
     // About one work-group per CU for eight-wave work-groups, two for
     // four-wave ones; with the side stream, one per CU for the 16x16 kernel
-    // (the decode work-groups take the other slot of each CU) and three
-    // quarters of the CUs for the 32x32 kernel (the decode work-groups take
-    // the remaining quarter).
+    // (the decode work-groups take the other slot of each CU) and five eighths
+    // of the CUs for the 32x32 kernel (the decode work-groups take the rest).
     const int per_cu = P->ctx_wide == 8 ? 1 : 2;
-    const int target = P->fork ? (P->ctx_wide ? kCUs * 3 / 4 : kCUs) : per_cu * kCUs;
+    const int target = P->fork ? (P->ctx_wide ? kCUs * 5 / 8 : kCUs) : per_cu * kCUs;
     int64_t splits = ceil_div(env_int("BIFATTN_CTX_WGS", target), (int64_t)d.g * P->ctx_row_blocks);
     if (splits < 1) splits = 1;
     const int64_t ck = round_up(ceil_div(d.m_c, splits), ck_step(key_step, d.m_c, splits));
