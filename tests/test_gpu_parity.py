@@ -8,7 +8,7 @@ import paper_2403_08845_amd as bif
 import workloads
 
 from .gpu_util import dims_of, run_decode, run_replicated, sample_rows, to_device, tokens_of
-from .parity import assert_parity
+from .parity import CONTRACT_MAX_ABS, assert_parity
 
 pytestmark = pytest.mark.gpu
 
@@ -395,6 +395,47 @@ def test_many_row_context_kernels(case, monkeypatch):
             out = run_decode(x, plan=plan)
         _report(f"many-row {case} wide={wide}", *assert_parity(out, ref, f"{case} wide={wide}", x=x))
 
+
+
+@pytest.mark.parametrize("pattern", ["growing", "needle"])
+@pytest.mark.parametrize("case", [(48, 32, 1, 128, 6000, 64), (64, 32, 8, 128, 3000, 100)],
+                         ids=lambda c: "b%d_h%d_g%d_d%d_mc%d_md%d" % c)
+def test_many_row_context_with_rising_logits(case, pattern, monkeypatch):
+    """Context keys whose logits keep rising past the running reference
+    maximum: key rows whose norm grows from 1x to 4x over every 128 keys (the
+    row maxima rise by more than 2^8 several times inside a key chunk), or
+    one key row scaled 8x in the middle of the context (a jump far above the
+    reference). Both many-row kernels take their rescale paths inside their
+    chunks and still match the oracle. The softmax is sharpened on purpose,
+    so single weights carry whole rows: the max-abs gate is the contract
+    bound and the values are halved (exactly), which keeps a dominant
+    weight's bf16 rounding (2^-9 of its value row) well inside it; the
+    relative-L2 gate is unchanged."""
+    b, h, g, d, m_c, m_d = case
+    x = workloads.make_inputs(b, h, g, d, m_c, m_d, seed=1700 + m_c, ragged=True)
+    kc = (x["Kc"].astype(np.uint32) << 16).view(np.float32)
+    t = np.arange(m_c, dtype=np.float32)
+    if pattern == "growing":
+        factor = (1.0 + 3.0 * (t % 128) / 127.0)[None, :, None]
+    else:
+        factor = np.ones((1, m_c, 1), np.float32)
+        # past the first 32-key block of its chunk for chunks of 96-192 keys
+        needle = next(t for t in range((3 * m_c) // 5, m_c)
+                      if all(t % c >= 32 for c in (96, 128, 160, 192)))
+        factor[0, needle] = 8.0
+    x["Kc"] = workloads.f32_to_bf16_bits(kc * factor)
+    for name in ("Vc", "Vd"):
+        x[name] = workloads.f32_to_bf16_bits((x[name].astype(np.uint32) << 16).view(np.float32) * 0.5)
+    ref = oracle.attention(**x)
+    monkeypatch.setenv("BIFATTN_FORK", "0")
+    for wide in ("1", "0"):
+        monkeypatch.setenv("BIFATTN_CTX_WIDE", wide)
+        with bif.Plan(b, h, g, d, m_c, m_d, path="bifurcated") as plan:
+            print(f"[case] rising logits {pattern} {case} wide={wide} {plan.info()}", flush=True)
+            out = run_decode(x, plan=plan)
+        _report(f"rising logits {pattern} {case} wide={wide}",
+                *assert_parity(out, ref, f"{pattern} {case} wide={wide}", x=x,
+                               gate_max_abs=CONTRACT_MAX_ABS))
 
 
 @pytest.mark.parametrize("kv", ["fp8_e4m3", "int8", "int4"])
