@@ -185,7 +185,11 @@ bifattn_status_t plan_splits(bifattn_plan_s* P, bool allow_fork = true) {
     // step with the 16x16 kernel beside the decode launch; 160 work-groups
     // 234-236 vs 240-241 us for 192, 243 for 144, 258 for 208: the two parts
     // take about as long either way, and fewer key splits leave the combine
-    // fewer partials); fewer rows keep the 16x16 kernel.
+    // fewer partials). 128 to 255 rows per group take its four-wave form on
+    // about one work-group per CU, the other slot of each CU left to decode
+    // work-groups (4 draft tokens: 89.8-89.9 vs 92.7-92.9 us for the 16x16
+    // kernel; 128-192 or 320 work-groups 92-94 us); fewer rows keep the 16x16
+    // kernel.
     // BIFATTN_FORK=0/1 and BIFATTN_CTX_WIDE=0/1 force either choice (d = 64
     // always takes the kernel of 16-row waves).
     const double dec_bytes = 2.0 * d.b * d.g * (double)d.m_d_max * kv_row_bytes(d.d, d.kv_type);
@@ -194,17 +198,18 @@ bifattn_status_t plan_splits(bifattn_plan_s* P, bool allow_fork = true) {
     const bool big_decode = dec_bytes >= 16.0 * (1 << 20) && dec_bytes / 5e12 > 0.5 * ctx_flops / 1e15;
     P->fork = allow_fork && d.m_d_max > 0 && (fork_env == -1 ? big_decode : fork_env == 1);
     const int wide_env = env_switch("BIFATTN_CTX_WIDE");
-    const bool wide = d.d == 128 && (wide_env == -1 ? (!P->fork || M >= 256) : wide_env == 1);
+    const bool wide = d.d == 128 && (wide_env == -1 ? (!P->fork || M >= 128) : wide_env == 1);
     P->ctx_wide = wide ? (M >= 256 ? 8 : 4) : 0;
     const int block_rows = wide ? 32 * P->ctx_wide : kLargeRowsPerBlock;
     const int key_step = wide ? 64 : kTileKeys;  // keys per stage of the kernel's loop
     P->ctx_row_blocks = (int)ceil_div(M, block_rows);
     // About one work-group per CU for eight-wave work-groups, two for
     // four-wave ones; with the side stream, one per CU for the 16x16 kernel
-    // (the decode work-groups take the other slot of each CU) and five eighths
-    // of the CUs for the 32x32 kernel (the decode work-groups take the rest).
+    // (the decode work-groups take the other slot of each CU) and for the
+    // four-wave 32x32 kernel, and five eighths of the CUs for the eight-wave
+    // 32x32 kernel (the decode work-groups take the rest).
     const int per_cu = P->ctx_wide == 8 ? 1 : 2;
-    const int target = P->fork ? (P->ctx_wide ? kCUs * 5 / 8 : kCUs) : per_cu * kCUs;
+    const int target = P->fork ? (P->ctx_wide == 8 ? kCUs * 5 / 8 : kCUs) : per_cu * kCUs;
     int64_t splits = ceil_div(env_int("BIFATTN_CTX_WGS", target), (int64_t)d.g * P->ctx_row_blocks);
     if (splits < 1) splits = 1;
     const int64_t ck = round_up(ceil_div(d.m_c, splits), ck_step(key_step, d.m_c, splits));

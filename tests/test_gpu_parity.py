@@ -299,8 +299,9 @@ def test_side_stream_decode(case, monkeypatch):
 
 def test_plan_rule_for_large_decode_parts(monkeypatch):
     """Without overrides, a many-row plan whose decode part is large takes the
-    side stream; with 256 or more rows per group it keeps the 32x32 context
-    kernel on five eighths of the CUs, with fewer rows the 16x16 kernel."""
+    side stream; with 256 or more rows per group it keeps the eight-wave 32x32
+    context kernel on five eighths of the CUs, with 128 to 255 rows its
+    four-wave form on about one work-group per CU."""
     for var in ("BIFATTN_FORK", "BIFATTN_CTX_WIDE", "BIFATTN_CTX_WGS"):
         monkeypatch.delenv(var, raising=False)
     with bif.Plan(256, 32, 8, 128, 32768, 1024) as plan:  # 1024 rows per group
@@ -309,7 +310,8 @@ def test_plan_rule_for_large_decode_parts(monkeypatch):
         assert info["ctx_blocks"] <= 160
     with bif.Plan(32, 32, 32, 128, 8192, 512, n=4) as plan:  # 128 rows per group
         info = plan.info()
-        assert info["side_stream"] == 1 and info["ctx_kernel"] == 1
+        assert info["side_stream"] == 1 and info["ctx_kernel"] == 2
+        assert info["ctx_blocks"] <= 256
 
 
 def test_largest_context_rows_are_addressed():
