@@ -464,39 +464,16 @@ __device__ __forceinline__ void tile_update(RowState<D, NT, MS>& st, KOp&& k_at,
 // Q^T operands of NT query tiles. row_ptr(r) gives the bf16 row of tile row r
 // (r = nt*16 + n) or nullptr when the row is padding; `sign` is XORed into
 // every pair of bf16 (0x80008000 negates q for a negative softmax scale).
-// With kEager, padding lanes load the valid row `any` and are zeroed
-// afterwards, so that all loads issue back to back (a load under a per-lane
-// condition waits for its data before the next one issues); without it
-// (kernels at the edge of their register budget) padding lanes skip the load.
-template <int D, int NT, bool kEager = true, typename RowPtr>
+template <int D, int NT, typename RowPtr>
 __device__ __forceinline__ void load_q(u32x4 (&qop)[NT][D / 32], RowPtr row_ptr, uint32_t sign,
-                                       int lane, const uint16_t* any) {
+                                       int lane) {
   const int n = lane & 15, G = lane >> 4;
-  if constexpr (!kEager) {
-#pragma unroll
-    for (int nt = 0; nt < NT; ++nt) {
-      const uint16_t* qr = row_ptr(nt * kRowsPerTile + n);
-#pragma unroll
-      for (int s = 0; s < D / 32; ++s)
-        qop[nt][s] = qr ? load16(qr + s * 32 + G * 8) ^ sign : u32x4{0, 0, 0, 0};
-    }
-    return;
-  }
-  bool valid[NT];
 #pragma unroll
   for (int nt = 0; nt < NT; ++nt) {
     const uint16_t* qr = row_ptr(nt * kRowsPerTile + n);
-    valid[nt] = qr != nullptr;
-    const uint16_t* src = valid[nt] ? qr : any;
-#pragma unroll
-    for (int s = 0; s < D / 32; ++s) qop[nt][s] = load16(src + s * 32 + G * 8);
-  }
-#pragma unroll
-  for (int nt = 0; nt < NT; ++nt) {
 #pragma unroll
     for (int s = 0; s < D / 32; ++s)
-#pragma unroll
-      for (int w = 0; w < 4; ++w) qop[nt][s][w] = valid[nt] ? qop[nt][s][w] ^ sign : 0u;
+      qop[nt][s] = qr ? load16(qr + s * 32 + G * 8) ^ sign : u32x4{0, 0, 0, 0};
   }
 }
 
@@ -690,12 +667,11 @@ __device__ __forceinline__ void stream_keys(RowState<D, NT>& st, const u32x4* qw
 // Stage this wave's Q^T operands of NT query tiles in its LDS slice qw.
 // row_ptr(r) gives the bf16 row of tile row r (r = nt*16 + n) or nullptr
 // for padding rows.
-template <int D, int NT, bool kEager = true, typename RowPtr>
-__device__ __forceinline__ void stage_q(u32x4* qw, RowPtr row_ptr, uint32_t sign, int lane,
-                                        const uint16_t* any) {
+template <int D, int NT, typename RowPtr>
+__device__ __forceinline__ void stage_q(u32x4* qw, RowPtr row_ptr, uint32_t sign, int lane) {
   constexpr int KS = D / 32;
   u32x4 qop[NT][KS];
-  load_q<D, NT, kEager>(qop, row_ptr, sign, lane, any);
+  load_q<D, NT>(qop, row_ptr, sign, lane);
 #pragma unroll
   for (int nt = 0; nt < NT; ++nt)
 #pragma unroll
@@ -748,7 +724,7 @@ __device__ void decode_block(const PartialsParams& P, int blk, int wave, int lan
   const uint16_t* qbase = P.q + ((size_t)i * P.h + (size_t)gam * P.p) * D;
   const int p = P.p;
   stage_q<D, NT>(qw, [&](int r) -> const uint16_t* { return r < p ? qbase + (size_t)r * D : nullptr; },
-                 P.q_sign, lane, P.q);
+                 P.q_sign, lane);
   RowState<D, NT> st;
   st.init();
   // Keys [k0, k1) of this chunk; the causal limits of the tokens count from
@@ -852,7 +828,7 @@ __device__ void ctx_small_block(const PartialsParams& P, int blk, int wave, int 
     if (r >= M) return nullptr;
     const int i = r / p, jp = r - i * p;
     return q + ((size_t)i * h + (size_t)gam * p + jp) * D;
-  }, P.q_sign, lane, P.q);
+  }, P.q_sign, lane);
   RowState<D, NT> st;
   st.init();
   stream_keys<D, NT, KV>(st, qw, kl, rk, rv, A, k0, P.m_c, P.m_c, P.S_c * kWaves * kTileKeys, 1,
@@ -890,8 +866,8 @@ __device__ void standard_block(const PartialsParams& P, int blk, int wave, int l
   A.template load<0>(rkc, rvc, k0, lane);  // first context tile in flight during the set-up
   const int p = P.p;
   const uint16_t* qbase = P.q + ((size_t)i * P.h + (size_t)gam * p) * D;
-  stage_q<D, NT, false>(qw, [&](int r) -> const uint16_t* { return r < p ? qbase + (size_t)r * D : nullptr; },
-                        P.q_sign, lane, P.q);
+  stage_q<D, NT>(qw, [&](int r) -> const uint16_t* { return r < p ? qbase + (size_t)r * D : nullptr; },
+                 P.q_sign, lane);
   const float sl2 = unit_scale_log2(P, gam);
   RowState<D, NT> st;
   st.init();
@@ -1025,7 +1001,7 @@ __device__ __forceinline__ void ctx_large_body(const PartialsParams& P) {
     if (row >= M) return nullptr;
     const int i = row / p, jp = row - i * p;
     return P.q + ((size_t)i * h + (size_t)gam * p + jp) * D;
-  }, P.q_sign, lane, P.q);
+  }, P.q_sign, lane);
   constexpr int T = kTileKeys;
   Stage S0, S1, S2;
   fetch(S0, 0);
